@@ -1,0 +1,44 @@
+"""Plain float64 CPU oracle for batched speculative verification.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call, link
+or execute this package: it is used by ``tests/``, by the smoke check of the
+build entry point and by the CPU-baseline leg of the benchmark.  It shares no
+code with the HIP library (no kernels, headers, helpers, tables or constant
+generators) and imports nothing from it.
+
+What it computes (StarSD, "One-for-Many Speculative Decoding"):
+
+* :mod:`oracle.attention` -- causal multi-query attention of the gamma + 1
+  verification queries of each request over that request's KV cache: the
+  target forward along the path's prefixes, which Algorithm 2 (EAGLE
+  speculative decoding, verification loop) says may run in parallel, and the
+  batched tree/path scoring of Sec. 2 ("Tree-based proposals").
+  Reached exactly by its textbook definition.
+* :mod:`oracle.logits` -- vocabulary projection and row log-sum-exp giving the
+  target distributions p_1..p_{gamma+1} of Algorithm 2.  Textbook definition.
+* :mod:`oracle.accept` -- the stochastic acceptance test, first rejection,
+  residual correction norm(max(0, p_{l+1} - q_{l+1})) and the final sample of
+  Algorithm 2, with the ratio rule of the Leviathan et al. formulation the
+  paper adopts in Sec. 2 and whose acceptance probability is Eq. (1) of
+  Sec. 3.2.  Followed step by step.
+* :mod:`oracle.step` -- the composition of the three for one pooled batch.
+
+Every function is pinned by ``tests/test_oracle_*.py`` against closed forms,
+special cases, library routines of other packages and brute-force enumeration;
+see those files for which pin covers which function.
+"""
+
+from .attention import verify_attention
+from .logits import verify_logits, probabilities
+from .accept import accept_request, accept_resample, near_threshold
+from .step import verify_step
+
+__all__ = [
+    "verify_attention",
+    "verify_logits",
+    "probabilities",
+    "accept_request",
+    "accept_resample",
+    "near_threshold",
+    "verify_step",
+]
