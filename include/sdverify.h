@@ -1,0 +1,177 @@
+/*
+ * sdverify.h -- batched, lossless speculative verification on one MI355X (gfx950).
+ *
+ * The verification step of StarSD's one-for-many speculative decoding: one
+ * verifier scores a pooled batch of B requests, each carrying gamma draft
+ * tokens x_1..x_gamma, the draft distributions q_1..q_gamma they were drawn
+ * from, its own KV cache and uniform draws, and returns for every request the
+ * accepted prefix plus one corrected (or bonus) token.
+ *   - Algorithm 2 (EAGLE speculative decoding), verification of a path: the
+ *     target model runs along the gamma + 1 prefixes in parallel, giving
+ *     p_1..p_{gamma+1}; a stochastic test gives the accept length l; a
+ *     correction is sampled from norm(max(0, p_{l+1} - q_{l+1})).
+ *   - Sec. 2 (Preliminary): the per-request primitive and the Leviathan et al.
+ *     formulation whose ratio test u < p_i(x_i)/q_i(x_i) is used here.
+ *   - Sec. 3.2, Eq. (1): the acceptance probability sum_x min(p, q) that test has.
+ *   - Algorithm 1 and its design properties: requests from many targets are
+ *     pooled, each isolated to its own state; here each request owns its own
+ *     KV segment and all share one vocabulary projection.
+ *
+ * Conventions shared by every call
+ *   - G = gamma + 1 query positions per request: position 0 is the root (last
+ *     verified token), position i >= 1 is draft x_i.  M = B * G.
+ *   - All pointers are DEVICE pointers unless marked (host).  Device buffers
+ *     are read or written only by work enqueued on `stream`; they must stay
+ *     alive until that work completes.  The library allocates no device memory,
+ *     keeps no pointer after returning, enqueues work only (never synchronises)
+ *     and is re-entrant.  Scratch space comes from the caller's `workspace`;
+ *     its size is given by sd_workspace_bytes.
+ *   - Device pointers to Q/K/V/hidden/W/workspace must be 16-byte aligned;
+ *     float/int32 arrays 4-byte aligned.
+ *   - Return value: SD_OK or a negative status (see sd_status_string).  All
+ *     argument checks run on the host before anything is enqueued; on an
+ *     error nothing is enqueued.  The library never aborts or exits.
+ *   - Device-array preconditions that are not checked (documented only):
+ *     draft tokens lie in [0, vocab) (a token outside it is treated as
+ *     rejected, never read out of bounds); q rows are distributions.
+ *   - Results are deterministic: no floating-point atomics, fixed reduction order.
+ */
+#ifndef SDVERIFY_H
+#define SDVERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define SD_API __attribute__((visibility("default")))
+#else
+#define SD_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A hipStream_t passed as an opaque pointer (NULL = the null stream). */
+typedef void* sd_stream_t;
+
+typedef enum {
+  SD_DTYPE_F32 = 0,  /* float32 Q/K/V/hidden/W; attention output float32 */
+  SD_DTYPE_BF16 = 1  /* bfloat16 Q/K/V/hidden/W; attention output bfloat16 */
+} sd_dtype_t;
+
+enum {
+  SD_OK = 0,
+  SD_ERR_INVALID_ARGUMENT = -1, /* null/misaligned pointer, bad size, inconsistent shape */
+  SD_ERR_UNSUPPORTED = -2,      /* valid but outside what the kernels implement */
+  SD_ERR_WORKSPACE = -3,        /* workspace smaller than sd_workspace_bytes requires */
+  SD_ERR_HIP = -4               /* a HIP launch or runtime call failed */
+};
+
+/* Problem shape.  Accumulation is always float32 (float64 for the sampling sums). */
+typedef struct {
+  int32_t batch;      /* B >= 1 pooled requests (one per target session) */
+  int32_t gamma;      /* draft tokens per request, >= 1 (the paper's depth d, branching 1) */
+  int32_t n_q_heads;  /* query heads, a multiple of n_kv_heads */
+  int32_t n_kv_heads; /* KV heads; query head h reads KV head h / (n_q_heads / n_kv_heads) */
+  int32_t head_dim;   /* 64 or 128 */
+  int32_t hidden;     /* width of the vocabulary projection's input, a multiple of 32 */
+  int32_t vocab;      /* V, 1 .. 2,097,152 */
+  int32_t dtype;      /* sd_dtype_t */
+} sd_dims_t;
+
+/*
+ * Workspace bytes needed by any call below for `dims` with every kv_len <=
+ * max_kv_len.  Returns 0 for an invalid shape.
+ */
+SD_API size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len);
+
+/*
+ * Causal multi-query verification attention (Algorithm 2: the target model
+ * along the gamma + 1 prefixes of a path, evaluated in parallel).
+ *   q        [B][G][Hq][D]          query vectors, already position-encoded
+ *   k_pool   request b: [Hkv][kv_len[b]][D] starting at element kv_off[b]
+ *   v_pool   same layout as k_pool
+ *   kv_off   (host) [B] element offsets; kv_off[b] * sizeof(dtype) % 16 == 0
+ *   kv_len   (host) [B] cached length L_b INCLUDING this step's G positions,
+ *            G <= L_b <= 2^30; query j attends to keys 0 .. L_b - G + j
+ *   scale    softmax scale (1/sqrt(head_dim) for the usual definition)
+ *   out      [B][G][Hq][D] in dtype: softmax(q k^T * scale) v per (request, head, query)
+ * Requires G * (n_q_heads / n_kv_heads) <= 128 (SD_ERR_UNSUPPORTED otherwise).
+ */
+SD_API int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool,
+                        const void* v_pool, const int64_t* kv_off, const int32_t* kv_len,
+                        float scale, void* out, void* workspace, size_t workspace_bytes,
+                        sd_stream_t stream);
+
+/*
+ * Vocabulary projection and row log-sum-exp: the target distributions
+ * p_1..p_{gamma+1} of Algorithm 2 (temperature 1).
+ *   hidden   [M][hidden] in dtype; row b*G + j feeds p_{j+1} of request b
+ *   w_vocab  [V][hidden] in dtype (one row per vocabulary entry)
+ *   logits   [M][V] float32 output: logits[m][v] = sum_k hidden[m][k] * w_vocab[v][k]
+ *   row_lse  [M] float32 output: log sum_v exp(logits[m][v])
+ * so that p_{j+1}(v) = exp(logits[b*G+j][v] - row_lse[b*G+j]).
+ */
+SD_API int sd_verify_logits(const sd_dims_t* dims, const void* hidden, const void* w_vocab,
+                     float* logits, float* row_lse, void* workspace, size_t workspace_bytes,
+                     sd_stream_t stream);
+
+/*
+ * Acceptance test, first rejection, residual resampling and output assembly
+ * (Algorithm 2, stochastic test and correction; Leviathan ratio rule).
+ *   logits_or_probs [M][V] float32: logits if row_lse != NULL, else probabilities
+ *   row_lse         [M] float32 or NULL
+ *   q_draft         [B][gamma][V] float32: q_draft[b][i] is the distribution x_{i+1} was drawn from
+ *   draft_tok       [B][gamma] int32: x_1..x_gamma
+ *   u               [B][G] float32 in [0,1): u[b][i] tests x_{i+1}; u[b][gamma] drives the final sample
+ *   kv_len          (host) [B] as for sd_verify_attention; required iff new_kv_len != NULL
+ *   accept_len      [B] int32 output: l_b in [0, gamma]
+ *   out_tok         [B][G] int32 output: x_1..x_l, then the sampled token, then -1 padding
+ *   new_kv_len      [B] int32 output or NULL: kv_len[b] - gamma + l_b (cache entries to keep)
+ * Rules (per request, p_i = row b*G + i - 1):
+ *   ratio_i = p_i(x_i) / q_i(x_i), with ratio = 0 if p_i(x_i) = 0 and +inf if
+ *   q_i(x_i) = 0 < p_i(x_i); x_i passes iff u[b][i-1] < ratio_i; l = number of
+ *   leading passes.  The final token is drawn from r = max(0, p_{l+1} - q_{l+1})
+ *   if l < gamma, else r = p_{gamma+1} (the bonus), by inverse CDF in ascending
+ *   token id: t = min{k : C_k > u[b][gamma] * Z}, C the float64 inclusive prefix
+ *   sums of r and Z = C_{V-1}; if no k qualifies, t is the largest k with
+ *   r(k) > 0; if Z is not positive, r falls back to p_{l+1}.  p(v) is evaluated
+ *   from logits as exp(logit - lse) with the difference kept exact; the ratio test
+ *   runs in float64.
+ */
+SD_API int sd_accept_resample(const sd_dims_t* dims, const float* logits_or_probs, const float* row_lse,
+                       const float* q_draft, const int32_t* draft_tok, const float* u,
+                       const int32_t* kv_len, int32_t* accept_len, int32_t* out_tok,
+                       int32_t* new_kv_len, void* workspace, size_t workspace_bytes,
+                       sd_stream_t stream);
+
+/*
+ * One whole verification step: sd_verify_attention, then sd_verify_logits on
+ * `hidden` (or, when hidden == NULL, on the attention output viewed as
+ * [M][n_q_heads * head_dim], which then must equal dims->hidden), then
+ * sd_accept_resample on the logits and row_lse it produced.  Arguments as in
+ * the three calls; attn_out, logits, row_lse are outputs the caller owns.
+ *   stage_events  (host) NULL, or 4 hipEvent_t handles recorded on `stream`
+ *                 before attention, after attention, after the vocabulary
+ *                 projection (including row_lse) and after acceptance.
+ */
+SD_API int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
+                   const int64_t* kv_off, const int32_t* kv_len, float scale,
+                   const void* hidden, const void* w_vocab, const float* q_draft,
+                   const int32_t* draft_tok, const float* u, void* attn_out, float* logits,
+                   float* row_lse, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
+                   void* workspace, size_t workspace_bytes, sd_stream_t stream,
+                   void* const* stage_events);
+
+/* Static description of a status code. */
+SD_API const char* sd_status_string(int status);
+
+/* Library version, "major.minor.patch". */
+SD_API const char* sd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SDVERIFY_H */

@@ -1,0 +1,31 @@
+"""Batched, lossless speculative verification on one MI355X (gfx950).
+
+Thin ctypes binding of ``libsdverify.so`` (the C-ABI declared in
+``include/sdverify.h``).  Each function has the C name, marshals torch device
+tensors, host integer arrays and the current HIP stream into the C call, and
+raises :class:`SdError` on a non-zero status.  No step of the computation runs
+in Python: every result comes from the HIP kernels, and the binding fails
+loudly when the library has not been built.
+"""
+
+from ._binding import (  # noqa: F401
+    SD_DTYPE_BF16,
+    SD_DTYPE_F32,
+    SD_ERR_HIP,
+    SD_ERR_INVALID_ARGUMENT,
+    SD_ERR_UNSUPPORTED,
+    SD_ERR_WORKSPACE,
+    SD_OK,
+    Dims,
+    SdError,
+    exported_symbols,
+    library,
+    library_path,
+    sd_accept_resample,
+    sd_status_string,
+    sd_verify_attention,
+    sd_verify_logits,
+    sd_verify_step,
+    sd_version,
+    sd_workspace_bytes,
+)

@@ -1,0 +1,198 @@
+"""ctypes marshalling for libsdverify.so.  Argument conversion only."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional, Sequence
+
+import numpy as np
+import torch  # loaded first so the library binds to the HIP runtime torch already uses
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_NAME = "libsdverify.so"
+_HEADER = os.path.join(os.path.dirname(_HERE), "include", "sdverify.h")
+
+SD_DTYPE_F32 = 0
+SD_DTYPE_BF16 = 1
+SD_OK = 0
+SD_ERR_INVALID_ARGUMENT = -1
+SD_ERR_UNSUPPORTED = -2
+SD_ERR_WORKSPACE = -3
+SD_ERR_HIP = -4
+
+
+class SdError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {sd_status_string(status)} (status {status})")
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("gamma", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("hidden", ctypes.c_int32),
+        ("vocab", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+    ]
+
+    @classmethod
+    def of(cls, cfg) -> "Dims":
+        """Dims of a workload description (anything with the same attribute names)."""
+        return cls(cfg.batch, cfg.gamma, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.hidden,
+                   cfg.vocab, SD_DTYPE_BF16 if cfg.dtype == "bf16" else SD_DTYPE_F32)
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def library_path() -> str:
+    return os.environ.get("SDVERIFY_LIB", os.path.join(_HERE, _LIB_NAME))
+
+
+def library() -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2601_21622_amd.build` "
+                           "(there is no fallback implementation)")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, SZ, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+    DP = ctypes.POINTER(Dims)
+    lib.sd_workspace_bytes.argtypes = [DP, I32]
+    lib.sd_workspace_bytes.restype = SZ
+    lib.sd_verify_attention.argtypes = [DP, P, P, P, P, P, F, P, P, SZ, P]
+    lib.sd_verify_attention.restype = ctypes.c_int
+    lib.sd_verify_logits.argtypes = [DP, P, P, P, P, P, SZ, P]
+    lib.sd_verify_logits.restype = ctypes.c_int
+    lib.sd_accept_resample.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.sd_accept_resample.restype = ctypes.c_int
+    lib.sd_verify_step.argtypes = [DP, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
+    lib.sd_verify_step.restype = ctypes.c_int
+    lib.sd_status_string.argtypes = [ctypes.c_int]
+    lib.sd_status_string.restype = ctypes.c_char_p
+    lib.sd_version.argtypes = []
+    lib.sd_version.restype = ctypes.c_char_p
+    _ = (I64,)
+    _lib = lib
+    return lib
+
+
+def exported_symbols() -> list:
+    """Names of the functions include/sdverify.h declares."""
+    with open(_HEADER) as f:
+        text = f.read()
+    return re.findall(r"SD_API\s+[\w\s\*]*?\b(sd_\w+)\s*\(", text)
+
+
+def sd_status_string(status: int) -> str:
+    return library().sd_status_string(int(status)).decode()
+
+
+def sd_version() -> str:
+    return library().sd_version().decode()
+
+
+# ---- marshalling helpers ------------------------------------------------------
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"expected a torch device tensor, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError("device arguments must be GPU tensors")
+    if not t.is_contiguous():
+        raise ValueError("device arguments must be contiguous")
+    return t.data_ptr()
+
+
+def _host(a, dtype):
+    if a is None:
+        return None, None
+    arr = np.ascontiguousarray(np.asarray(a, dtype=dtype))
+    return arr, arr.ctypes.data_as(ctypes.c_void_p)
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def _check(status: int, where: str) -> None:
+    if status != SD_OK:
+        raise SdError(status, where)
+
+
+# ---- the C calls ----------------------------------------------------------------
+
+def sd_workspace_bytes(dims: Dims, max_kv_len: int) -> int:
+    return int(library().sd_workspace_bytes(ctypes.byref(dims), int(max_kv_len)))
+
+
+def sd_verify_attention(dims: Dims, q, k_pool, v_pool, kv_off: Sequence[int], kv_len: Sequence[int],
+                        scale: float, out, workspace, stream=None) -> None:
+    _off, off_p = _host(kv_off, np.int64)
+    _len, len_p = _host(kv_len, np.int32)
+    st = library().sd_verify_attention(ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p,
+                                       float(scale), _ptr(out), _ptr(workspace), _nbytes(workspace),
+                                       _stream(stream))
+    _check(st, "sd_verify_attention")
+
+
+def sd_verify_logits(dims: Dims, hidden, w_vocab, logits, row_lse, workspace, stream=None) -> None:
+    st = library().sd_verify_logits(ctypes.byref(dims), _ptr(hidden), _ptr(w_vocab), _ptr(logits),
+                                    _ptr(row_lse), _ptr(workspace), _nbytes(workspace), _stream(stream))
+    _check(st, "sd_verify_logits")
+
+
+def sd_accept_resample(dims: Dims, logits_or_probs, row_lse, q_draft, draft_tok, u, kv_len, accept_len,
+                       out_tok, new_kv_len, workspace=None, stream=None) -> None:
+    _len, len_p = _host(kv_len, np.int32)
+    ws_bytes = 0 if workspace is None else _nbytes(workspace)
+    st = library().sd_accept_resample(ctypes.byref(dims), _ptr(logits_or_probs), _ptr(row_lse), _ptr(q_draft),
+                                      _ptr(draft_tok), _ptr(u), len_p, _ptr(accept_len), _ptr(out_tok),
+                                      _ptr(new_kv_len), _ptr(workspace), ws_bytes, _stream(stream))
+    _check(st, "sd_accept_resample")
+
+
+def sd_verify_step(dims: Dims, q, k_pool, v_pool, kv_off, kv_len, scale: float, hidden, w_vocab, q_draft,
+                   draft_tok, u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace,
+                   stream=None, stage_events=None) -> None:
+    _off, off_p = _host(kv_off, np.int64)
+    _len, len_p = _host(kv_len, np.int32)
+    ev = None
+    if stage_events is not None:
+        handles = []
+        for e in stage_events:
+            if not isinstance(e, int):
+                if e.cuda_event == 0:  # torch creates its event lazily, on first record
+                    e.record()
+                e = e.cuda_event
+            handles.append(e)
+        if len(handles) != 4:
+            raise ValueError("stage_events needs exactly 4 events")
+        ev = (ctypes.c_void_p * 4)(*handles)
+    st = library().sd_verify_step(ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p,
+                                  float(scale), _ptr(hidden), _ptr(w_vocab), _ptr(q_draft), _ptr(draft_tok),
+                                  _ptr(u), _ptr(attn_out), _ptr(logits), _ptr(row_lse), _ptr(accept_len),
+                                  _ptr(out_tok), _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace),
+                                  _stream(stream), ev)
+    _check(st, "sd_verify_step")

@@ -1,0 +1,273 @@
+// C-ABI of the verification library: argument checks, workspace layout and
+// the launch sequence of each entry point.  Every check runs on the host
+// before anything is enqueued.
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "../../include/sdverify.h"
+#include "launch.h"
+
+namespace {
+
+using namespace sdv;
+
+constexpr int kMaxRows = 128;       // G * (Hq / Hkv) handled by one attention workgroup
+constexpr int kMaxRowsF32 = 64;
+constexpr int kMaxVocab = 2097152;
+constexpr int kMaxGamma = 63;
+constexpr int64_t kMaxKvLen = int64_t(1) << 30;
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t elem_size(int dtype) { return dtype == SD_DTYPE_BF16 ? 2 : 4; }
+
+size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+int check_dims(const sd_dims_t* d) {
+  if (d == nullptr) return SD_ERR_INVALID_ARGUMENT;
+  if (d->batch < 1 || d->gamma < 1 || d->n_q_heads < 1 || d->n_kv_heads < 1 || d->hidden < 1 ||
+      d->vocab < 1 || d->head_dim < 1)
+    return SD_ERR_INVALID_ARGUMENT;
+  if (d->dtype != SD_DTYPE_F32 && d->dtype != SD_DTYPE_BF16) return SD_ERR_INVALID_ARGUMENT;
+  if (d->n_q_heads % d->n_kv_heads != 0) return SD_ERR_INVALID_ARGUMENT;
+  if (d->head_dim != 64 && d->head_dim != 128) return SD_ERR_UNSUPPORTED;
+  if (d->hidden % 32 != 0) return SD_ERR_UNSUPPORTED;
+  if (d->vocab > kMaxVocab) return SD_ERR_UNSUPPORTED;
+  if (d->gamma > kMaxGamma) return SD_ERR_UNSUPPORTED;
+  const int64_t rows = int64_t(d->gamma + 1) * (d->n_q_heads / d->n_kv_heads);
+  if (rows > (d->dtype == SD_DTYPE_F32 ? kMaxRowsF32 : kMaxRows)) return SD_ERR_UNSUPPORTED;
+  if (int64_t(d->batch) * (d->gamma + 1) > (int64_t(1) << 24)) return SD_ERR_UNSUPPORTED;
+  return SD_OK;
+}
+
+AttnShape attn_shape(const sd_dims_t* d, float scale) {
+  AttnShape s;
+  s.G = d->gamma + 1;
+  s.Hq = d->n_q_heads;
+  s.Hkv = d->n_kv_heads;
+  s.D = d->head_dim;
+  s.group = d->n_q_heads / d->n_kv_heads;
+  s.rows = s.G * s.group;
+  s.chunk_keys = attn_chunk_keys(d->dtype, s.rows, s.D);
+  s.scale_log2 = scale * 1.4426950408889634f;
+  return s;
+}
+
+int64_t total_chunks(const int32_t* kv_len, int B, int chunk) {
+  int64_t n = 0;
+  for (int b = 0; b < B; ++b) n += (kv_len[b] + chunk - 1) / chunk;
+  return n;
+}
+
+size_t attention_ws(const sd_dims_t* d, int64_t chunks) {
+  const AttnShape s = attn_shape(d, 1.f);
+  return align_up(attn_partial_bytes(chunks, s.Hkv, s.rows, s.D));
+}
+
+size_t logits_ws(const sd_dims_t* d) {
+  const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab);
+  return align_up(vocab_partial_bytes(p));
+}
+
+int check_kv(const sd_dims_t* d, const int64_t* kv_off, const int32_t* kv_len) {
+  if (kv_off == nullptr || kv_len == nullptr) return SD_ERR_INVALID_ARGUMENT;
+  const int G = d->gamma + 1;
+  const size_t es = elem_size(d->dtype);
+  for (int b = 0; b < d->batch; ++b) {
+    if (kv_len[b] < G || kv_len[b] > kMaxKvLen) return SD_ERR_INVALID_ARGUMENT;
+    if (kv_off[b] < 0 || (uint64_t(kv_off[b]) * es) % 16 != 0) return SD_ERR_INVALID_ARGUMENT;
+  }
+  return SD_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
+
+// Enqueue attention (partials + combine) for all requests, in launches of at
+// most kMaxReqPerLaunch requests whose tables ride in the kernel arguments.
+int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* v, const int64_t* kv_off,
+                  const int32_t* kv_len, float scale, void* out, void* ws, hipStream_t stream) {
+  const AttnShape s = attn_shape(d, scale);
+  const int64_t chunks = total_chunks(kv_len, d->batch, s.chunk_keys);
+  const AttnPartials parts = attn_carve(ws, chunks, s.Hkv, s.rows, s.D);
+  int64_t chunk_base = 0;
+  for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
+    AttnBatch bt;
+    memset(&bt, 0, sizeof(bt));
+    bt.nreq = std::min(kMaxReqPerLaunch, d->batch - r0);
+    bt.req0 = r0;
+    bt.chunk_base = static_cast<int32_t>(chunk_base);
+    int32_t acc = 0;
+    for (int i = 0; i < bt.nreq; ++i) {
+      bt.chunk_prefix[i] = acc;
+      bt.kv_len[i] = kv_len[r0 + i];
+      bt.kv_off[i] = kv_off[r0 + i];
+      acc += (kv_len[r0 + i] + s.chunk_keys - 1) / s.chunk_keys;
+    }
+    bt.chunk_prefix[bt.nreq] = acc;
+    hipError_t e = launch_attention(d->dtype, s, bt, acc, q, k, v, parts, stream);
+    if (e == hipSuccess) e = launch_attention_combine(d->dtype, s, bt, parts, out, stream);
+    if (e != hipSuccess) return SD_ERR_HIP;
+    chunk_base += acc;
+  }
+  return SD_OK;
+}
+
+int run_logits(const sd_dims_t* d, const void* hidden, const void* w, float* logits, float* row_lse, void* ws,
+               hipStream_t stream) {
+  const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab);
+  float2* partials = static_cast<float2*>(ws);
+  hipError_t e = launch_vocab(d->dtype, p, hidden, w, logits, partials, stream);
+  if (e == hipSuccess) e = launch_lse_combine(p, partials, row_lse, stream);
+  return hip_status(e);
+}
+
+int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const float* q_draft,
+               const int32_t* draft_tok, const float* u, const int32_t* kv_len, int32_t* accept_len,
+               int32_t* out_tok, int32_t* new_kv_len, hipStream_t stream) {
+  for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
+    AcceptBatch bt;
+    memset(&bt, 0, sizeof(bt));
+    bt.nreq = std::min(kMaxReqPerLaunch, d->batch - r0);
+    bt.req0 = r0;
+    bt.has_kv_len = kv_len != nullptr;
+    if (kv_len != nullptr)
+      for (int i = 0; i < bt.nreq; ++i) bt.kv_len[i] = kv_len[r0 + i];
+    hipError_t e = launch_accept(d->gamma, d->vocab, bt, x, row_lse, q_draft, draft_tok, u, accept_len,
+                                 out_tok, new_kv_len, stream);
+    if (e != hipSuccess) return SD_ERR_HIP;
+  }
+  return SD_OK;
+}
+
+int check_accept_args(const float* x, const float* row_lse, const float* q_draft, const int32_t* draft_tok,
+                      const float* u, const int32_t* kv_len, const int32_t* accept_len, const int32_t* out_tok,
+                      const int32_t* new_kv_len) {
+  if (!x || !q_draft || !draft_tok || !u || !accept_len || !out_tok) return SD_ERR_INVALID_ARGUMENT;
+  if (new_kv_len != nullptr && kv_len == nullptr) return SD_ERR_INVALID_ARGUMENT;
+  const void* p4[] = {x, row_lse, q_draft, draft_tok, u, accept_len, out_tok, new_kv_len};
+  for (const void* p : p4)
+    if (p != nullptr && !aligned(p, 4)) return SD_ERR_INVALID_ARGUMENT;
+  return SD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
+  if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
+  const AttnShape s = attn_shape(dims, 1.f);
+  const int64_t chunks = int64_t(dims->batch) * ((int64_t(max_kv_len) + s.chunk_keys - 1) / s.chunk_keys);
+  return std::max(attention_ws(dims, chunks), logits_ws(dims));
+}
+
+int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
+                        const int64_t* kv_off, const int32_t* kv_len, float scale, void* out, void* workspace,
+                        size_t workspace_bytes, sd_stream_t stream) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!q || !k_pool || !v_pool || !out || !workspace) return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(out, 16) ||
+      !aligned(workspace, 16))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (!(scale == scale)) return SD_ERR_INVALID_ARGUMENT;
+  st = check_kv(dims, kv_off, kv_len);
+  if (st != SD_OK) return st;
+  const AttnShape s = attn_shape(dims, scale);
+  if (workspace_bytes < attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)))
+    return SD_ERR_WORKSPACE;
+  return run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, out, workspace,
+                       static_cast<hipStream_t>(stream));
+}
+
+int sd_verify_logits(const sd_dims_t* dims, const void* hidden, const void* w_vocab, float* logits,
+                     float* row_lse, void* workspace, size_t workspace_bytes, sd_stream_t stream) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!hidden || !w_vocab || !logits || !row_lse || !workspace) return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(hidden, 16) || !aligned(w_vocab, 16) || !aligned(logits, 16) || !aligned(row_lse, 4) ||
+      !aligned(workspace, 16))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < logits_ws(dims)) return SD_ERR_WORKSPACE;
+  return run_logits(dims, hidden, w_vocab, logits, row_lse, workspace, static_cast<hipStream_t>(stream));
+}
+
+int sd_accept_resample(const sd_dims_t* dims, const float* logits_or_probs, const float* row_lse,
+                       const float* q_draft, const int32_t* draft_tok, const float* u, const int32_t* kv_len,
+                       int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len, void* workspace,
+                       size_t workspace_bytes, sd_stream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  st = check_accept_args(logits_or_probs, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
+                         new_kv_len);
+  if (st != SD_OK) return st;
+  if (kv_len != nullptr)
+    for (int b = 0; b < dims->batch; ++b)
+      if (kv_len[b] < dims->gamma + 1 || kv_len[b] > kMaxKvLen) return SD_ERR_INVALID_ARGUMENT;
+  return run_accept(dims, logits_or_probs, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
+                    new_kv_len, static_cast<hipStream_t>(stream));
+}
+
+int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
+                   const int64_t* kv_off, const int32_t* kv_len, float scale, const void* hidden,
+                   const void* w_vocab, const float* q_draft, const int32_t* draft_tok, const float* u,
+                   void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
+                   int32_t* new_kv_len, void* workspace, size_t workspace_bytes, sd_stream_t stream,
+                   void* const* stage_events) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!q || !k_pool || !v_pool || !attn_out || !w_vocab || !logits || !row_lse || !workspace)
+    return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(attn_out, 16) ||
+      !aligned(w_vocab, 16) || !aligned(logits, 16) || !aligned(row_lse, 4) || !aligned(workspace, 16) ||
+      (hidden != nullptr && !aligned(hidden, 16)))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (hidden == nullptr && dims->hidden != dims->n_q_heads * dims->head_dim) return SD_ERR_INVALID_ARGUMENT;
+  if (!(scale == scale)) return SD_ERR_INVALID_ARGUMENT;
+  st = check_accept_args(logits, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok, new_kv_len);
+  if (st != SD_OK) return st;
+  st = check_kv(dims, kv_off, kv_len);
+  if (st != SD_OK) return st;
+  const AttnShape s = attn_shape(dims, scale);
+  const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
+                               logits_ws(dims));
+  if (workspace_bytes < need) return SD_ERR_WORKSPACE;
+
+  hipStream_t stm = static_cast<hipStream_t>(stream);
+  auto record = [&](int i) -> bool {
+    if (stage_events == nullptr) return true;
+    return hipEventRecord(static_cast<hipEvent_t>(stage_events[i]), stm) == hipSuccess;
+  };
+  if (!record(0)) return SD_ERR_HIP;
+  st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out, workspace, stm);
+  if (st != SD_OK) return st;
+  if (!record(1)) return SD_ERR_HIP;
+  // The attention partials are dead once the combine has run; the vocabulary
+  // statistics reuse the same workspace (stream order serialises them).
+  st = run_logits(dims, hidden != nullptr ? hidden : attn_out, w_vocab, logits, row_lse, workspace, stm);
+  if (st != SD_OK) return st;
+  if (!record(2)) return SD_ERR_HIP;
+  st = run_accept(dims, logits, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok, new_kv_len, stm);
+  if (st != SD_OK) return st;
+  if (!record(3)) return SD_ERR_HIP;
+  return SD_OK;
+}
+
+const char* sd_status_string(int status) {
+  switch (status) {
+    case SD_OK: return "SD_OK: success";
+    case SD_ERR_INVALID_ARGUMENT: return "SD_ERR_INVALID_ARGUMENT: null or misaligned pointer, bad size or inconsistent shape";
+    case SD_ERR_UNSUPPORTED: return "SD_ERR_UNSUPPORTED: shape outside what the kernels implement";
+    case SD_ERR_WORKSPACE: return "SD_ERR_WORKSPACE: workspace smaller than sd_workspace_bytes requires";
+    case SD_ERR_HIP: return "SD_ERR_HIP: a HIP launch or runtime call failed";
+    default: return "unknown status";
+  }
+}
+
+const char* sd_version(void) { return "0.1.0"; }
+
+}  // extern "C"

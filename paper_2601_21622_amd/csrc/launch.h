@@ -1,0 +1,75 @@
+// Host-side launchers of the verification kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sdv {
+
+// Requests handled by one attention / acceptance launch.  Their per-request
+// table travels in the kernel arguments, so no host-to-device copy is needed.
+constexpr int kMaxReqPerLaunch = 64;
+
+struct AttnBatch {
+  int32_t nreq;                                  // requests in this launch
+  int32_t req0;                                  // global index of the first one
+  int32_t chunk_base;                            // global chunk index of this launch's first chunk
+  int32_t chunk_prefix[kMaxReqPerLaunch + 1];    // local chunk index where each request starts
+  int32_t kv_len[kMaxReqPerLaunch];
+  int64_t kv_off[kMaxReqPerLaunch];
+};
+
+struct AttnShape {
+  int G;            // query positions per request
+  int Hq, Hkv, D;
+  int group;        // Hq / Hkv
+  int rows;         // G * group query rows per KV head
+  int chunk_keys;   // keys per partial (one workgroup)
+  float scale_log2; // softmax scale * log2(e)
+};
+
+// Partial results of one (chunk, KV head): running max m (log2 domain),
+// sum l = sum exp2(s - m), unnormalised o = sum exp2(s - m) v.
+struct AttnPartials {
+  float* m;  // [slots][rows]
+  float* l;  // [slots][rows]
+  float* o;  // [slots][rows][D]
+};
+
+int attn_chunk_keys(int dtype, int rows, int head_dim);
+size_t attn_partial_bytes(int64_t total_chunks, int Hkv, int rows, int D);
+AttnPartials attn_carve(void* ws, int64_t total_chunks, int Hkv, int rows, int D);
+
+hipError_t launch_attention(int dtype, const AttnShape& s, const AttnBatch& batch, int nchunks,
+                            const void* q, const void* k_pool, const void* v_pool,
+                            AttnPartials parts, hipStream_t stream);
+hipError_t launch_attention_combine(int dtype, const AttnShape& s, const AttnBatch& batch,
+                                    AttnPartials parts, void* out, hipStream_t stream);
+
+// Vocabulary projection.
+struct VocabPlan {
+  int M, K, V;
+  int tile_n;      // vocabulary columns per workgroup
+  int ntiles;      // ceil(V / tile_n)
+};
+VocabPlan vocab_plan(int dtype, int M, int K, int V);
+size_t vocab_partial_bytes(const VocabPlan& p);
+hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w,
+                        float* logits, float2* partials, hipStream_t stream);
+hipError_t launch_lse_combine(const VocabPlan& p, const float2* partials, float* row_lse,
+                              hipStream_t stream);
+
+// Acceptance and resampling.
+struct AcceptBatch {
+  int32_t nreq;
+  int32_t req0;
+  int32_t has_kv_len;
+  int32_t kv_len[kMaxReqPerLaunch];
+};
+hipError_t launch_accept(int gamma, int V, const AcceptBatch& batch, const float* x,
+                         const float* row_lse, const float* q_draft, const int32_t* draft_tok,
+                         const float* u, int32_t* accept_len, int32_t* out_tok,
+                         int32_t* new_kv_len, hipStream_t stream);
+
+}  // namespace sdv

@@ -1,0 +1,121 @@
+"""The C-ABI library on the CPU: it loads, exports every function the header
+declares, and rejects invalid arguments with the documented status before
+enqueuing anything (these calls never reach a kernel launch)."""
+
+import ctypes
+
+import pytest
+import torch
+
+import paper_2601_21622_amd as sd
+
+# Fake, suitably aligned device addresses: every call below fails its host
+# checks before any pointer is used.
+P = 0x100000
+cpu_only = pytest.mark.skipif(torch.cuda.is_available(), reason="host-validation tests use fake pointers")
+
+
+def dims(**kw):
+    base = dict(batch=2, gamma=3, n_q_heads=8, n_kv_heads=2, head_dim=128, hidden=1024, vocab=1000, dtype=1)
+    base.update(kw)
+    return sd.Dims(**base)
+
+
+def test_library_loads_and_exports_header_symbols():
+    lib = sd.library()
+    names = sd.exported_symbols()
+    assert set(names) == {"sd_workspace_bytes", "sd_verify_attention", "sd_verify_logits", "sd_accept_resample",
+                          "sd_verify_step", "sd_status_string", "sd_version"}
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sd.sd_version().count(".") == 2
+
+
+def test_status_strings():
+    for st in (sd.SD_OK, sd.SD_ERR_INVALID_ARGUMENT, sd.SD_ERR_UNSUPPORTED, sd.SD_ERR_WORKSPACE, sd.SD_ERR_HIP):
+        assert sd.sd_status_string(st).startswith("SD_")
+    assert sd.sd_status_string(12345) == "unknown status"
+
+
+def test_workspace_bytes():
+    d = dims()
+    a = sd.sd_workspace_bytes(d, 1000)
+    b = sd.sd_workspace_bytes(d, 100000)
+    assert 0 < a < b
+    assert sd.sd_workspace_bytes(d, 3) == 0           # shorter than gamma + 1
+    assert sd.sd_workspace_bytes(dims(head_dim=96), 1000) == 0
+    assert sd.sd_workspace_bytes(dims(n_q_heads=7), 1000) == 0
+
+
+def _attn(d, kv_off=(0, 8 * 128 * 2 * 64), kv_len=(64, 64), ws_bytes=1 << 30, q=P, k=P, v=P, out=P, ws=P,
+          scale=0.088):
+    lib = sd.library()
+    off = (ctypes.c_int64 * len(kv_off))(*kv_off)
+    ln = (ctypes.c_int32 * len(kv_len))(*kv_len)
+    return lib.sd_verify_attention(ctypes.byref(d), q, k, v, off, ln, scale, out, ws, ws_bytes, None)
+
+
+@cpu_only
+@pytest.mark.parametrize("bad,status", [
+    (dict(batch=0), sd.SD_ERR_INVALID_ARGUMENT),
+    (dict(gamma=0), sd.SD_ERR_INVALID_ARGUMENT),
+    (dict(n_q_heads=6, n_kv_heads=4), sd.SD_ERR_INVALID_ARGUMENT),
+    (dict(dtype=7), sd.SD_ERR_INVALID_ARGUMENT),
+    (dict(head_dim=96), sd.SD_ERR_UNSUPPORTED),
+    (dict(hidden=100), sd.SD_ERR_UNSUPPORTED),
+    (dict(gamma=64), sd.SD_ERR_UNSUPPORTED),
+    (dict(n_q_heads=68, n_kv_heads=2), sd.SD_ERR_UNSUPPORTED),   # 4 * 34 > 128 rows per KV head
+    (dict(vocab=3_000_000), sd.SD_ERR_UNSUPPORTED),
+])
+def test_attention_rejects_bad_dims(bad, status):
+    assert _attn(dims(**bad)) == status
+
+
+@cpu_only
+def test_attention_rejects_bad_pointers_lengths_and_workspace():
+    d = dims()
+    assert _attn(d, q=None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert _attn(d, k=P + 8) == sd.SD_ERR_INVALID_ARGUMENT        # misaligned
+    assert _attn(d, kv_len=(3, 64)) == sd.SD_ERR_INVALID_ARGUMENT  # shorter than gamma + 1
+    assert _attn(d, kv_off=(0, 3)) == sd.SD_ERR_INVALID_ARGUMENT   # offset not 16-byte aligned
+    assert _attn(d, kv_off=(-8, 0)) == sd.SD_ERR_INVALID_ARGUMENT
+    assert _attn(d, ws_bytes=16) == sd.SD_ERR_WORKSPACE
+    assert _attn(d, scale=float("nan")) == sd.SD_ERR_INVALID_ARGUMENT
+    lib = sd.library()
+    assert lib.sd_verify_attention(ctypes.byref(d), P, P, P, None, None, 0.1, P, P, 1 << 30, None) == \
+        sd.SD_ERR_INVALID_ARGUMENT
+    assert lib.sd_verify_attention(None, P, P, P, None, None, 0.1, P, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT
+
+
+@cpu_only
+def test_logits_and_accept_reject_bad_arguments():
+    lib = sd.library()
+    d = dims()
+    assert lib.sd_verify_logits(ctypes.byref(d), None, P, P, P, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert lib.sd_verify_logits(ctypes.byref(d), P, P, P + 4, P, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert lib.sd_verify_logits(ctypes.byref(d), P, P, P, P, P, 8, None) == sd.SD_ERR_WORKSPACE
+    # new_kv_len without kv_len
+    assert lib.sd_accept_resample(ctypes.byref(d), P, P, P, P, P, None, P, P, P, None, 0, None) == \
+        sd.SD_ERR_INVALID_ARGUMENT
+    assert lib.sd_accept_resample(ctypes.byref(d), P, P, P, P + 2, P, None, P, P, None, None, 0, None) == \
+        sd.SD_ERR_INVALID_ARGUMENT
+    short = (ctypes.c_int32 * 2)(2, 10)
+    assert lib.sd_accept_resample(ctypes.byref(d), P, P, P, P, P, short, P, P, P, None, 0, None) == \
+        sd.SD_ERR_INVALID_ARGUMENT
+
+
+@cpu_only
+def test_step_rejects_hidden_null_with_mismatched_width():
+    lib = sd.library()
+    d = dims(hidden=2048)  # != n_q_heads * head_dim = 1024
+    off = (ctypes.c_int64 * 2)(0, 8 * 128 * 2 * 64)
+    ln = (ctypes.c_int32 * 2)(64, 64)
+    st = lib.sd_verify_step(ctypes.byref(d), P, P, P, off, ln, 0.1, None, P, P, P, P, P, P, P, P, P, P, P,
+                            1 << 30, None, None)
+    assert st == sd.SD_ERR_INVALID_ARGUMENT
+
+
+def test_binding_requires_device_tensors():
+    d = dims()
+    with pytest.raises((TypeError, ValueError)):
+        sd.sd_verify_logits(d, torch.zeros(4), torch.zeros(4), torch.zeros(4), torch.zeros(4), torch.zeros(4))

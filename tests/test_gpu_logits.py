@@ -1,0 +1,58 @@
+"""GPU parity: sd_verify_logits (vocabulary projection + row log-sum-exp)
+against the float64 oracle.  Shapes cover ragged vocabulary tiles (V not a
+multiple of 64, and not of 4), every K-chunk path, several M-tiles, and the
+tiny fp32 case."""
+
+import numpy as np
+import pytest
+
+from oracle import verify_logits
+from workloads import get_config, make_inputs
+
+from gpu_util import RTOL, DeviceBatch, announce, assert_close_rows, to_np
+
+pytestmark = pytest.mark.gpu
+
+_v = get_config("vicuna7b")
+CASES = {
+    "tiny_f32": get_config("tiny"),
+    "m18_k512_v1000": _v.replace(batch=3, n_q_heads=4, n_kv_heads=4, hidden=512, vocab=1000,
+                                 lengths=("fixed", 16)),
+    "m18_k512_v1003": _v.replace(batch=3, n_q_heads=4, n_kv_heads=4, hidden=512, vocab=1003,
+                                 lengths=("fixed", 16)),
+    "m100_k256_v777": _v.replace(batch=20, gamma=4, n_q_heads=2, n_kv_heads=2, hidden=256, vocab=777,
+                                 lengths=("fixed", 8)),
+    "m320_k96_v300": _v.replace(batch=64, gamma=4, n_q_heads=2, n_kv_heads=2, hidden=96, vocab=300,
+                                lengths=("fixed", 8)),
+    "m336_k256_v130": _v.replace(batch=56, gamma=5, n_q_heads=2, n_kv_heads=2, hidden=256, vocab=130,
+                                 lengths=("fixed", 8)),
+    "f32_m70_k128_v65": get_config("tiny").replace(batch=14, gamma=4, hidden=128, vocab=65, lengths=("fixed", 8)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_logits_match_oracle(name):
+    cfg = CASES[name]
+    announce(f"logits parity case={name} M={cfg.rows} K={cfg.hidden} V={cfg.vocab} dtype={cfg.dtype}")
+    x = make_inputs(cfg)
+    db = DeviceBatch(x)
+    db.logits_()
+    ref_logits, ref_lse = verify_logits(x.f32("hidden"), x.f32("w"))
+    err = assert_close_rows(to_np(db.logits), ref_logits, RTOL[cfg.dtype], f"logits[{name}]")
+    lse = to_np(db.lse).astype(np.float64)
+    assert np.all(np.abs(lse - ref_lse) <= RTOL[cfg.dtype] * np.maximum(np.abs(ref_lse), 1.0)), (lse, ref_lse)
+    # The float32 logits with the float32 lse give distributions that sum to one.
+    p = np.exp(to_np(db.logits).astype(np.float64) - lse[:, None])
+    assert np.allclose(p.sum(axis=1), 1.0, atol=1e-5)
+    announce(f"logits case={name} max scaled err {err:.3e} max |dlse| {np.abs(lse - ref_lse).max():.3e}")
+
+
+def test_logits_deterministic():
+    x = make_inputs(CASES["m100_k256_v777"])
+    db = DeviceBatch(x)
+    db.logits_()
+    a, b = to_np(db.logits).copy(), to_np(db.lse).copy()
+    db.logits.zero_()
+    db.lse.zero_()
+    db.logits_()
+    assert np.array_equal(a, to_np(db.logits)) and np.array_equal(b, to_np(db.lse))
