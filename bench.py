@@ -1,0 +1,267 @@
+#!/usr/bin/env python3
+"""Throughput of the batched speculative-verification step on one MI355X.
+
+A step is one pass of the whole hot path over one pooled batch: causal
+multi-query attention over every request's KV cache, the vocabulary
+projection with its softmax statistics, and the acceptance test with residual
+resampling (sd_verify_step).  The default workload is the Vicuna-7B-shaped
+single-layer verify: B = 8 requests, gamma = 5 drafts, 32 heads of 128,
+hidden 4096, vocabulary 32000, kv_len ~ U[512, 2048], bf16.
+
+Inputs are synthetic and seeded (no weights or prompts exist here).  They are
+resident in HBM before timing starts, and the timed steps rotate over several
+identical copies placed at different addresses, so that each step streams its
+KV cache and vocabulary weights from HBM rather than from the 256 MB Infinity
+Cache.
+
+Prints one JSON line.  `value` is verified (emitted) tokens per second: each
+request emits its accepted drafts plus one corrected or bonus token.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
+INFINITY_CACHE_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_digest(name: str) -> str:
+    with open(os.path.join(ROOT, "paper_2601_21622_amd", "csrc", name), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def counter_traffic(kernel: str, workload: str, source: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when there is none or the kernel source changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            entries = json.load(f)
+    except (OSError, ValueError):
+        return None
+    for e in entries:
+        if e.get("kernel") == kernel and e.get("workload") == workload:
+            if e.get("source_sha256") != source_digest(source):
+                return None
+            return float(e["bytes_per_launch"])
+    return None
+
+
+def cpu_baseline(x, budget_s: float):
+    """The oracle (plain float64 numpy) on the same batch, repeated until about
+    budget_s seconds of CPU work; emitted tokens per second."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import verify_step
+
+    c = x.cfg
+    q, k, v, h, w = x.f32("q"), x.f32("k_pool"), x.f32("v_pool"), x.f32("hidden"), x.f32("w")
+    runs, t_total, emitted = 0, 0.0, 0
+    while runs < 1 or (t_total < budget_s and runs < 20):
+        t0 = time.perf_counter()
+        out = verify_step(q, k, v, x.kv_off, x.kv_len, c.n_kv_heads, h, w, x.q_draft, x.draft, x.u)
+        t_total += time.perf_counter() - t0
+        runs += 1
+        emitted = int((out["accept_len"] + 1).sum())
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {
+        "value": emitted * runs / t_total,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"the full {c.batch}-request batch of the {c.name} workload, {runs} step(s) "
+                  f"({t_total:.1f} s), float64 numpy",
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="vicuna7b")
+    ap.add_argument("--copies", type=int, default=0, help="input copies to rotate over (0: enough to exceed "
+                                                           "4x the Infinity Cache)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a device copy of known size (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the verification step "
+              "does not shard across GPUs in this build)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2601_21622_amd as sd
+    from workloads import get_config, make_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    torch.cuda.set_device(0)
+    cfg = get_config(args.workload)
+    B, G, M, V, K = cfg.batch, cfg.positions, cfg.rows, cfg.vocab, cfg.hidden
+    log(f"generating workload {cfg.name}")
+    x = make_inputs(cfg)
+    dims = sd.Dims.of(cfg)
+    scale = 1.0 / math.sqrt(cfg.head_dim)
+
+    def dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    big_bytes = x.k_pool.nbytes + x.v_pool.nbytes + x.w.nbytes
+    ncopies = args.copies or max(2, math.ceil(4 * INFINITY_CACHE_BYTES / big_bytes) + 1)
+    adt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    ws_bytes = sd.sd_workspace_bytes(dims, int(x.kv_len.max()))
+    copies = []
+    base = {n: dev(getattr(x, n)) for n in ("q", "k_pool", "v_pool", "hidden", "w", "q_draft", "draft", "u")}
+    for i in range(ncopies):
+        t = {n: (a if i == 0 else a.clone()) for n, a in base.items()}
+        t["attn"] = torch.empty((B, G, cfg.n_q_heads, cfg.head_dim), dtype=adt, device="cuda")
+        t["logits"] = torch.empty((M, V), dtype=torch.float32, device="cuda")
+        t["lse"] = torch.empty((M,), dtype=torch.float32, device="cuda")
+        t["acc"] = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+        t["tok"] = torch.empty((B, G), dtype=torch.int32, device="cuda")
+        t["new"] = torch.empty((B,), dtype=torch.int32, device="cuda")
+        t["ws"] = torch.empty((ws_bytes,), dtype=torch.uint8, device="cuda")
+        copies.append(t)
+    log(f"{ncopies} input copies of {big_bytes / 1e6:.0f} MB each")
+
+    def prepared(t, events=None):
+        return sd.prepare_verify_step(dims, t["q"], t["k_pool"], t["v_pool"], x.kv_off, x.kv_len, scale, t["hidden"],
+                                      t["w"], t["q_draft"], t["draft"], t["u"], t["attn"], t["logits"], t["lse"],
+                                      t["acc"], t["tok"], t["new"], t["ws"], kernel_events=events)
+
+    calls = [prepared(t) for t in copies]
+
+    if args.calibrate_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    for i in range(args.warmup):
+        calls[i % ncopies]()
+    torch.cuda.synchronize()
+
+    # Headline: steps back to back, nothing else on the stream.
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    w0 = time.perf_counter()
+    for i in range(args.steps):
+        calls[(args.warmup + i) % ncopies]()
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+    log(f"timed {args.steps} steps: {ms_total:.3f} ms on the GPU clock, {wall * 1e3:.3f} ms wall")
+
+    # Per-kernel times: the same steps again, each kernel launch recording its
+    # own start/stop events (hipExtLaunchKernelGGL), which adds no stream work.
+    nev = min(args.steps, 200)
+    kev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(nev)]
+    kcalls = [prepared(copies[i % ncopies], kev[i]) for i in range(nev)]
+    torch.cuda.synchronize()
+    s2, e2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s2.record()
+    for c in kcalls:
+        c()
+    e2.record()
+    torch.cuda.synchronize()
+    ms_step_ev = s2.elapsed_time(e2) / nev
+    stage = np.array([[ev[2 * j].elapsed_time(ev[2 * j + 1]) for j in range(3)] for ev in kev])  # ms
+    st_mean = stage.mean(axis=0)
+
+    acc = [t["acc"].cpu().numpy() for t in copies]
+    if not all(np.array_equal(acc[0], a) for a in acc):
+        raise RuntimeError("input copies disagree on the accept lengths")
+    emitted = int((acc[0] + 1).sum())
+    accepted = int(acc[0].sum())
+
+    # Roofline of each kernel stage (algorithmic bytes / flops per launch).
+    kv_bytes = 2 * int(x.kv_len.astype(np.int64).sum()) * cfg.n_kv_heads * cfg.head_dim * (2 if cfg.dtype == "bf16" else 4)
+    esz = 2 if cfg.dtype == "bf16" else 4
+    attn_bytes = kv_bytes + 2 * B * G * cfg.n_q_heads * cfg.head_dim * esz
+    ntiles = (V + 63) // 64
+    vocab_bytes = V * K * esz + M * K * esz + M * V * 4 + M * ntiles * 8
+    vocab_flops = 2.0 * M * K * V
+    attn_gbps = attn_bytes / (st_mean[0] * 1e-3) / 1e9
+    vocab_gbps = vocab_bytes / (st_mean[1] * 1e-3) / 1e9
+    vocab_tflops = vocab_flops / (st_mean[1] * 1e-3) / 1e12
+    dominant = "vocab" if st_mean[1] >= st_mean[0] else "attention"
+    if dominant == "vocab":
+        traffic = counter_traffic("vocab_bf16_kernel", cfg.name, "vocab.hip")
+        roof = {"bound": "hbm", "achieved": vocab_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": vocab_gbps / HBM_PEAK_GBPS, "traffic": traffic, "kernel": "vocab_bf16_kernel",
+                "bytes_per_launch": vocab_bytes, "ms_per_launch": float(st_mean[1])}
+    else:
+        traffic = counter_traffic("attn_bf16_kernel", cfg.name, "attention.hip")
+        roof = {"bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": attn_gbps / HBM_PEAK_GBPS, "traffic": traffic, "kernel": "attn_bf16_kernel",
+                "bytes_per_launch": attn_bytes, "ms_per_launch": float(st_mean[0])}
+
+    result = {
+        "metric": "verified tokens/sec per MI355X",
+        "value": emitted / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name,
+            "batch": B, "gamma": cfg.gamma, "n_q_heads": cfg.n_q_heads, "n_kv_heads": cfg.n_kv_heads,
+            "head_dim": cfg.head_dim, "hidden": K, "vocab": V,
+            "kv_len": list(cfg.lengths), "kv_tokens": int(x.kv_len.sum()), "draft": list(cfg.draft),
+            "input_copies": ncopies,
+        },
+        "roofline": roof,
+        "scored_tokens_per_s": B * G / (ms_step * 1e-3),
+        "accepted_tokens_per_s": accepted / (ms_step * 1e-3),
+        "emitted_per_step": emitted,
+        "kernel_ms": {"attention": float(st_mean[0]), "vocab_projection": float(st_mean[1]),
+                      "accept_segments": float(st_mean[2])},
+        "ms_per_step_with_kernel_events": ms_step_ev,
+        "attention_hbm_gbps": attn_gbps,
+        "vocab_hbm_gbps": vocab_gbps,
+        "vocab_mfma_frac": vocab_tflops / BF16_MFMA_PEAK_TFLOPS,
+        "vocab_attainable_frac": vocab_tflops / min(BF16_MFMA_PEAK_TFLOPS, vocab_flops / vocab_bytes * HBM_PEAK_GBPS / 1e3),
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on the same batch")
+        result["cpu_baseline"] = cpu_baseline(x, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

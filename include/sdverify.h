@@ -129,6 +129,7 @@ SD_API int sd_verify_logits(const sd_dims_t* dims, const void* hidden, const voi
  *   accept_len      [B] int32 output: l_b in [0, gamma]
  *   out_tok         [B][G] int32 output: x_1..x_l, then the sampled token, then -1 padding
  *   new_kv_len      [B] int32 output or NULL: kv_len[b] - gamma + l_b (cache entries to keep)
+ *   workspace       at least sd_workspace_bytes(dims, ...) bytes (per-segment partial sums)
  * Rules (per request, p_i = row b*G + i - 1):
  *   ratio_i = p_i(x_i) / q_i(x_i), with ratio = 0 if p_i(x_i) = 0 and +inf if
  *   q_i(x_i) = 0 < p_i(x_i); x_i passes iff u[b][i-1] < ratio_i; l = number of
@@ -152,9 +153,12 @@ SD_API int sd_accept_resample(const sd_dims_t* dims, const float* logits_or_prob
  * [M][n_q_heads * head_dim], which then must equal dims->hidden), then
  * sd_accept_resample on the logits and row_lse it produced.  Arguments as in
  * the three calls; attn_out, logits, row_lse are outputs the caller owns.
- *   stage_events  (host) NULL, or 4 hipEvent_t handles recorded on `stream`
- *                 before attention, after attention, after the vocabulary
- *                 projection (including row_lse) and after acceptance.
+ *   kernel_events  (host) NULL, or 6 hipEvent_t handles (created with timing
+ *                  enabled): start/stop of the attention kernel, of the
+ *                  vocabulary-projection kernel and of the acceptance
+ *                  segment kernel.  They are recorded by the kernel launches
+ *                  themselves (no extra work on the stream), so the elapsed
+ *                  time of each pair is that kernel's execution time.
  */
 SD_API int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
                    const int64_t* kv_off, const int32_t* kv_len, float scale,
@@ -162,7 +166,7 @@ SD_API int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_po
                    const int32_t* draft_tok, const float* u, void* attn_out, float* logits,
                    float* row_lse, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
                    void* workspace, size_t workspace_bytes, sd_stream_t stream,
-                   void* const* stage_events);
+                   void* const* kernel_events);
 
 /* Static description of a status code. */
 SD_API const char* sd_status_string(int status);

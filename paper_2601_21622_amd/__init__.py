@@ -17,10 +17,12 @@ from ._binding import (  # noqa: F401
     SD_ERR_WORKSPACE,
     SD_OK,
     Dims,
+    PreparedCall,
     SdError,
     exported_symbols,
     library,
     library_path,
+    prepare_verify_step,
     sd_accept_resample,
     sd_status_string,
     sd_verify_attention,

@@ -164,35 +164,66 @@ def sd_verify_logits(dims: Dims, hidden, w_vocab, logits, row_lse, workspace, st
 
 
 def sd_accept_resample(dims: Dims, logits_or_probs, row_lse, q_draft, draft_tok, u, kv_len, accept_len,
-                       out_tok, new_kv_len, workspace=None, stream=None) -> None:
+                       out_tok, new_kv_len, workspace, stream=None) -> None:
     _len, len_p = _host(kv_len, np.int32)
-    ws_bytes = 0 if workspace is None else _nbytes(workspace)
     st = library().sd_accept_resample(ctypes.byref(dims), _ptr(logits_or_probs), _ptr(row_lse), _ptr(q_draft),
                                       _ptr(draft_tok), _ptr(u), len_p, _ptr(accept_len), _ptr(out_tok),
-                                      _ptr(new_kv_len), _ptr(workspace), ws_bytes, _stream(stream))
+                                      _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace), _stream(stream))
     _check(st, "sd_accept_resample")
+
+
+def _event_handles(events):
+    if events is None:
+        return None
+    handles = []
+    for e in events:
+        if not isinstance(e, int):
+            if e.cuda_event == 0:  # torch creates its event lazily, on first record
+                e.record()
+            e = e.cuda_event
+        handles.append(e)
+    if len(handles) != 6:
+        raise ValueError("kernel_events needs 6 events (start/stop of three kernels)")
+    return (ctypes.c_void_p * 6)(*handles)
+
+
+class PreparedCall:
+    """One C call whose arguments were converted once.  Calling it re-issues
+    the call with the same pointers, sizes and stream; the caller keeps every
+    buffer alive.  (For tight launch loops, where per-call marshalling would
+    cost more than the GPU work.)"""
+
+    def __init__(self, fn, args, keep, where):
+        self._fn, self._args, self._keep, self._where = fn, args, keep, where
+
+    def __call__(self) -> None:
+        st = self._fn(*self._args)
+        if st != SD_OK:
+            raise SdError(st, self._where)
+
+
+def _step_args(dims, q, k_pool, v_pool, kv_off, kv_len, scale, hidden, w_vocab, q_draft, draft_tok, u, attn_out,
+               logits, row_lse, accept_len, out_tok, new_kv_len, workspace, stream=None, kernel_events=None):
+    off, off_p = _host(kv_off, np.int64)
+    ln, len_p = _host(kv_len, np.int32)
+    ev = _event_handles(kernel_events)
+    args = (ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p, float(scale), _ptr(hidden),
+            _ptr(w_vocab), _ptr(q_draft), _ptr(draft_tok), _ptr(u), _ptr(attn_out), _ptr(logits), _ptr(row_lse),
+            _ptr(accept_len), _ptr(out_tok), _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace),
+            _stream(stream), ev)
+    return args, (dims, off, ln, ev)
 
 
 def sd_verify_step(dims: Dims, q, k_pool, v_pool, kv_off, kv_len, scale: float, hidden, w_vocab, q_draft,
                    draft_tok, u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace,
-                   stream=None, stage_events=None) -> None:
-    _off, off_p = _host(kv_off, np.int64)
-    _len, len_p = _host(kv_len, np.int32)
-    ev = None
-    if stage_events is not None:
-        handles = []
-        for e in stage_events:
-            if not isinstance(e, int):
-                if e.cuda_event == 0:  # torch creates its event lazily, on first record
-                    e.record()
-                e = e.cuda_event
-            handles.append(e)
-        if len(handles) != 4:
-            raise ValueError("stage_events needs exactly 4 events")
-        ev = (ctypes.c_void_p * 4)(*handles)
-    st = library().sd_verify_step(ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p,
-                                  float(scale), _ptr(hidden), _ptr(w_vocab), _ptr(q_draft), _ptr(draft_tok),
-                                  _ptr(u), _ptr(attn_out), _ptr(logits), _ptr(row_lse), _ptr(accept_len),
-                                  _ptr(out_tok), _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace),
-                                  _stream(stream), ev)
-    _check(st, "sd_verify_step")
+                   stream=None, kernel_events=None) -> None:
+    args, _keep = _step_args(dims, q, k_pool, v_pool, kv_off, kv_len, scale, hidden, w_vocab, q_draft, draft_tok,
+                             u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace, stream,
+                             kernel_events)
+    _check(library().sd_verify_step(*args), "sd_verify_step")
+
+
+def prepare_verify_step(*a, **kw) -> PreparedCall:
+    """sd_verify_step with the same arguments, converted once (see PreparedCall)."""
+    args, keep = _step_args(*a, **kw)
+    return PreparedCall(library().sd_verify_step, args, (keep, a, kw), "sd_verify_step")

@@ -1,16 +1,24 @@
 // Acceptance test, first rejection, residual resampling and output assembly.
 //
-// One workgroup per request:
-//  1. wave 0 evaluates the gamma ratio tests in float64 (lane i tests x_{i+1}:
-//     u < p_i(x_i) / q_i(x_i)) and finds the first failure with a ballot;
-//  2. the four waves sum the unnormalised continuation distribution
-//     r = max(0, p_{l+1} - q_{l+1}) (or p_{gamma+1} after a full accept) over
-//     512-entry segments of the vocabulary, in float64;
-//  3. wave 0 prefix-sums the segment totals (Z is the last one), finds the
-//     segment holding u * Z and scans it in token order for the first entry
-//     whose cumulative sum exceeds u * Z.
-// p(v) = exp(logit - lse) is evaluated with the difference kept exact (TwoSum)
-// so its error stays a few float32 ulp, far below the 1e-6 decision band.
+// Three short kernels, so that no single workgroup walks a whole vocabulary
+// row and each has one or two dependent memory round trips:
+//  accept_prepare: one workgroup per request.  Optionally folds the
+//     vocabulary kernel's per-tile statistics into the row log-sum-exp of the
+//     request's rows (one wave per row); then lanes 0..gamma-1 run the ratio
+//     tests in float64 (lane i: u < p_i(x_i) / q_i(x_i)) and a ballot gives
+//     the accept length l.
+//  accept_segments: one wave per (512-entry vocabulary segment, request) sums,
+//     in float64, the unnormalised continuation distribution over its segment:
+//     r = max(0, p_{l+1} - q_{l+1}) after a rejection, p_{gamma+1} after a
+//     full accept.
+//  accept_finalize: one wave per request prefix-sums the segment totals (Z is
+//     the last), finds the segment holding u * Z and scans it in token order
+//     for the first entry whose running sum exceeds u * Z; then writes the
+//     accept length, the emitted tokens and the new cache length.
+// p(v) = exp(logit - lse) keeps the difference exact (TwoSum) so its error is
+// a few float32 ulp, far below the 1e-6 decision band.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "launch.h"
 
@@ -18,9 +26,8 @@ namespace sdv {
 
 namespace {
 
-constexpr int kAccThreads = 256;
-constexpr int kAccWaves = 4;
 constexpr int kSeg = 512;
+constexpr int kPerLane = kSeg / kWave;
 constexpr int kMaxSeg = 4096;  // vocabularies up to 2,097,152 entries
 
 // exp(a - b), with a - b carried exactly as s + err.
@@ -32,166 +39,239 @@ __device__ __forceinline__ float exp_diff(float a, float b) {
   return fmaf(e, err, e);
 }
 
-struct RowView {
-  const float* x;    // logits or probabilities of the row p_{l+1}
-  const float* q;    // q_{l+1}, or nullptr for the bonus row
-  float lse;
-  bool from_logits;
-  bool residual;
-
-  __device__ __forceinline__ float r(int v) const {
-    const float p = from_logits ? exp_diff(x[v], lse) : x[v];
-    if (!residual) return p;
-    const float d = p - q[v];
-    return d > 0.f ? d : 0.f;
-  }
+struct AcceptArgs {
+  int gamma, V, nseg;
+  const float* x;        // [M][V] logits (lse != nullptr) or probabilities
+  const float* lse;      // [M] or nullptr
+  const float* q;        // [B][gamma][V]
+  const int32_t* draft;  // [B][gamma]
+  const float* u;        // [B][G]
+  double* segsum;        // [B][nseg]
+  int32_t* acc_ws;       // [B] accept length handed from segments to finalize
 };
 
-__global__ __launch_bounds__(kAccThreads)
-void accept_kernel(int gamma, int V, const AcceptBatch bt, const float* __restrict__ x,
-                   const float* __restrict__ row_lse, const float* __restrict__ q_draft,
-                   const int32_t* __restrict__ draft_tok, const float* __restrict__ u,
-                   int32_t* __restrict__ accept_len, int32_t* __restrict__ out_tok,
-                   int32_t* __restrict__ new_kv_len) {
-  __shared__ double seg[kMaxSeg];
-  __shared__ int s_l;
-  __shared__ int s_t;
-  __shared__ double s_z;
+__device__ __forceinline__ float r_of(const AcceptArgs& a, const float* xrow, const float* qrow, float lse,
+                                      bool residual, int v) {
+  const float p = a.lse != nullptr ? exp_diff(xrow[v], lse) : xrow[v];
+  if (!residual) return p;
+  const float d = p - qrow[v];
+  return d > 0.f ? d : 0.f;
+}
 
-  const int b = blockIdx.x;
-  const int req = bt.req0 + b;
-  const int G = gamma + 1;
+// Accept length of request `req` given the log-sum-exp of its rows in `lse`
+// (or probabilities when a.lse is null); every lane returns it.
+__device__ __forceinline__ int accept_length(const AcceptArgs& a, int req, const float* lse) {
+  const int lane = threadIdx.x & 63;
+  const int G = a.gamma + 1;
+  bool fail = false;
+  if (lane < a.gamma) {
+    const int tok = a.draft[(int64_t)req * a.gamma + lane];
+    double ratio = 0.0;
+    if (tok >= 0 && tok < a.V) {
+      const int64_t row = (int64_t)req * G + lane;
+      const float xv = a.x[row * a.V + tok];
+      const double px = a.lse != nullptr ? exp((double)xv - (double)lse[lane]) : (double)xv;
+      const double qx = (double)a.q[((int64_t)req * a.gamma + lane) * a.V + tok];
+      ratio = (px <= 0.0) ? 0.0 : (qx <= 0.0 ? (double)INFINITY : px / qx);
+    }
+    fail = !((double)a.u[(int64_t)req * G + lane] < ratio);
+  }
+  const unsigned long long fails = __ballot(fail);
+  return fails ? (__ffsll(fails) - 1) : a.gamma;
+}
+
+// partials != nullptr: fold them into the row log-sum-exp, write it to a.lse
+// (the caller's row_lse output) and use it; otherwise read a.lse if given.
+__global__ __launch_bounds__(256)
+void accept_prepare_kernel(const AcceptArgs a, int req0, const float2* __restrict__ partials, int ntiles) {
+  __shared__ float s_lse[kWave];
+  const int req = req0 + blockIdx.x;
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const float* xr = x + (int64_t)req * G * V;
-  const bool from_logits = row_lse != nullptr;
-
-  // 1. Ratio tests and the first rejection.
-  if (wave == 0) {
-    bool fail = false;
-    if (lane < gamma) {
-      const int tok = draft_tok[(int64_t)req * gamma + lane];
-      double ratio = 0.0;
-      if (tok >= 0 && tok < V) {
-        const double px = from_logits
-                              ? exp((double)xr[(int64_t)lane * V + tok] - (double)row_lse[(int64_t)req * G + lane])
-                              : (double)xr[(int64_t)lane * V + tok];
-        const double qx = (double)q_draft[((int64_t)req * gamma + lane) * V + tok];
-        ratio = (px <= 0.0) ? 0.0 : (qx <= 0.0 ? (double)INFINITY : px / qx);
+  const int G = a.gamma + 1;
+  if (partials != nullptr) {
+    for (int j = wave; j < G; j += 4) {
+      const float v = row_lse_from_partials(partials + ((int64_t)req * G + j) * ntiles, ntiles);
+      if (lane == 0) {
+        s_lse[j] = v;
+        const_cast<float*>(a.lse)[(int64_t)req * G + j] = v;
       }
-      fail = !((double)u[(int64_t)req * G + lane] < ratio);
     }
-    const unsigned long long fails = __ballot(fail);
-    if (lane == 0) s_l = fails ? (__ffsll(fails) - 1) : gamma;
+  } else if (a.lse != nullptr && threadIdx.x < G) {
+    s_lse[threadIdx.x] = a.lse[(int64_t)req * G + threadIdx.x];
   }
   __syncthreads();
-  const int l = s_l;
-
-  RowView rv;
-  rv.x = xr + (int64_t)l * V;
-  rv.q = (l < gamma) ? q_draft + ((int64_t)req * gamma + l) * V : nullptr;
-  rv.lse = from_logits ? row_lse[(int64_t)req * G + l] : 0.f;
-  rv.from_logits = from_logits;
-  rv.residual = l < gamma;
-  const int nseg = (V + kSeg - 1) / kSeg;
-  const double uf = (double)u[(int64_t)req * G + gamma];
-
-  double z = 0.0;
-  for (int attempt = 0; attempt < 2; ++attempt) {
-    // 2. Segment sums.
-    for (int sg = wave; sg < nseg; sg += kAccWaves) {
-      double acc = 0.0;
-#pragma unroll 4
-      for (int e = 0; e < kSeg / kWave; ++e) {
-        const int v = sg * kSeg + e * kWave + lane;
-        if (v < V) acc += (double)rv.r(v);
-      }
-      acc = wave_sum_f64(acc);
-      if (lane == 0) seg[sg] = acc;
-    }
-    __syncthreads();
-    // 3a. Inclusive prefix of the segment sums.
-    if (wave == 0) {
-      double carry = 0.0;
-      for (int base = 0; base < nseg; base += kWave) {
-        const int i = base + lane;
-        const double v = i < nseg ? seg[i] : 0.0;
-        const double c = wave_inclusive_scan_f64(v) + carry;
-        if (i < nseg) seg[i] = c;
-        carry = __shfl(c, 63);
-      }
-      if (lane == 0) s_z = carry;
-    }
-    __syncthreads();
-    z = s_z;
-    if (z > 0.0 || !rv.residual) break;
-    // Residual vanished (possible only through rounding): sample from p_{l+1}.
-    rv.residual = false;
-    __syncthreads();
-  }
-
-  // 3b. Locate u * Z and scan its segment in token order.
   if (wave == 0) {
-    const double thr = uf * z;
-    int found = -1;
-    for (int base = 0; base < nseg && found < 0; base += kWave) {
+    const int l = accept_length(a, req, s_lse);
+    if (lane == 0) a.acc_ws[req] = l;
+  }
+}
+
+__global__ __launch_bounds__(kWave)
+void accept_segments_kernel(const AcceptArgs a, int req0) {
+  const int sg = blockIdx.x;
+  const int req = req0 + blockIdx.y;
+  const int lane = threadIdx.x;
+  const int G = a.gamma + 1;
+  const int l = a.acc_ws[req];
+  const bool residual = l < a.gamma;
+  const int64_t row = (int64_t)req * G + l;
+  const float* xrow = a.x + row * a.V;
+  const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
+  const float lse = a.lse != nullptr ? a.lse[row] : 0.f;
+  float r[kPerLane];
+#pragma unroll
+  for (int e = 0; e < kPerLane; ++e) {
+    const int v = sg * kSeg + e * kWave + lane;
+    r[e] = v < a.V ? r_of(a, xrow, qrow, lse, residual, v) : 0.f;
+  }
+  double acc = 0.0;
+#pragma unroll
+  for (int e = 0; e < kPerLane; ++e) acc += (double)r[e];
+  acc = wave_sum_f64(acc);
+  if (lane == 0) a.segsum[(int64_t)req * a.nseg + sg] = acc;
+}
+
+// Sum of r over one segment, recomputed (used only on the rare fallback path).
+__device__ double segment_sum(const AcceptArgs& a, const float* xrow, const float* qrow, float lse, bool residual,
+                              int sg) {
+  const int lane = threadIdx.x & 63;
+  double acc = 0.0;
+  for (int e = 0; e < kPerLane; ++e) {
+    const int v = sg * kSeg + e * kWave + lane;
+    if (v < a.V) acc += (double)r_of(a, xrow, qrow, lse, residual, v);
+  }
+  return wave_sum_f64(acc);
+}
+
+__global__ __launch_bounds__(kWave)
+void accept_finalize_kernel(const AcceptArgs a, const AcceptBatch bt, int32_t* __restrict__ accept_len,
+                            int32_t* __restrict__ out_tok, int32_t* __restrict__ new_kv_len) {
+  const int b = blockIdx.x;
+  const int req = bt.req0 + b;
+  const int lane = threadIdx.x;
+  const int G = a.gamma + 1;
+  const int l = a.acc_ws[req];
+  bool residual = l < a.gamma;
+  const int64_t row = (int64_t)req * G + l;
+  const float* xrow = a.x + row * a.V;
+  const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
+  const float lse = a.lse != nullptr ? a.lse[row] : 0.f;
+  __shared__ double seg[kMaxSeg];
+  for (int i = lane; i < a.nseg; i += kWave) seg[i] = a.segsum[(int64_t)req * a.nseg + i];
+  lds_wait();
+
+  // Inclusive prefix of the segment totals, in place (LDS, one wave).
+  auto prefix = [&]() -> double {
+    lds_wait();
+    double carry = 0.0;
+    for (int base = 0; base < a.nseg; base += kWave) {
       const int i = base + lane;
-      const unsigned long long hit = __ballot(i < nseg && seg[i] > thr);
-      if (hit) found = base + __ffsll(hit) - 1;
+      const double v = i < a.nseg ? seg[i] : 0.0;
+      const double c = wave_inclusive_scan_f64(v) + carry;
+      if (i < a.nseg) seg[i] = c;
+      carry = __shfl(c, 63);
     }
-    int t = -1;
-    if (found >= 0) {
-      double c = found > 0 ? seg[found - 1] : 0.0;
-      int last_pos = -1;
-      for (int e = 0; e < kSeg / kWave && t < 0; ++e) {
-        const int v = found * kSeg + e * kWave + lane;
-        const double r = v < V ? (double)rv.r(v) : 0.0;
-        const double cum = wave_inclusive_scan_f64(r) + c;
-        const unsigned long long hit = __ballot(v < V && r > 0.0 && cum > thr);
-        if (hit) t = found * kSeg + e * kWave + __ffsll(hit) - 1;
-        const unsigned long long pos = __ballot(v < V && r > 0.0);
-        if (pos) last_pos = found * kSeg + e * kWave + 63 - __clzll(pos);
-        c = __shfl(cum, 63);
-      }
-      if (t < 0) t = last_pos;  // rounding put u * Z past this segment's scan
+    lds_wait();
+    return carry;
+  };
+  double z = prefix();
+  if (!(z > 0.0) && residual) {
+    // The residual vanished (possible only through rounding): sample from p_{l+1}.
+    residual = false;
+    for (int sg = 0; sg < a.nseg; ++sg) {
+      const double s = segment_sum(a, xrow, qrow, lse, false, sg);
+      if (lane == 0) seg[sg] = s;
     }
-    if (t < 0) {
-      // No prefix sum exceeds u * Z: the largest token with mass.
-      for (int sg = nseg - 1; sg >= 0 && t < 0; --sg) {
-        for (int e = kSeg / kWave - 1; e >= 0 && t < 0; --e) {
-          const int v = sg * kSeg + e * kWave + lane;
-          const unsigned long long pos = __ballot(v < V && rv.r(v) > 0.f);
-          if (pos) t = sg * kSeg + e * kWave + 63 - __clzll(pos);
-        }
-      }
-      if (t < 0) t = 0;  // no mass at all (non-finite input)
-    }
-    if (lane == 0) s_t = t;
+    z = prefix();
   }
-  __syncthreads();
 
-  // Output assembly.
-  if (threadIdx.x < G) {
-    const int i = threadIdx.x;
-    int32_t v = -1;
-    if (i < l) v = draft_tok[(int64_t)req * gamma + i];
-    else if (i == l) v = s_t;
-    out_tok[(int64_t)req * G + i] = v;
+  const double thr = (double)a.u[(int64_t)req * G + a.gamma] * z;
+  int found = -1;
+  for (int base = 0; base < a.nseg && found < 0; base += kWave) {
+    const int i = base + lane;
+    const unsigned long long hit = __ballot(i < a.nseg && seg[i] > thr);
+    if (hit) found = base + __ffsll(hit) - 1;
   }
-  if (threadIdx.x == 0) {
+  int t = -1;
+  if (found >= 0) {
+    float rv[kPerLane];
+#pragma unroll
+    for (int e = 0; e < kPerLane; ++e) {
+      const int v = found * kSeg + e * kWave + lane;
+      rv[e] = v < a.V ? r_of(a, xrow, qrow, lse, residual, v) : 0.f;
+    }
+    double c = found > 0 ? seg[found - 1] : 0.0;
+    int last_pos = -1;
+#pragma unroll
+    for (int e = 0; e < kPerLane; ++e) {
+      const int v = found * kSeg + e * kWave + lane;
+      const double r = (double)rv[e];
+      const double cum = wave_inclusive_scan_f64(r) + c;
+      const unsigned long long hit = __ballot(v < a.V && r > 0.0 && cum > thr);
+      if (hit && t < 0) t = found * kSeg + e * kWave + __ffsll(hit) - 1;
+      const unsigned long long pos = __ballot(v < a.V && r > 0.0);
+      if (pos) last_pos = found * kSeg + e * kWave + 63 - __clzll(pos);
+      c = __shfl(cum, 63);
+    }
+    if (t < 0) t = last_pos;  // rounding put u * Z past this segment's own scan
+  }
+  if (t < 0) {
+    // No prefix sum exceeds u * Z: the largest token with mass.
+    for (int sg = a.nseg - 1; sg >= 0 && t < 0; --sg) {
+      for (int e = kPerLane - 1; e >= 0 && t < 0; --e) {
+        const int v = sg * kSeg + e * kWave + lane;
+        const unsigned long long pos = __ballot(v < a.V && r_of(a, xrow, qrow, lse, residual, v) > 0.f);
+        if (pos) t = sg * kSeg + e * kWave + 63 - __clzll(pos);
+      }
+    }
+    if (t < 0) t = 0;  // no mass at all (non-finite input)
+  }
+
+  if (lane < G) {
+    int32_t v = -1;
+    if (lane < l) v = a.draft[(int64_t)req * a.gamma + lane];
+    else if (lane == l) v = t;
+    out_tok[(int64_t)req * G + lane] = v;
+  }
+  if (lane == 0) {
     accept_len[req] = l;
-    if (new_kv_len != nullptr && bt.has_kv_len) new_kv_len[req] = bt.kv_len[b] - gamma + l;
+    if (new_kv_len != nullptr && bt.has_kv_len) new_kv_len[req] = bt.kv_len[b] - a.gamma + l;
   }
 }
 
 }  // namespace
 
-hipError_t launch_accept(int gamma, int V, const AcceptBatch& bt, const float* x, const float* row_lse,
-                         const float* q_draft, const int32_t* draft_tok, const float* u,
-                         int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len, hipStream_t stream) {
+size_t accept_workspace_bytes(int B, int V) {
+  const int nseg = (V + kSeg - 1) / kSeg;
+  return sizeof(double) * static_cast<size_t>(B) * nseg + sizeof(int32_t) * static_cast<size_t>(B) + 512;
+}
+
+hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
+                         const float2* partials, int ntiles, const float* q_draft, const int32_t* draft_tok,
+                         const float* u, void* ws, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
+                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (bt.nreq <= 0) return hipSuccess;
-  hipLaunchKernelGGL(accept_kernel, dim3(bt.nreq), dim3(kAccThreads), 0, stream, gamma, V, bt, x, row_lse,
-                     q_draft, draft_tok, u, accept_len, out_tok, new_kv_len);
+  AcceptArgs a;
+  a.gamma = gamma;
+  a.V = V;
+  a.nseg = (V + kSeg - 1) / kSeg;
+  a.x = x;
+  a.lse = row_lse;
+  a.q = q_draft;
+  a.draft = draft_tok;
+  a.u = u;
+  a.segsum = static_cast<double*>(ws);
+  a.acc_ws = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + sizeof(double) * static_cast<size_t>(B) * a.nseg);
+  hipLaunchKernelGGL(accept_prepare_kernel, dim3(bt.nreq), dim3(256), 0, stream, a, bt.req0, partials, ntiles);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipExtLaunchKernelGGL(accept_segments_kernel, dim3(a.nseg, bt.nreq), dim3(kWave), 0, stream, ev_start, ev_stop,
+                        0, a, bt.req0);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(accept_finalize_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, a, bt, accept_len, out_tok,
+                     new_kv_len);
   return hipGetLastError();
 }
 

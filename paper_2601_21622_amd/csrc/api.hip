@@ -6,7 +6,7 @@
 
 #include <algorithm>
 
-#include "../../include/sdverify.h"
+#include "sdverify.h"
 #include "launch.h"
 
 namespace {
@@ -87,7 +87,8 @@ int hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
 // Enqueue attention (partials + combine) for all requests, in launches of at
 // most kMaxReqPerLaunch requests whose tables ride in the kernel arguments.
 int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* v, const int64_t* kv_off,
-                  const int32_t* kv_len, float scale, void* out, void* ws, hipStream_t stream) {
+                  const int32_t* kv_len, float scale, void* out, void* ws, hipStream_t stream,
+                  hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
   const AttnShape s = attn_shape(d, scale);
   const int64_t chunks = total_chunks(kv_len, d->batch, s.chunk_keys);
   const AttnPartials parts = attn_carve(ws, chunks, s.Hkv, s.rows, s.D);
@@ -106,7 +107,9 @@ int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* 
       acc += (kv_len[r0 + i] + s.chunk_keys - 1) / s.chunk_keys;
     }
     bt.chunk_prefix[bt.nreq] = acc;
-    hipError_t e = launch_attention(d->dtype, s, bt, acc, q, k, v, parts, stream);
+    const bool first = r0 == 0, last = r0 + kMaxReqPerLaunch >= d->batch;
+    hipError_t e = launch_attention(d->dtype, s, bt, acc, q, k, v, parts, stream, first ? ev_start : nullptr,
+                                    last ? ev_stop : nullptr);
     if (e == hipSuccess) e = launch_attention_combine(d->dtype, s, bt, parts, out, stream);
     if (e != hipSuccess) return SD_ERR_HIP;
     chunk_base += acc;
@@ -115,17 +118,21 @@ int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* 
 }
 
 int run_logits(const sd_dims_t* d, const void* hidden, const void* w, float* logits, float* row_lse, void* ws,
-               hipStream_t stream) {
+               hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
   const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab);
   float2* partials = static_cast<float2*>(ws);
-  hipError_t e = launch_vocab(d->dtype, p, hidden, w, logits, partials, stream);
+  hipError_t e = launch_vocab(d->dtype, p, hidden, w, logits, partials, stream, ev_start, ev_stop);
   if (e == hipSuccess) e = launch_lse_combine(p, partials, row_lse, stream);
   return hip_status(e);
 }
 
-int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const float* q_draft,
-               const int32_t* draft_tok, const float* u, const int32_t* kv_len, int32_t* accept_len,
-               int32_t* out_tok, int32_t* new_kv_len, hipStream_t stream) {
+// x holds logits with row_lse, or probabilities when row_lse is null.
+// With `partials`, row_lse is an output: the log-sum-exp fold runs inside the
+// acceptance stage.
+int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const float2* partials, int ntiles,
+               const float* q_draft, const int32_t* draft_tok, const float* u, const int32_t* kv_len,
+               int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len, void* ws, hipStream_t stream,
+               hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
   for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
     AcceptBatch bt;
     memset(&bt, 0, sizeof(bt));
@@ -134,12 +141,16 @@ int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const f
     bt.has_kv_len = kv_len != nullptr;
     if (kv_len != nullptr)
       for (int i = 0; i < bt.nreq; ++i) bt.kv_len[i] = kv_len[r0 + i];
-    hipError_t e = launch_accept(d->gamma, d->vocab, bt, x, row_lse, q_draft, draft_tok, u, accept_len,
-                                 out_tok, new_kv_len, stream);
+    const bool first = r0 == 0, last = r0 + kMaxReqPerLaunch >= d->batch;
+    hipError_t e = launch_accept(d->gamma, d->vocab, d->batch, bt, x, row_lse, partials, ntiles, q_draft, draft_tok,
+                                 u, ws, accept_len, out_tok, new_kv_len, stream, first ? ev_start : nullptr,
+                                 last ? ev_stop : nullptr);
     if (e != hipSuccess) return SD_ERR_HIP;
   }
   return SD_OK;
 }
+
+size_t accept_ws(const sd_dims_t* d) { return align_up(accept_workspace_bytes(d->batch, d->vocab)); }
 
 int check_accept_args(const float* x, const float* row_lse, const float* q_draft, const int32_t* draft_tok,
                       const float* u, const int32_t* kv_len, const int32_t* accept_len, const int32_t* out_tok,
@@ -160,7 +171,7 @@ size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
   if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
   const AttnShape s = attn_shape(dims, 1.f);
   const int64_t chunks = int64_t(dims->batch) * ((int64_t(max_kv_len) + s.chunk_keys - 1) / s.chunk_keys);
-  return std::max(attention_ws(dims, chunks), logits_ws(dims));
+  return std::max(attention_ws(dims, chunks), logits_ws(dims) + accept_ws(dims));
 }
 
 int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
@@ -198,18 +209,18 @@ int sd_accept_resample(const sd_dims_t* dims, const float* logits_or_probs, cons
                        const float* q_draft, const int32_t* draft_tok, const float* u, const int32_t* kv_len,
                        int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len, void* workspace,
                        size_t workspace_bytes, sd_stream_t stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   int st = check_dims(dims);
   if (st != SD_OK) return st;
   st = check_accept_args(logits_or_probs, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
                          new_kv_len);
   if (st != SD_OK) return st;
+  if (workspace == nullptr || !aligned(workspace, 16)) return SD_ERR_INVALID_ARGUMENT;
   if (kv_len != nullptr)
     for (int b = 0; b < dims->batch; ++b)
       if (kv_len[b] < dims->gamma + 1 || kv_len[b] > kMaxKvLen) return SD_ERR_INVALID_ARGUMENT;
-  return run_accept(dims, logits_or_probs, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
-                    new_kv_len, static_cast<hipStream_t>(stream));
+  if (workspace_bytes < accept_ws(dims)) return SD_ERR_WORKSPACE;
+  return run_accept(dims, logits_or_probs, row_lse, nullptr, 0, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
+                    new_kv_len, workspace, static_cast<hipStream_t>(stream));
 }
 
 int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
@@ -217,7 +228,7 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
                    const void* w_vocab, const float* q_draft, const int32_t* draft_tok, const float* u,
                    void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
                    int32_t* new_kv_len, void* workspace, size_t workspace_bytes, sd_stream_t stream,
-                   void* const* stage_events) {
+                   void* const* kernel_events) {
   int st = check_dims(dims);
   if (st != SD_OK) return st;
   if (!q || !k_pool || !v_pool || !attn_out || !w_vocab || !logits || !row_lse || !workspace)
@@ -234,27 +245,29 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   if (st != SD_OK) return st;
   const AttnShape s = attn_shape(dims, scale);
   const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
-                               logits_ws(dims));
+                               logits_ws(dims) + accept_ws(dims));
   if (workspace_bytes < need) return SD_ERR_WORKSPACE;
 
+  hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  if (kernel_events != nullptr)
+    for (int i = 0; i < 6; ++i) ev[i] = static_cast<hipEvent_t>(kernel_events[i]);
   hipStream_t stm = static_cast<hipStream_t>(stream);
-  auto record = [&](int i) -> bool {
-    if (stage_events == nullptr) return true;
-    return hipEventRecord(static_cast<hipEvent_t>(stage_events[i]), stm) == hipSuccess;
-  };
-  if (!record(0)) return SD_ERR_HIP;
-  st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out, workspace, stm);
+  // Stream order serialises the stages, so they share one workspace: the
+  // attention partials are dead once the combine has run, the vocabulary
+  // statistics once the log-sum-exp combine has run.
+  st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out, workspace, stm, ev[0], ev[1]);
   if (st != SD_OK) return st;
-  if (!record(1)) return SD_ERR_HIP;
-  // The attention partials are dead once the combine has run; the vocabulary
-  // statistics reuse the same workspace (stream order serialises them).
-  st = run_logits(dims, hidden != nullptr ? hidden : attn_out, w_vocab, logits, row_lse, workspace, stm);
-  if (st != SD_OK) return st;
-  if (!record(2)) return SD_ERR_HIP;
-  st = run_accept(dims, logits, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok, new_kv_len, stm);
-  if (st != SD_OK) return st;
-  if (!record(3)) return SD_ERR_HIP;
-  return SD_OK;
+  // The vocabulary statistics live at the start of the workspace and the
+  // acceptance sums after them, since the fold reads the former while the
+  // segment kernel writes the latter.
+  const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab);
+  float2* partials = static_cast<float2*>(workspace);
+  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, partials, stm, ev[2],
+                   ev[3]) != hipSuccess)
+    return SD_ERR_HIP;
+  void* acc_ws = static_cast<char*>(workspace) + logits_ws(dims);
+  return run_accept(dims, logits, row_lse, partials, vp.ntiles, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
+                    new_kv_len, acc_ws, stm, ev[4], ev[5]);
 }
 
 const char* sd_status_string(int status) {

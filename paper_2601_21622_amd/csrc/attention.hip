@@ -16,6 +16,8 @@
 // The four waves then merge their (max, sum, O) through LDS and one partial
 // per workgroup goes to the workspace; a combine kernel merges the chunks of
 // each request in fixed order and writes O in the input dtype.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "launch.h"
 
@@ -26,6 +28,7 @@ namespace {
 constexpr int kAttnThreads = 256;
 constexpr int kAttnWaves = 4;
 constexpr int kTile = 32;
+
 
 __device__ __forceinline__ int find_request(const AttnBatch& bt, int c) {
   int lo = 0, hi = bt.nreq - 1;  // largest b with chunk_prefix[b] <= c
@@ -113,6 +116,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   constexpr int LPR = D / 8;      // lanes per staged V row (16 bytes each)
   constexpr int KPI = 64 / LPR;   // V rows per wave-wide load
 
+  constexpr int NV = kTile / KPI;
   for (int t = wave; t < ntiles; t += kAttnWaves) {
     const int k0 = k_begin + t * kTile;
     // K fragments (A operand): lane holds key k0 + kb*16 + lr; keys past L are clamped and masked.
@@ -123,10 +127,10 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = load_bf16x8(Kb + (int64_t)key * D + ds * 32 + lg * 8);
     }
-    // V rows of the tile, coalesced 16-byte loads, staged row-major in LDS.
-    u32x4 vreg[kTile / KPI];
+    // V rows of the tile, coalesced 16-byte loads, staged row-major in LDS below.
+    u32x4 vreg[NV];
 #pragma unroll
-    for (int it = 0; it < kTile / KPI; ++it) {
+    for (int it = 0; it < NV; ++it) {
       const int key = min(k0 + it * KPI + lane / LPR, L - 1);
       vreg[it] = *reinterpret_cast<const u32x4*>(Vb + (int64_t)key * D + (lane % LPR) * 8);
     }
@@ -143,7 +147,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
       }
 
 #pragma unroll
-    for (int it = 0; it < kTile / KPI; ++it) {
+    for (int it = 0; it < NV; ++it) {
       uint16_t* dst = vst + (it * KPI + lane / LPR) * VS + (lane % LPR) * 8;
       reinterpret_cast<u32x2*>(dst)[0] = u32x2{vreg[it][0], vreg[it][1]};
       reinterpret_cast<u32x2*>(dst)[1] = u32x2{vreg[it][2], vreg[it][3]};
@@ -339,7 +343,9 @@ __device__ __forceinline__ void store_out<uint16_t>(uint16_t* p, float v) {
   *p = __builtin_bit_cast(uint16_t, (__bf16)v);
 }
 
-// Merge the chunk partials of one (request, KV head) in chunk order.
+// Merge the chunk partials of one (request, KV head) in chunk order.  One
+// thread per (row, 4 consecutive d); chunk loads are unrolled so they are in
+// flight together.
 template <typename OutT>
 __global__ __launch_bounds__(kAttnThreads)
 void attn_combine_kernel(const AttnShape s, const AttnBatch bt, AttnPartials parts, OutT* __restrict__ out) {
@@ -348,44 +354,51 @@ void attn_combine_kernel(const AttnShape s, const AttnBatch bt, AttnPartials par
   const int req = bt.req0 + b;
   const int c0 = bt.chunk_base + bt.chunk_prefix[b];
   const int c1 = bt.chunk_base + bt.chunk_prefix[b + 1];
-  for (int i = threadIdx.x; i < s.rows * s.D; i += kAttnThreads) {
-    const int row = i / s.D, d = i - row * s.D;
-    float mx = kNegBig;
-    for (int c = c0; c < c1; ++c) mx = fmaxf(mx, parts.m[((int64_t)c * s.Hkv + g) * s.rows + row]);
-    float den = 0.f, num = 0.f;
-    for (int c = c0; c < c1; ++c) {
-      const int64_t slot = (int64_t)c * s.Hkv + g;
-      const float a = exp2f(parts.m[slot * s.rows + row] - mx);
-      den = fmaf(a, parts.l[slot * s.rows + row], den);
-      num = fmaf(a, parts.o[(slot * s.rows + row) * s.D + d], num);
-    }
-    const int j = row / s.group;
-    const int h = g * s.group + (row - j * s.group);
-    store_out(out + (((int64_t)req * s.G + j) * s.Hq + h) * s.D + d, num / den);
+  const int D4 = s.D / 4;
+  const int i = blockIdx.z * kAttnThreads + threadIdx.x;
+  if (i >= s.rows * D4) return;
+  const int row = i / D4, d = (i - row * D4) * 4;
+  float mx = kNegBig;
+#pragma unroll 8
+  for (int c = c0; c < c1; ++c) mx = fmaxf(mx, parts.m[((int64_t)c * s.Hkv + g) * s.rows + row]);
+  float den = 0.f;
+  f32x4 num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int c = c0; c < c1; ++c) {
+    const int64_t slot = (int64_t)c * s.Hkv + g;
+    const float a = exp2f(parts.m[slot * s.rows + row] - mx);
+    den = fmaf(a, parts.l[slot * s.rows + row], den);
+    const f32x4 o = *reinterpret_cast<const f32x4*>(parts.o + (slot * s.rows + row) * s.D + d);
+    num += a * o;
   }
+  const int j = row / s.group;
+  const int h = g * s.group + (row - j * s.group);
+  OutT* dst = out + (((int64_t)req * s.G + j) * s.Hq + h) * s.D + d;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) store_out(dst + e, num[e] / den);
 }
 
 template <int RB, int D>
-hipError_t launch_bf16(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q,
-                       const void* k, const void* v, AttnPartials parts, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_bf16_kernel<RB, D>), dim3(nchunks, s.Hkv), dim3(kAttnThreads), 0, stream, s, bt,
-                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                     static_cast<const uint16_t*>(v), parts);
+hipError_t launch_bf16(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
+                       const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  hipExtLaunchKernelGGL((attn_bf16_kernel<RB, D>), dim3(nchunks, s.Hkv), dim3(kAttnThreads), 0, stream, e0, e1, 0,
+                        s, bt, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                        static_cast<const uint16_t*>(v), parts);
   return hipGetLastError();
 }
 
 template <int D>
-hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q,
-                       const void* k, const void* v, AttnPartials parts, hipStream_t stream) {
+hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
+                       const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   switch (rb) {
-    case 1: return launch_bf16<1, D>(s, bt, nchunks, q, k, v, parts, stream);
-    case 2: return launch_bf16<2, D>(s, bt, nchunks, q, k, v, parts, stream);
-    case 3: return launch_bf16<3, D>(s, bt, nchunks, q, k, v, parts, stream);
-    case 4: return launch_bf16<4, D>(s, bt, nchunks, q, k, v, parts, stream);
-    case 5: return launch_bf16<5, D>(s, bt, nchunks, q, k, v, parts, stream);
-    case 6: return launch_bf16<6, D>(s, bt, nchunks, q, k, v, parts, stream);
-    case 7: return launch_bf16<7, D>(s, bt, nchunks, q, k, v, parts, stream);
-    case 8: return launch_bf16<8, D>(s, bt, nchunks, q, k, v, parts, stream);
+    case 1: return launch_bf16<1, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 2: return launch_bf16<2, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 3: return launch_bf16<3, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 4: return launch_bf16<4, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 5: return launch_bf16<5, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 6: return launch_bf16<6, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 7: return launch_bf16<7, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 8: return launch_bf16<8, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
@@ -418,30 +431,31 @@ AttnPartials attn_carve(void* ws, int64_t total_chunks, int Hkv, int rows, int D
 
 hipError_t launch_attention(int dtype, const AttnShape& s, const AttnBatch& bt, int nchunks,
                             const void* q, const void* k, const void* v, AttnPartials parts,
-                            hipStream_t stream) {
+                            hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   if (nchunks <= 0) return hipSuccess;
   if (dtype == 0) {
     const size_t shm = sizeof(float) * static_cast<size_t>(s.rows) * (s.D + s.chunk_keys);
-    hipLaunchKernelGGL(attn_f32_kernel, dim3(nchunks, s.Hkv), dim3(kAttnThreads), shm, stream, s, bt,
-                       static_cast<const float*>(q), static_cast<const float*>(k),
-                       static_cast<const float*>(v), parts);
+    hipExtLaunchKernelGGL(attn_f32_kernel, dim3(nchunks, s.Hkv), dim3(kAttnThreads), shm, stream, e0, e1, 0, s, bt,
+                          static_cast<const float*>(q), static_cast<const float*>(k),
+                          static_cast<const float*>(v), parts);
     return hipGetLastError();
   }
   const int rb = (s.rows + 15) / 16;
-  if (s.D == 128) return dispatch_rb<128>(rb, s, bt, nchunks, q, k, v, parts, stream);
-  if (s.D == 64) return dispatch_rb<64>(rb, s, bt, nchunks, q, k, v, parts, stream);
+  if (s.D == 128) return dispatch_rb<128>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+  if (s.D == 64) return dispatch_rb<64>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_attention_combine(int dtype, const AttnShape& s, const AttnBatch& bt,
                                     AttnPartials parts, void* out, hipStream_t stream) {
   if (bt.nreq <= 0) return hipSuccess;
+  const dim3 grid(bt.nreq, s.Hkv, (s.rows * (s.D / 4) + kAttnThreads - 1) / kAttnThreads);
   if (dtype == 0)
-    hipLaunchKernelGGL(attn_combine_kernel<float>, dim3(bt.nreq, s.Hkv), dim3(kAttnThreads), 0, stream, s,
-                       bt, parts, static_cast<float*>(out));
+    hipLaunchKernelGGL(attn_combine_kernel<float>, grid, dim3(kAttnThreads), 0, stream, s, bt, parts,
+                       static_cast<float*>(out));
   else
-    hipLaunchKernelGGL(attn_combine_kernel<uint16_t>, dim3(bt.nreq, s.Hkv), dim3(kAttnThreads), 0, stream,
-                       s, bt, parts, static_cast<uint16_t*>(out));
+    hipLaunchKernelGGL(attn_combine_kernel<uint16_t>, grid, dim3(kAttnThreads), 0, stream, s, bt, parts,
+                       static_cast<uint16_t*>(out));
   return hipGetLastError();
 }
 

@@ -43,7 +43,8 @@ AttnPartials attn_carve(void* ws, int64_t total_chunks, int Hkv, int rows, int D
 
 hipError_t launch_attention(int dtype, const AttnShape& s, const AttnBatch& batch, int nchunks,
                             const void* q, const void* k_pool, const void* v_pool,
-                            AttnPartials parts, hipStream_t stream);
+                            AttnPartials parts, hipStream_t stream, hipEvent_t ev_start,
+                            hipEvent_t ev_stop);
 hipError_t launch_attention_combine(int dtype, const AttnShape& s, const AttnBatch& batch,
                                     AttnPartials parts, void* out, hipStream_t stream);
 
@@ -56,7 +57,8 @@ struct VocabPlan {
 VocabPlan vocab_plan(int dtype, int M, int K, int V);
 size_t vocab_partial_bytes(const VocabPlan& p);
 hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w,
-                        float* logits, float2* partials, hipStream_t stream);
+                        float* logits, float2* partials, hipStream_t stream, hipEvent_t ev_start,
+                        hipEvent_t ev_stop);
 hipError_t launch_lse_combine(const VocabPlan& p, const float2* partials, float* row_lse,
                               hipStream_t stream);
 
@@ -67,9 +69,16 @@ struct AcceptBatch {
   int32_t has_kv_len;
   int32_t kv_len[kMaxReqPerLaunch];
 };
-hipError_t launch_accept(int gamma, int V, const AcceptBatch& batch, const float* x,
-                         const float* row_lse, const float* q_draft, const int32_t* draft_tok,
-                         const float* u, int32_t* accept_len, int32_t* out_tok,
-                         int32_t* new_kv_len, hipStream_t stream);
+size_t accept_workspace_bytes(int B, int V);
+// x: logits with row_lse, or probabilities when row_lse is null.  With
+// `partials` (the vocabulary kernel's per-tile statistics, ntiles per row) the
+// row log-sum-exp is folded first and written to row_lse.  ws holds
+// accept_workspace_bytes(B, V).  ev_start/ev_stop (may be null) time the
+// segment-sum kernel.
+hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& batch, const float* x,
+                         const float* row_lse, const float2* partials, int ntiles,
+                         const float* q_draft, const int32_t* draft_tok, const float* u, void* ws,
+                         int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
+                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop);
 
 }  // namespace sdv

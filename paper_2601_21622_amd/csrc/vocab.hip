@@ -13,6 +13,8 @@
 // writes the float32 logits and, per (row, tile), the tile maximum and the sum
 // of exp(logit - maximum); a second kernel combines the tiles of each row in
 // fixed order into the row's log-sum-exp.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "launch.h"
 
@@ -227,22 +229,16 @@ void lse_combine_kernel(int M, int ntiles, const float2* __restrict__ partials, 
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= M) return;
-  const float2* p = partials + (int64_t)row * ntiles;
-  float mx = -INFINITY;
-  for (int t = lane; t < ntiles; t += kWave) mx = fmaxf(mx, p[t].x);
-  mx = wave_max(mx);
-  double s = 0.0;
-  for (int t = lane; t < ntiles; t += kWave) s += (double)p[t].y * exp((double)p[t].x - (double)mx);
-  s = wave_sum_f64(s);
-  if (lane == 0) row_lse[row] = (float)((double)mx + log(s));
+  const float v = row_lse_from_partials(partials + (int64_t)row * ntiles, ntiles);
+  if (lane == 0) row_lse[row] = v;
 }
 
 template <int MB, int KC>
 hipError_t launch_mb_kc(const VocabPlan& p, int mtiles, const void* hidden, const void* w, float* logits,
-                        float2* partials, hipStream_t stream) {
-  hipLaunchKernelGGL((vocab_bf16_kernel<MB, KC>), dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, p.M,
-                     p.K, p.V, p.ntiles, static_cast<const uint16_t*>(hidden),
-                     static_cast<const uint16_t*>(w), logits, partials);
+                        float2* partials, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC>), dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, e0, e1, 0,
+                        p.M, p.K, p.V, p.ntiles, static_cast<const uint16_t*>(hidden),
+                        static_cast<const uint16_t*>(w), logits, partials);
   return hipGetLastError();
 }
 
@@ -250,10 +246,10 @@ hipError_t launch_mb_kc(const VocabPlan& p, int mtiles, const void* hidden, cons
 // 32 (one MFMA step) whenever K is not a multiple of the preferred chunk.
 template <int MB>
 hipError_t launch_mb(const VocabPlan& p, int mtiles, const void* hidden, const void* w, float* logits,
-                     float2* partials, hipStream_t stream) {
+                     float2* partials, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   constexpr int KC = MB <= 4 ? 256 : (MB <= 8 ? 128 : (MB <= 16 ? 64 : 32));
-  if (p.K % KC == 0) return launch_mb_kc<MB, KC>(p, mtiles, hidden, w, logits, partials, stream);
-  if (p.K % 32 == 0) return launch_mb_kc<MB, 32>(p, mtiles, hidden, w, logits, partials, stream);
+  if (p.K % KC == 0) return launch_mb_kc<MB, KC>(p, mtiles, hidden, w, logits, partials, stream, e0, e1);
+  if (p.K % 32 == 0) return launch_mb_kc<MB, 32>(p, mtiles, hidden, w, logits, partials, stream, e0, e1);
   return hipErrorInvalidValue;
 }
 
@@ -275,21 +271,21 @@ size_t vocab_partial_bytes(const VocabPlan& p) {
 }
 
 hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w, float* logits,
-                        float2* partials, hipStream_t stream) {
+                        float2* partials, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   if (dtype == 0) {
     const int mtiles = (p.M + 63) / 64;
-    hipLaunchKernelGGL(vocab_f32_kernel, dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, p.M, p.K, p.V,
-                       p.ntiles, static_cast<const float*>(hidden), static_cast<const float*>(w), logits,
-                       partials);
+    hipExtLaunchKernelGGL(vocab_f32_kernel, dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, e0, e1, 0, p.M, p.K,
+                          p.V, p.ntiles, static_cast<const float*>(hidden), static_cast<const float*>(w), logits,
+                          partials);
     return hipGetLastError();
   }
+  const int blocks = (p.M + 15) / 16;
   // Rows per M-tile: up to 20 blocks of 16 (320 rows) so that W is streamed
   // once for every pooled batch up to that size.
-  const int blocks = (p.M + 15) / 16;
   const int mtiles = (blocks + 19) / 20;
   const int mb = (blocks + mtiles - 1) / mtiles;
   switch (mb) {
-#define SDV_MB(n) case n: return launch_mb<n>(p, mtiles, hidden, w, logits, partials, stream);
+#define SDV_MB(n) case n: return launch_mb<n>(p, mtiles, hidden, w, logits, partials, stream, e0, e1);
     SDV_MB(1) SDV_MB(2) SDV_MB(3) SDV_MB(4) SDV_MB(5) SDV_MB(6) SDV_MB(7) SDV_MB(8) SDV_MB(9) SDV_MB(10)
     SDV_MB(11) SDV_MB(12) SDV_MB(13) SDV_MB(14) SDV_MB(15) SDV_MB(16) SDV_MB(17) SDV_MB(18) SDV_MB(19)
     SDV_MB(20)

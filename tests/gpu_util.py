@@ -69,13 +69,13 @@ class DeviceBatch:
         x = self.logits if probs is None else probs
         l = self.lse if (probs is None and lse == "own") else None
         sd.sd_accept_resample(self.dims, x, l, self.q_draft, self.draft, self.u, self.x.kv_len,
-                              self.accept_len, self.out_tok, self.new_kv_len)
+                              self.accept_len, self.out_tok, self.new_kv_len, self.ws)
 
-    def step(self, use_hidden=True, stage_events=None):
+    def step(self, use_hidden=True, kernel_events=None):
         sd.sd_verify_step(self.dims, self.q, self.k, self.v, self.x.kv_off, self.x.kv_len, self.scale,
                           self.hidden if use_hidden else None, self.w, self.q_draft, self.draft, self.u,
                           self.attn, self.logits, self.lse, self.accept_len, self.out_tok, self.new_kv_len,
-                          self.ws, stage_events=stage_events)
+                          self.ws, kernel_events=kernel_events)
 
 
 def to_np(t: torch.Tensor) -> np.ndarray:

@@ -71,7 +71,8 @@ def _run(logits, lse, q, draft, u, kv_len, probs_mode=False, oracle=True):
     acc = torch.empty((B,), dtype=torch.int32, device="cuda")
     tok = torch.empty((B, G), dtype=torch.int32, device="cuda")
     new = torch.empty((B,), dtype=torch.int32, device="cuda")
-    sd.sd_accept_resample(dims, dx, dl, tensor(q), tensor(draft), tensor(u), kv_len, acc, tok, new)
+    ws = torch.empty((sd.sd_workspace_bytes(dims, int(kv_len.max())),), dtype=torch.uint8, device="cuda")
+    sd.sd_accept_resample(dims, dx, dl, tensor(q), tensor(draft), tensor(u), kv_len, acc, tok, new, ws)
     ref = accept_resample(x, None if probs_mode else lse, q, draft, u, kv_len=kv_len) if oracle else None
     return to_np(acc), to_np(tok), to_np(new), ref
 

@@ -33,10 +33,10 @@ def _check(name, use_hidden):
     announce(f"step parity case={name} use_hidden={use_hidden}")
     x = make_inputs(cfg)
     db = DeviceBatch(x)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-    db.step(use_hidden=use_hidden, stage_events=ev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    db.step(use_hidden=use_hidden, kernel_events=ev)
     torch.cuda.synchronize()
-    assert all(ev[i].elapsed_time(ev[i + 1]) >= 0 for i in range(3))
+    assert all(ev[2 * i].elapsed_time(ev[2 * i + 1]) > 0 for i in range(3))
     rtol = RTOL[cfg.dtype]
     attn_ref = verify_attention(x.f32("q"), x.f32("k_pool"), x.f32("v_pool"), x.kv_off, x.kv_len, cfg.n_kv_heads)
     assert_close_rows(to_np(db.attn), attn_ref, rtol, f"step attention[{name}]")
