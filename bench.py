@@ -97,6 +97,8 @@ def main() -> int:
     ap.add_argument("--workload", default="vicuna7b")
     ap.add_argument("--copies", type=int, default=0, help="input copies to rotate over (0: enough to exceed "
                                                            "4x the Infinity Cache)")
+    ap.add_argument("--vocab-layout", choices=["packed", "row-major"], default="packed",
+                    help="LM-head weight layout: repacked once before timing (sd_pack_vocab), or [V][hidden]")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -121,7 +123,8 @@ def main() -> int:
     B, G, M, V, K = cfg.batch, cfg.positions, cfg.rows, cfg.vocab, cfg.hidden
     log(f"generating workload {cfg.name}")
     x = make_inputs(cfg)
-    dims = sd.Dims.of(cfg)
+    packed = args.vocab_layout == "packed" and cfg.dtype == "bf16"
+    dims = sd.Dims.of(cfg, packed_vocab=packed)
     scale = 1.0 / math.sqrt(cfg.head_dim)
 
     def dev(a):
@@ -135,6 +138,12 @@ def main() -> int:
     ws_bytes = sd.sd_workspace_bytes(dims, int(x.kv_len.max()))
     copies = []
     base = {n: dev(getattr(x, n)) for n in ("q", "k_pool", "v_pool", "hidden", "w", "q_draft", "draft", "u")}
+    if packed:
+        # Weight-load-time repacking of the LM head (not part of a step).
+        wp = torch.empty((sd.sd_vocab_packed_bytes(dims) // 2,), dtype=torch.bfloat16, device="cuda")
+        sd.sd_pack_vocab(dims, base["w"], wp)
+        torch.cuda.synchronize()
+        base["w"] = wp
     for i in range(ncopies):
         t = {n: (a if i == 0 else a.clone()) for n, a in base.items()}
         t["attn"] = torch.empty((B, G, cfg.n_q_heads, cfg.head_dim), dtype=adt, device="cuda")
@@ -241,7 +250,7 @@ def main() -> int:
             "batch": B, "gamma": cfg.gamma, "n_q_heads": cfg.n_q_heads, "n_kv_heads": cfg.n_kv_heads,
             "head_dim": cfg.head_dim, "hidden": K, "vocab": V,
             "kv_len": list(cfg.lengths), "kv_tokens": int(x.kv_len.sum()), "draft": list(cfg.draft),
-            "input_copies": ncopies,
+            "input_copies": ncopies, "vocab_layout": "packed" if packed else "row-major",
         },
         "roofline": roof,
         "scored_tokens_per_s": B * G / (ms_step * 1e-3),

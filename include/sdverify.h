@@ -68,6 +68,12 @@ enum {
   SD_ERR_HIP = -4               /* a HIP launch or runtime call failed */
 };
 
+/* Flags of sd_dims_t.flags. */
+enum {
+  /* w_vocab arguments point to weights repacked by sd_pack_vocab (bf16 only). */
+  SD_FLAG_PACKED_VOCAB = 1
+};
+
 /* Problem shape.  Accumulation is always float32 (float64 for the sampling sums). */
 typedef struct {
   int32_t batch;      /* B >= 1 pooled requests (one per target session) */
@@ -78,6 +84,7 @@ typedef struct {
   int32_t hidden;     /* width of the vocabulary projection's input, a multiple of 32 */
   int32_t vocab;      /* V, 1 .. 2,097,152 */
   int32_t dtype;      /* sd_dtype_t */
+  int32_t flags;      /* bitwise OR of SD_FLAG_*, 0 by default */
 } sd_dims_t;
 
 /*
@@ -105,10 +112,28 @@ SD_API int sd_verify_attention(const sd_dims_t* dims, const void* q, const void*
                         sd_stream_t stream);
 
 /*
+ * Repacked vocabulary weights.  The projection streams W once per step; in
+ * the [V][hidden] layout every MFMA operand load touches 16 rows 2*hidden
+ * bytes apart.  sd_pack_vocab rewrites W once (at weight-load time) into
+ * fragment order, [hidden/32][ceil(V/16)][64 lanes][8 bf16]: fragment (s, n)
+ * holds, for lane l, W[16n + l%16][32s + 8(l/16) .. +8], rows past V zero.
+ * Each operand load is then 1 KB contiguous, and at every k-step the whole
+ * grid reads one contiguous slab.  A w_vocab in this layout is passed with
+ * SD_FLAG_PACKED_VOCAB set in dims->flags.  bf16 only.
+ *   sd_vocab_packed_bytes  bytes of the packed buffer (0 for an invalid or fp32 shape)
+ *   sd_pack_vocab          w_vocab [V][hidden] bf16 (device) -> w_packed (device,
+ *                          sd_vocab_packed_bytes bytes, 16-byte aligned, not
+ *                          overlapping w_vocab); enqueued on `stream`.
+ */
+SD_API size_t sd_vocab_packed_bytes(const sd_dims_t* dims);
+SD_API int sd_pack_vocab(const sd_dims_t* dims, const void* w_vocab, void* w_packed, sd_stream_t stream);
+
+/*
  * Vocabulary projection and row log-sum-exp: the target distributions
  * p_1..p_{gamma+1} of Algorithm 2 (temperature 1).
  *   hidden   [M][hidden] in dtype; row b*G + j feeds p_{j+1} of request b
- *   w_vocab  [V][hidden] in dtype (one row per vocabulary entry)
+ *   w_vocab  [V][hidden] in dtype (one row per vocabulary entry), or the
+ *            sd_pack_vocab layout when dims->flags has SD_FLAG_PACKED_VOCAB
  *   logits   [M][V] float32 output: logits[m][v] = sum_k hidden[m][k] * w_vocab[v][k]
  *   row_lse  [M] float32 output: log sum_v exp(logits[m][v])
  * so that p_{j+1}(v) = exp(logits[b*G+j][v] - row_lse[b*G+j]).

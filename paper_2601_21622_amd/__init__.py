@@ -15,6 +15,7 @@ from ._binding import (  # noqa: F401
     SD_ERR_INVALID_ARGUMENT,
     SD_ERR_UNSUPPORTED,
     SD_ERR_WORKSPACE,
+    SD_FLAG_PACKED_VOCAB,
     SD_OK,
     Dims,
     PreparedCall,
@@ -24,10 +25,12 @@ from ._binding import (  # noqa: F401
     library_path,
     prepare_verify_step,
     sd_accept_resample,
+    sd_pack_vocab,
     sd_status_string,
     sd_verify_attention,
     sd_verify_logits,
     sd_verify_step,
     sd_version,
+    sd_vocab_packed_bytes,
     sd_workspace_bytes,
 )

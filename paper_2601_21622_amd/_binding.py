@@ -16,6 +16,7 @@ _HEADER = os.path.join(os.path.dirname(_HERE), "include", "sdverify.h")
 
 SD_DTYPE_F32 = 0
 SD_DTYPE_BF16 = 1
+SD_FLAG_PACKED_VOCAB = 1
 SD_OK = 0
 SD_ERR_INVALID_ARGUMENT = -1
 SD_ERR_UNSUPPORTED = -2
@@ -39,13 +40,19 @@ class Dims(ctypes.Structure):
         ("hidden", ctypes.c_int32),
         ("vocab", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
+        ("flags", ctypes.c_int32),
     ]
 
     @classmethod
-    def of(cls, cfg) -> "Dims":
+    def of(cls, cfg, packed_vocab: bool = False) -> "Dims":
         """Dims of a workload description (anything with the same attribute names)."""
         return cls(cfg.batch, cfg.gamma, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.hidden,
-                   cfg.vocab, SD_DTYPE_BF16 if cfg.dtype == "bf16" else SD_DTYPE_F32)
+                   cfg.vocab, SD_DTYPE_BF16 if cfg.dtype == "bf16" else SD_DTYPE_F32,
+                   SD_FLAG_PACKED_VOCAB if packed_vocab else 0)
+
+    def with_flags(self, flags: int) -> "Dims":
+        return Dims(self.batch, self.gamma, self.n_q_heads, self.n_kv_heads, self.head_dim, self.hidden,
+                    self.vocab, self.dtype, flags)
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -77,6 +84,10 @@ def library() -> ctypes.CDLL:
     lib.sd_accept_resample.restype = ctypes.c_int
     lib.sd_verify_step.argtypes = [DP, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
     lib.sd_verify_step.restype = ctypes.c_int
+    lib.sd_vocab_packed_bytes.argtypes = [DP]
+    lib.sd_vocab_packed_bytes.restype = SZ
+    lib.sd_pack_vocab.argtypes = [DP, P, P, P]
+    lib.sd_pack_vocab.restype = ctypes.c_int
     lib.sd_status_string.argtypes = [ctypes.c_int]
     lib.sd_status_string.restype = ctypes.c_char_p
     lib.sd_version.argtypes = []
@@ -145,6 +156,15 @@ def _check(status: int, where: str) -> None:
 
 def sd_workspace_bytes(dims: Dims, max_kv_len: int) -> int:
     return int(library().sd_workspace_bytes(ctypes.byref(dims), int(max_kv_len)))
+
+
+def sd_vocab_packed_bytes(dims: Dims) -> int:
+    return int(library().sd_vocab_packed_bytes(ctypes.byref(dims)))
+
+
+def sd_pack_vocab(dims: Dims, w_vocab, w_packed, stream=None) -> None:
+    st = library().sd_pack_vocab(ctypes.byref(dims), _ptr(w_vocab), _ptr(w_packed), _stream(stream))
+    _check(st, "sd_pack_vocab")
 
 
 def sd_verify_attention(dims: Dims, q, k_pool, v_pool, kv_off: Sequence[int], kv_len: Sequence[int],

@@ -47,7 +47,7 @@ struct AcceptArgs {
   const int32_t* draft;  // [B][gamma]
   const float* u;        // [B][G]
   double* segsum;        // [B][nseg]
-  int32_t* acc_ws;       // [B] accept length handed from segments to finalize
+  int2* desc;            // [B] (accept length l, bits of the log-sum-exp of row l) from prepare
 };
 
 __device__ __forceinline__ float r_of(const AcceptArgs& a, const float* xrow, const float* qrow, float lse,
@@ -58,39 +58,32 @@ __device__ __forceinline__ float r_of(const AcceptArgs& a, const float* xrow, co
   return d > 0.f ? d : 0.f;
 }
 
-// Accept length of request `req` given the log-sum-exp of its rows in `lse`
-// (or probabilities when a.lse is null); every lane returns it.
-__device__ __forceinline__ int accept_length(const AcceptArgs& a, int req, const float* lse) {
-  const int lane = threadIdx.x & 63;
-  const int G = a.gamma + 1;
-  bool fail = false;
-  if (lane < a.gamma) {
-    const int tok = a.draft[(int64_t)req * a.gamma + lane];
-    double ratio = 0.0;
-    if (tok >= 0 && tok < a.V) {
-      const int64_t row = (int64_t)req * G + lane;
-      const float xv = a.x[row * a.V + tok];
-      const double px = a.lse != nullptr ? exp((double)xv - (double)lse[lane]) : (double)xv;
-      const double qx = (double)a.q[((int64_t)req * a.gamma + lane) * a.V + tok];
-      ratio = (px <= 0.0) ? 0.0 : (qx <= 0.0 ? (double)INFINITY : px / qx);
-    }
-    fail = !((double)a.u[(int64_t)req * G + lane] < ratio);
-  }
-  const unsigned long long fails = __ballot(fail);
-  return fails ? (__ffsll(fails) - 1) : a.gamma;
-}
-
-// partials != nullptr: fold them into the row log-sum-exp, write it to a.lse
-// (the caller's row_lse output) and use it; otherwise read a.lse if given.
-__global__ __launch_bounds__(256)
+// One workgroup per request.  The ratio-test operands (draft token, its logit
+// or probability, its draft probability, the draw) are gathered first, so
+// their latency overlaps the log-sum-exp fold; with `partials` the fold of the
+// request's rows (one wave per row) writes row_lse; then wave 0 runs the tests
+// in float64 and stores (l, lse of row l) for the next two kernels.
+__global__ __launch_bounds__(512)
 void accept_prepare_kernel(const AcceptArgs a, int req0, const float2* __restrict__ partials, int ntiles) {
   __shared__ float s_lse[kWave];
   const int req = req0 + blockIdx.x;
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int G = a.gamma + 1;
+
+  float xv = 0.f, qv = 0.f, uv = 0.f;
+  bool valid = false;
+  if (wave == 0 && lane < a.gamma) {
+    const int tok = a.draft[(int64_t)req * a.gamma + lane];
+    valid = tok >= 0 && tok < a.V;
+    if (valid) {
+      xv = a.x[((int64_t)req * G + lane) * a.V + tok];
+      qv = a.q[((int64_t)req * a.gamma + lane) * a.V + tok];
+    }
+    uv = a.u[(int64_t)req * G + lane];
+  }
   if (partials != nullptr) {
-    for (int j = wave; j < G; j += 4) {
+    for (int j = wave; j < G; j += 8) {
       const float v = row_lse_from_partials(partials + ((int64_t)req * G + j) * ntiles, ntiles);
       if (lane == 0) {
         s_lse[j] = v;
@@ -102,8 +95,19 @@ void accept_prepare_kernel(const AcceptArgs a, int req0, const float2* __restric
   }
   __syncthreads();
   if (wave == 0) {
-    const int l = accept_length(a, req, s_lse);
-    if (lane == 0) a.acc_ws[req] = l;
+    bool fail = false;
+    if (lane < a.gamma) {
+      double ratio = 0.0;
+      if (valid) {
+        const double px = a.lse != nullptr ? exp((double)xv - (double)s_lse[lane]) : (double)xv;
+        const double qx = (double)qv;
+        ratio = (px <= 0.0) ? 0.0 : (qx <= 0.0 ? (double)INFINITY : px / qx);
+      }
+      fail = !((double)uv < ratio);
+    }
+    const unsigned long long fails = __ballot(fail);
+    const int l = fails ? (__ffsll(fails) - 1) : a.gamma;
+    if (lane == 0) a.desc[req] = make_int2(l, __float_as_int(a.lse != nullptr ? s_lse[l] : 0.f));
   }
 }
 
@@ -113,12 +117,13 @@ void accept_segments_kernel(const AcceptArgs a, int req0) {
   const int req = req0 + blockIdx.y;
   const int lane = threadIdx.x;
   const int G = a.gamma + 1;
-  const int l = a.acc_ws[req];
+  const int2 d = a.desc[req];
+  const int l = d.x;
+  const float lse = __int_as_float(d.y);
   const bool residual = l < a.gamma;
   const int64_t row = (int64_t)req * G + l;
   const float* xrow = a.x + row * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
-  const float lse = a.lse != nullptr ? a.lse[row] : 0.f;
   float r[kPerLane];
 #pragma unroll
   for (int e = 0; e < kPerLane; ++e) {
@@ -151,14 +156,15 @@ void accept_finalize_kernel(const AcceptArgs a, const AcceptBatch bt, int32_t* _
   const int req = bt.req0 + b;
   const int lane = threadIdx.x;
   const int G = a.gamma + 1;
-  const int l = a.acc_ws[req];
+  __shared__ double seg[kMaxSeg];
+  for (int i = lane; i < a.nseg; i += kWave) seg[i] = a.segsum[(int64_t)req * a.nseg + i];
+  const int2 d = a.desc[req];
+  const int l = d.x;
+  const float lse = __int_as_float(d.y);
   bool residual = l < a.gamma;
   const int64_t row = (int64_t)req * G + l;
   const float* xrow = a.x + row * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
-  const float lse = a.lse != nullptr ? a.lse[row] : 0.f;
-  __shared__ double seg[kMaxSeg];
-  for (int i = lane; i < a.nseg; i += kWave) seg[i] = a.segsum[(int64_t)req * a.nseg + i];
   lds_wait();
 
   // Inclusive prefix of the segment totals, in place (LDS, one wave).
@@ -244,7 +250,7 @@ void accept_finalize_kernel(const AcceptArgs a, const AcceptBatch bt, int32_t* _
 
 size_t accept_workspace_bytes(int B, int V) {
   const int nseg = (V + kSeg - 1) / kSeg;
-  return sizeof(double) * static_cast<size_t>(B) * nseg + sizeof(int32_t) * static_cast<size_t>(B) + 512;
+  return sizeof(double) * static_cast<size_t>(B) * nseg + sizeof(int2) * static_cast<size_t>(B) + 512;
 }
 
 hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
@@ -262,8 +268,8 @@ hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const f
   a.draft = draft_tok;
   a.u = u;
   a.segsum = static_cast<double*>(ws);
-  a.acc_ws = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + sizeof(double) * static_cast<size_t>(B) * a.nseg);
-  hipLaunchKernelGGL(accept_prepare_kernel, dim3(bt.nreq), dim3(256), 0, stream, a, bt.req0, partials, ntiles);
+  a.desc = reinterpret_cast<int2*>(static_cast<char*>(ws) + sizeof(double) * static_cast<size_t>(B) * a.nseg);
+  hipLaunchKernelGGL(accept_prepare_kernel, dim3(bt.nreq), dim3(512), 0, stream, a, bt.req0, partials, ntiles);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(accept_segments_kernel, dim3(a.nseg, bt.nreq), dim3(kWave), 0, stream, ev_start, ev_stop,

@@ -39,6 +39,8 @@ int check_dims(const sd_dims_t* d) {
   const int64_t rows = int64_t(d->gamma + 1) * (d->n_q_heads / d->n_kv_heads);
   if (rows > (d->dtype == SD_DTYPE_F32 ? kMaxRowsF32 : kMaxRows)) return SD_ERR_UNSUPPORTED;
   if (int64_t(d->batch) * (d->gamma + 1) > (int64_t(1) << 24)) return SD_ERR_UNSUPPORTED;
+  if ((d->flags & ~SD_FLAG_PACKED_VOCAB) != 0) return SD_ERR_INVALID_ARGUMENT;
+  if ((d->flags & SD_FLAG_PACKED_VOCAB) && d->dtype != SD_DTYPE_BF16) return SD_ERR_UNSUPPORTED;
   return SD_OK;
 }
 
@@ -67,7 +69,7 @@ size_t attention_ws(const sd_dims_t* d, int64_t chunks) {
 }
 
 size_t logits_ws(const sd_dims_t* d) {
-  const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab);
+  const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab, (d->flags & SD_FLAG_PACKED_VOCAB) != 0);
   return align_up(vocab_partial_bytes(p));
 }
 
@@ -119,7 +121,7 @@ int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* 
 
 int run_logits(const sd_dims_t* d, const void* hidden, const void* w, float* logits, float* row_lse, void* ws,
                hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
-  const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab);
+  const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab, (d->flags & SD_FLAG_PACKED_VOCAB) != 0);
   float2* partials = static_cast<float2*>(ws);
   hipError_t e = launch_vocab(d->dtype, p, hidden, w, logits, partials, stream, ev_start, ev_stop);
   if (e == hipSuccess) e = launch_lse_combine(p, partials, row_lse, stream);
@@ -260,7 +262,7 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   // The vocabulary statistics live at the start of the workspace and the
   // acceptance sums after them, since the fold reads the former while the
   // segment kernel writes the latter.
-  const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab);
+  const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab, (dims->flags & SD_FLAG_PACKED_VOCAB) != 0);
   float2* partials = static_cast<float2*>(workspace);
   if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, partials, stm, ev[2],
                    ev[3]) != hipSuccess)
@@ -268,6 +270,24 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   void* acc_ws = static_cast<char*>(workspace) + logits_ws(dims);
   return run_accept(dims, logits, row_lse, partials, vp.ntiles, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
                     new_kv_len, acc_ws, stm, ev[4], ev[5]);
+}
+
+size_t sd_vocab_packed_bytes(const sd_dims_t* dims) {
+  if (check_dims(dims) != SD_OK || dims->dtype != SD_DTYPE_BF16) return 0;
+  return vocab_packed_bytes(dims->hidden, dims->vocab);
+}
+
+int sd_pack_vocab(const sd_dims_t* dims, const void* w_vocab, void* w_packed, sd_stream_t stream) {
+  const int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (dims->dtype != SD_DTYPE_BF16) return SD_ERR_UNSUPPORTED;
+  if (!w_vocab || !w_packed || !aligned(w_vocab, 16) || !aligned(w_packed, 16)) return SD_ERR_INVALID_ARGUMENT;
+  const char* a = static_cast<const char*>(w_vocab);
+  const char* b = static_cast<const char*>(w_packed);
+  const size_t na = sizeof(uint16_t) * static_cast<size_t>(dims->vocab) * dims->hidden;
+  const size_t nb = vocab_packed_bytes(dims->hidden, dims->vocab);
+  if (a < b + nb && b < a + na) return SD_ERR_INVALID_ARGUMENT;  // overlapping buffers
+  return hip_status(launch_pack_vocab(dims->hidden, dims->vocab, w_vocab, w_packed, static_cast<hipStream_t>(stream)));
 }
 
 const char* sd_status_string(int status) {

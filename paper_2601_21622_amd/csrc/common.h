@@ -82,38 +82,36 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // Row log-sum-exp from per-tile (maximum, sum of exp(x - maximum)) pairs, one
-// wave: each lane folds its tiles (lane, lane + 64, ...) into a running
-// (maximum, float64 sum), eight loads in flight at a time, then the lanes are
-// folded by a butterfly.  The order is fixed, so the result is deterministic;
-// lane 0's value is broadcast so every lane returns the same bits.
-__device__ __forceinline__ void lse_fold(float& m, double& s, float mt, double st) {
-  if (!(mt > -INFINITY)) return;
-  const float mn = fmaxf(m, mt);
-  s = s * exp((double)m - (double)mn) + st * exp((double)mt - (double)mn);
-  m = mn;
-}
-
+// wave, two passes over registers: the row maximum m, then
+// sum_t S_t * exp(M_t - m) accumulated in float64, lse = m + log(sum).  Each
+// lane holds tiles lane, lane + 64, ...; the lane sums are added by a fixed
+// butterfly and lane 0's value is broadcast, so the result is deterministic
+// and every lane returns the same bits.
 __device__ __forceinline__ float row_lse_from_partials(const float2* p, int ntiles) {
   const int lane = threadIdx.x & 63;
-  float m = -INFINITY;
-  double s = 0.0;
-  for (int base = 0; base < ntiles; base += 8 * kWave) {
-    float2 v[8];
+  constexpr int kR = 8;  // tiles per lane held in registers per round
+  float mx = -INFINITY;
+  for (int base = 0; base < ntiles; base += kR * kWave) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < kR; ++j) {
+      const int t = base + j * kWave + lane;
+      if (t < ntiles) mx = fmaxf(mx, p[t].x);
+    }
+  }
+  mx = wave_max(mx);
+  double s = 0.0;
+  for (int base = 0; base < ntiles; base += kR * kWave) {
+    float2 v[kR];
+#pragma unroll
+    for (int j = 0; j < kR; ++j) {
       const int t = base + j * kWave + lane;
       v[j] = t < ntiles ? p[t] : make_float2(-INFINITY, 0.f);
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) lse_fold(m, s, v[j].x, (double)v[j].y);
+    for (int j = 0; j < kR; ++j) s += (double)v[j].y * (double)expf(v[j].x - mx);
   }
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const float mo = __shfl_xor(m, o);
-    const double so = __shfl_xor(s, o);
-    lse_fold(m, s, mo, so);
-  }
-  const float r = (float)((double)m + log(s));
+  s = wave_sum_f64(s);
+  const float r = (float)((double)mx + log(s));
   return __shfl(r, 0);
 }
 

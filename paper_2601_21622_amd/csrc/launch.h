@@ -53,8 +53,11 @@ struct VocabPlan {
   int M, K, V;
   int tile_n;      // vocabulary columns per workgroup
   int ntiles;      // ceil(V / tile_n)
+  bool packed;     // W in the fragment-order layout of launch_pack_vocab
 };
-VocabPlan vocab_plan(int dtype, int M, int K, int V);
+VocabPlan vocab_plan(int dtype, int M, int K, int V, bool packed);
+size_t vocab_packed_bytes(int K, int V);
+hipError_t launch_pack_vocab(int K, int V, const void* w, void* out, hipStream_t stream);
 size_t vocab_partial_bytes(const VocabPlan& p);
 hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w,
                         float* logits, float2* partials, hipStream_t stream, hipEvent_t ev_start,

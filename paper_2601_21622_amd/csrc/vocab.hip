@@ -15,6 +15,8 @@
 // fixed order into the row's log-sum-exp.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "launch.h"
 
@@ -34,7 +36,7 @@ struct VocabCfg {
   static constexpr int kPiecesPerThread = (kPieces + kVThreads - 1) / kVThreads;
 };
 
-template <int MB, int KC>
+template <int MB, int KC, bool PACKED>
 __global__ __launch_bounds__(kVThreads)
 void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restrict__ hidden,
                        const uint16_t* __restrict__ w, float* __restrict__ logits,
@@ -49,8 +51,19 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15;
   const int lg = lane >> 4;
-  const int nrow = min(V - 1, tile * kTileN + wave * 16 + lr);  // clamped; masked in the epilogue
-  const uint16_t* wrow = w + (int64_t)nrow * K + lg * 8;
+  // W fragment stream of this wave: 16 vocabulary rows (clamped; masked in the
+  // epilogue).  Row-major: the lane's row from column lg*8.  Packed: fragment
+  // (k-step s, block) at ((s * nblk + block) * 64 + lane) * 8.
+  const int nblk = (V + 15) / 16;
+  const uint16_t* wrow;
+  int64_t wstep;  // elements between consecutive k-steps
+  if (PACKED) {
+    wrow = w + ((int64_t)min(nblk - 1, tile * 4 + wave) * 64 + lane) * 8;
+    wstep = (int64_t)nblk * 64 * 8;
+  } else {
+    wrow = w + (int64_t)min(V - 1, tile * kTileN + wave * 16 + lr) * K + lg * 8;
+    wstep = 32;
+  }
   const int nchunks = K / KC;
 
   // Cooperative A-chunk load: piece p -> (row, 16-byte k piece), coalesced along k.
@@ -84,7 +97,7 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
   bf16x8 wcur[C::kSteps], wnext[C::kSteps];
   auto load_w = [&](bf16x8* dst, int kc) {
 #pragma unroll
-    for (int ks = 0; ks < C::kSteps; ++ks) dst[ks] = load_bf16x8(wrow + kc * KC + ks * 32);
+    for (int ks = 0; ks < C::kSteps; ++ks) dst[ks] = load_bf16x8(wrow + (int64_t)(kc * C::kSteps + ks) * wstep);
   };
 
   f32x4 acc[MB];
@@ -233,12 +246,35 @@ void lse_combine_kernel(int M, int ntiles, const float2* __restrict__ partials, 
   if (lane == 0) row_lse[row] = v;
 }
 
+// Repack W [V][K] into fragment order [K/32][ceil(V/16)][64][8]: one thread
+// per 16-byte piece, writes coalesced; rows past V are zero.
+__global__ __launch_bounds__(kVThreads)
+void pack_vocab_kernel(int K, int V, const uint16_t* __restrict__ w, uint16_t* __restrict__ out) {
+  const int nblk = (V + 15) / 16;
+  const int64_t pieces = (int64_t)(K / 32) * nblk * 64;
+  for (int64_t i = (int64_t)blockIdx.x * kVThreads + threadIdx.x; i < pieces; i += (int64_t)gridDim.x * kVThreads) {
+    const int lane = (int)(i & 63);
+    const int64_t f = i >> 6;
+    const int blk = (int)(f % nblk);
+    const int s = (int)(f / nblk);
+    const int row = blk * 16 + (lane & 15);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row < V) v = *reinterpret_cast<const u32x4*>(w + (int64_t)row * K + s * 32 + (lane >> 4) * 8);
+    *reinterpret_cast<u32x4*>(out + i * 8) = v;
+  }
+}
+
 template <int MB, int KC>
 hipError_t launch_mb_kc(const VocabPlan& p, int mtiles, const void* hidden, const void* w, float* logits,
                         float2* partials, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC>), dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, e0, e1, 0,
-                        p.M, p.K, p.V, p.ntiles, static_cast<const uint16_t*>(hidden),
-                        static_cast<const uint16_t*>(w), logits, partials);
+  if (p.packed)
+    hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC, true>), dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, e0,
+                          e1, 0, p.M, p.K, p.V, p.ntiles, static_cast<const uint16_t*>(hidden),
+                          static_cast<const uint16_t*>(w), logits, partials);
+  else
+    hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC, false>), dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, e0,
+                          e1, 0, p.M, p.K, p.V, p.ntiles, static_cast<const uint16_t*>(hidden),
+                          static_cast<const uint16_t*>(w), logits, partials);
   return hipGetLastError();
 }
 
@@ -255,9 +291,22 @@ hipError_t launch_mb(const VocabPlan& p, int mtiles, const void* hidden, const v
 
 }  // namespace
 
-VocabPlan vocab_plan(int dtype, int M, int K, int V) {
+size_t vocab_packed_bytes(int K, int V) {
+  return sizeof(uint16_t) * static_cast<size_t>(K) * ((static_cast<size_t>(V) + 15) / 16) * 16;
+}
+
+hipError_t launch_pack_vocab(int K, int V, const void* w, void* out, hipStream_t stream) {
+  const int64_t pieces = (int64_t)(K / 32) * ((V + 15) / 16) * 64;
+  const int64_t blocks = std::min<int64_t>((pieces + kVThreads - 1) / kVThreads, 65536);
+  hipLaunchKernelGGL(pack_vocab_kernel, dim3((unsigned)blocks), dim3(kVThreads), 0, stream, K, V,
+                     static_cast<const uint16_t*>(w), static_cast<uint16_t*>(out));
+  return hipGetLastError();
+}
+
+VocabPlan vocab_plan(int dtype, int M, int K, int V, bool packed) {
   (void)dtype;
   VocabPlan p;
+  p.packed = packed;
   p.M = M;
   p.K = K;
   p.V = V;

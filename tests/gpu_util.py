@@ -31,17 +31,21 @@ def tensor(a: np.ndarray, dev="cuda"):
 class DeviceBatch:
     """Device copies of a VerifyInputs plus output buffers and the workspace."""
 
-    def __init__(self, x, dev="cuda"):
+    def __init__(self, x, dev="cuda", packed_vocab=False):
         c = x.cfg
         self.x = x
         self.cfg = c
-        self.dims = sd.Dims.of(c)
+        self.dims = sd.Dims.of(c, packed_vocab=packed_vocab)
         B, G, M, V = c.batch, c.positions, c.rows, c.vocab
         self.q = tensor(x.q, dev)
         self.k = tensor(x.k_pool, dev)
         self.v = tensor(x.v_pool, dev)
         self.hidden = tensor(x.hidden, dev)
         self.w = tensor(x.w, dev)
+        if packed_vocab:
+            packed = torch.empty((sd.sd_vocab_packed_bytes(self.dims) // 2,), dtype=torch.bfloat16, device=dev)
+            sd.sd_pack_vocab(self.dims, self.w, packed)
+            self.w = packed
         self.q_draft = tensor(x.q_draft, dev)
         self.draft = tensor(x.draft, dev)
         self.u = tensor(x.u, dev)

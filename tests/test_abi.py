@@ -25,7 +25,8 @@ def test_library_loads_and_exports_header_symbols():
     lib = sd.library()
     names = sd.exported_symbols()
     assert set(names) == {"sd_workspace_bytes", "sd_verify_attention", "sd_verify_logits", "sd_accept_resample",
-                          "sd_verify_step", "sd_status_string", "sd_version"}
+                          "sd_verify_step", "sd_status_string", "sd_version", "sd_vocab_packed_bytes",
+                          "sd_pack_vocab"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2
@@ -113,6 +114,21 @@ def test_step_rejects_hidden_null_with_mismatched_width():
     st = lib.sd_verify_step(ctypes.byref(d), P, P, P, off, ln, 0.1, None, P, P, P, P, P, P, P, P, P, P, P,
                             1 << 30, None, None)
     assert st == sd.SD_ERR_INVALID_ARGUMENT
+
+
+@cpu_only
+def test_packed_vocab_sizes_and_validation():
+    d = dims()
+    assert sd.sd_vocab_packed_bytes(d) == 2 * 1024 * 1008   # V rounded up to 16
+    assert sd.sd_vocab_packed_bytes(dims(dtype=0)) == 0      # fp32 is not packed
+    lib = sd.library()
+    assert lib.sd_pack_vocab(ctypes.byref(dims(dtype=0)), P, P + (1 << 24), None) == sd.SD_ERR_UNSUPPORTED
+    assert lib.sd_pack_vocab(ctypes.byref(d), P, P + 8, None) == sd.SD_ERR_INVALID_ARGUMENT     # misaligned
+    assert lib.sd_pack_vocab(ctypes.byref(d), P, P + 4096, None) == sd.SD_ERR_INVALID_ARGUMENT  # overlap
+    assert lib.sd_pack_vocab(ctypes.byref(d), None, P, None) == sd.SD_ERR_INVALID_ARGUMENT
+    bad = dims(flags=4)
+    assert sd.sd_workspace_bytes(bad, 1000) == 0
+    assert sd.sd_workspace_bytes(dims(dtype=0, flags=1), 1000) == 0
 
 
 def test_binding_requires_device_tensors():

@@ -27,12 +27,14 @@ def _sampled_attention(x, reqs):
                             c.n_kv_heads)
 
 
-@pytest.mark.parametrize("name", ["vicuna7b", "pooled", "llama3_8b", "llama70b_share"])
-def test_full_size_step(name):
+@pytest.mark.parametrize("name,packed", [("vicuna7b", True), ("vicuna7b", False), ("pooled", True),
+                                         ("llama3_8b", True), ("llama70b_share", True)])
+def test_full_size_step(name, packed):
     cfg = get_config(name)
-    announce(f"full-size step case={name} B={cfg.batch} gamma={cfg.gamma} V={cfg.vocab} hidden={cfg.hidden}")
+    announce(f"full-size step case={name} packed_vocab={packed} B={cfg.batch} gamma={cfg.gamma} V={cfg.vocab} "
+             f"hidden={cfg.hidden}")
     x = make_inputs(cfg)
-    db = DeviceBatch(x)
+    db = DeviceBatch(x, packed_vocab=packed)
     db.step(use_hidden=True)
     torch.cuda.synchronize()
     announce(f"full-size step case={name}: GPU step done")

@@ -5,6 +5,7 @@ tiny fp32 case."""
 
 import numpy as np
 import pytest
+import torch
 
 from oracle import verify_logits
 from workloads import get_config, make_inputs
@@ -45,6 +46,29 @@ def test_logits_match_oracle(name):
     p = np.exp(to_np(db.logits).astype(np.float64) - lse[:, None])
     assert np.allclose(p.sum(axis=1), 1.0, atol=1e-5)
     announce(f"logits case={name} max scaled err {err:.3e} max |dlse| {np.abs(lse - ref_lse).max():.3e}")
+
+
+@pytest.mark.parametrize("name", ["m18_k512_v1000", "m18_k512_v1003", "m100_k256_v777", "m336_k256_v130"])
+def test_packed_vocab_matches_row_major_bitwise(name):
+    """The packed layout changes where W is read from, not the arithmetic:
+    logits and log-sum-exp must be bit-identical to the row-major path."""
+    cfg = CASES[name]
+    announce(f"packed vocab case={name}")
+    x = make_inputs(cfg)
+    a = DeviceBatch(x)
+    b = DeviceBatch(x, packed_vocab=True)
+    a.logits_()
+    b.logits_()
+    assert np.array_equal(to_np(a.logits), to_np(b.logits))
+    assert np.array_equal(to_np(a.lse), to_np(b.lse))
+    # The packed buffer itself: fragment (s, n), lane l holds W[16n + l%16][32s + 8(l/16) .. +8].
+    V, K = cfg.vocab, cfg.hidden
+    nb = (V + 15) // 16
+    w = np.zeros((nb * 16, K), dtype=np.uint16)
+    w[:V] = x.w
+    want = w.reshape(nb, 16, K // 32, 4, 8).transpose(2, 0, 3, 1, 4).reshape(-1)
+    got = b.w.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, want)
 
 
 def test_logits_deterministic():
