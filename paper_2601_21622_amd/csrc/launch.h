@@ -53,6 +53,10 @@ struct VocabPlan {
   int M, K, V;
   int tile_n;      // vocabulary columns per workgroup
   int ntiles;      // ceil(V / tile_n)
+  int mtiles;      // workgroups along the hidden rows
+  int mblocks;     // 16-row blocks per M-tile (bf16)
+  int nbw;         // 16-entry vocabulary blocks per wave (bf16)
+  bool deep;       // bf16 deep-pipelined schedule (more than 64 rows)
   bool packed;     // W in the fragment-order layout of launch_pack_vocab
 };
 VocabPlan vocab_plan(int dtype, int M, int K, int V, bool packed);

@@ -1,18 +1,26 @@
 // Vocabulary projection with a fused softmax-statistics epilogue (gfx950).
 //
 // logits^T = W hidden^T on MFMA 16x16x32 bf16: a W fragment (16 vocabulary
-// rows x 32 k, loaded in place from the [V][K] layout) is the A operand and a
-// hidden fragment (16 rows x 32 k) the B operand.  Each lane then holds four
-// consecutive vocabulary entries of one hidden row, which is what the logits
-// store and the row statistics want.
+// rows x 32 k) is the A operand and a hidden fragment (16 rows x 32 k) the B
+// operand.  Each lane then holds four consecutive vocabulary entries of one
+// hidden row, which is what the logits store and the row statistics want.
 //
-// One workgroup owns a tile of 64 vocabulary rows for all M hidden rows of its
-// M-tile, so W (the dominant stream, K*V*2 bytes) is read from HBM once; the
-// hidden rows, shared by every workgroup, are staged per K-chunk in LDS in
-// MFMA-fragment order (double-buffered) and stay L2-resident.  The epilogue
-// writes the float32 logits and, per (row, tile), the tile maximum and the sum
-// of exp(logit - maximum); a second kernel combines the tiles of each row in
-// fixed order into the row's log-sum-exp.
+// A workgroup (4 waves) owns a tile of vocabulary rows for all hidden rows of
+// its M-tile, so W (the dominant stream, K*V*2 bytes) is read from HBM once.
+// Every wave streams its own W fragments straight into registers; the hidden
+// rows, shared by every workgroup and L2-resident, are staged per K-chunk in
+// LDS in MFMA-fragment order and read by all four waves.  Two schedules:
+//   * shallow (at most 64 hidden rows): one 16-entry vocabulary block per
+//     wave, 256-wide K-chunks, one chunk of prefetch; several workgroups per
+//     CU keep enough W in flight.
+//   * deep (more rows): the accumulators of up to 320 rows pin one workgroup
+//     to a CU, so W and hidden are prefetched through a 4-deep register ring
+//     of 32-wide K-chunks (three chunks in flight while one is multiplied),
+//     and each wave owns 2 or 4 vocabulary blocks, so that one LDS read of a
+//     hidden fragment feeds 2 or 4 MFMAs.
+// The epilogue writes the float32 logits and, per (row, tile), the tile
+// maximum and the sum of exp(logit - maximum); a second kernel combines the
+// tiles of each row in fixed order into the row's log-sum-exp.
 #include <hip/hip_ext.h>
 
 #include <algorithm>
@@ -26,6 +34,79 @@ namespace {
 
 constexpr int kVThreads = 256;
 constexpr int kTileN = 64;  // vocabulary rows per workgroup (4 waves x 16)
+
+// Epilogue of one workgroup.  acc[mb][nb] of a lane holds hidden row
+// m0 + mb*16 + (lane & 15) and vocabulary entries (blk0 + nb)*16 + (lane>>4)*4
+// .. +3, where blk0 is the wave's first 16-entry block.  Writes the logits,
+// then the tile's per-row maximum and sum of exponentials, combined over the
+// four waves through `red` ([4][MBW*16] floats).
+template <int MBW, int NBW>
+__device__ __forceinline__ void tile_epilogue(const f32x4 (&acc)[MBW][NBW], int M, int V, int ntiles, int tile,
+                                              int m0, int blk0, float* __restrict__ logits,
+                                              float2* __restrict__ partials, float (*red)[MBW * 16]) {
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15;
+  const int lg = lane >> 4;
+  const bool v4 = (V % 4) == 0;
+  float tmax[MBW];
+#pragma unroll
+  for (int mb = 0; mb < MBW; ++mb) {
+    const int m = m0 + mb * 16 + lr;
+    float x = -INFINITY;
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+      const int v0 = (blk0 + nb) * 16 + lg * 4;
+      if (m < M) {
+        float* dst = logits + (int64_t)m * V + v0;
+        if (v4 && v0 + 3 < V) {
+          *reinterpret_cast<f32x4*>(dst) = acc[mb][nb];
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (v0 + i < V) dst[i] = acc[mb][nb][i];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x = (v0 + i < V) ? fmaxf(x, acc[mb][nb][i]) : x;
+    }
+    x = fmaxf(x, __shfl_xor(x, 16));
+    x = fmaxf(x, __shfl_xor(x, 32));
+    if (lg == 0) red[wave][mb * 16 + lr] = x;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int mb = 0; mb < MBW; ++mb) {
+    const int r = mb * 16 + lr;
+    tmax[mb] = fmaxf(fmaxf(red[0][r], red[1][r]), fmaxf(red[2][r], red[3][r]));
+  }
+  __syncthreads();
+#pragma unroll
+  for (int mb = 0; mb < MBW; ++mb) {
+    float sm = 0.f;
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+      const int v0 = (blk0 + nb) * 16 + lg * 4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sm += (v0 + i < V) ? expf(acc[mb][nb][i] - tmax[mb]) : 0.f;
+    }
+    sm += __shfl_xor(sm, 16);
+    sm += __shfl_xor(sm, 32);
+    if (lg == 0) red[wave][mb * 16 + lr] = sm;
+  }
+  __syncthreads();
+  if (wave == 0 && lg == 0) {
+#pragma unroll
+    for (int mb = 0; mb < MBW; ++mb) {
+      const int r = mb * 16 + lr;
+      const int m = m0 + r;
+      if (m < M) {
+        const float sm = (red[0][r] + red[1][r]) + (red[2][r] + red[3][r]);
+        partials[(int64_t)m * ntiles + tile] = make_float2(tmax[mb], sm);
+      }
+    }
+  }
+}
 
 template <int MB, int KC>
 struct VocabCfg {
@@ -100,9 +181,9 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
     for (int ks = 0; ks < C::kSteps; ++ks) dst[ks] = load_bf16x8(wrow + (int64_t)(kc * C::kSteps + ks) * wstep);
   };
 
-  f32x4 acc[MB];
+  f32x4 acc[MB][1];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int mb = 0; mb < MB; ++mb) acc[mb][0] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   load_a(0);
   load_w(wcur, 0);
@@ -121,7 +202,7 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
       for (int mb = 0; mb < MB; ++mb) {
         const bf16x8 a = __builtin_bit_cast(
             bf16x8, *reinterpret_cast<const u32x4*>(abuf[buf] + ((mb * C::kSteps + ks) * 64 + lane) * 16));
-        acc[mb] = mfma16x16x32(wcur[ks], a, acc[mb]);
+        acc[mb][0] = mfma16x16x32(wcur[ks], a, acc[mb][0]);
       }
     }
     if (more) {
@@ -132,61 +213,123 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
     lds_barrier();
   }
 
-  // Epilogue.  Lane holds hidden row m0 + mb*16 + lr, vocabulary v0 .. v0+3.
-  const int v0 = tile * kTileN + wave * 16 + lg * 4;
-  const bool vec_ok = (V % 4 == 0) && (v0 + 3 < V);
+  tile_epilogue<MB, 1>(acc, M, V, ntiles, tile, m0, tile * 4 + wave, logits, partials, red);
+}
+
+// Deep schedule: the workgroup's hidden rows (MBW blocks of 16) times
+// 4 waves x NBW vocabulary blocks, K in 32-wide chunks.  W fragments go
+// through a register ring of 4 slots and hidden pieces through one of 2
+// slots.  At chunk c a wave issues the hidden loads of chunk c+2 and the W
+// loads of chunk c+3, multiplies chunk c (W from the ring, hidden from LDS
+// buffer c&1) and writes hidden chunk c+1 from its ring slot into the other
+// LDS buffer.  Loads complete in issue order, so while chunk c is multiplied
+// the W of chunks c+1..c+3 and the hidden of c+1..c+2 are in flight, and the
+// wait for hidden c+1 never waits for W past c+2.  Loads past the last chunk
+// re-read the last chunk (in bounds) and chunks past the end multiply a zero
+// W, which keeps the loop free of branches around memory operations.
+template <int MBW, int NBW>
+struct DeepCfg {
+  static constexpr int kRows = MBW * 16;
+  static constexpr int kBufBytes = MBW * 1024;  // one 32-wide hidden chunk, fragment order
+  static constexpr int kPieces = kRows * 4;     // 16-byte pieces per chunk
+  static constexpr int kPiecesPerThread = (kPieces + kVThreads - 1) / kVThreads;
+};
+
+template <int MBW, int NBW, bool PACKED>
+__global__ __launch_bounds__(kVThreads, 1)
+void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, const uint16_t* __restrict__ hidden,
+                            const uint16_t* __restrict__ w, float* __restrict__ logits,
+                            float2* __restrict__ partials) {
+  using C = DeepCfg<MBW, NBW>;
+  constexpr int PPT = C::kPiecesPerThread;
+  __shared__ __align__(16) unsigned char abuf[2][C::kBufBytes];
+  __shared__ float red[4][C::kRows];
+
+  const int tile = blockIdx.x;
+  const int m0 = blockIdx.y * C::kRows;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15;
+  const int lg = lane >> 4;
+  const int nblk = (V + 15) / 16;
+  const int blk0 = (tile * 4 + wave) * NBW;
+  const uint16_t* wrow[NBW];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int m = m0 + mb * 16 + lr;
-    if (m < M) {
-      float* dst = logits + (int64_t)m * V + v0;
-      if (vec_ok) {
-        *reinterpret_cast<f32x4*>(dst) = acc[mb];
-      } else {
+  for (int nb = 0; nb < NBW; ++nb) {
+    if (PACKED)
+      wrow[nb] = w + ((int64_t)min(nblk - 1, blk0 + nb) * 64 + lane) * 8;
+    else
+      wrow[nb] = w + (int64_t)min(V - 1, (blk0 + nb) * 16 + lr) * K + lg * 8;
+  }
+  const int64_t wstep = PACKED ? (int64_t)nblk * 64 * 8 : 32;
+  const int nchunks = K / 32;
+
+  // Hidden piece p of a chunk: row p/4 (clamped to M-1; such rows are never
+  // stored), 16-byte k piece p%4; pieces past kPieces repeat the last one.
+  const uint16_t* hsrc[PPT];
+  int hslot[PPT];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (v0 + i < V) dst[i] = acc[mb][i];
+  for (int i = 0; i < PPT; ++i) {
+    const int p = min((int)threadIdx.x + i * kVThreads, C::kPieces - 1);
+    const int row = p >> 2, kp = p & 3;
+    hsrc[i] = hidden + (int64_t)min(M - 1, m0 + row) * K + kp * 8;
+    hslot[i] = ((row >> 4) * 64 + (row & 15) + 16 * kp) * 16;
+  }
+
+  u32x4 hreg[2][PPT];
+  bf16x8 wreg[4][NBW];
+  auto issue_h = [&](int slot, int c) {
+    c = min(c, nchunks - 1);
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) hreg[slot][i] = *reinterpret_cast<const u32x4*>(hsrc[i] + c * 32);
+  };
+  auto issue_w = [&](int slot, int c) {
+    c = min(c, nchunks - 1);
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) wreg[slot][nb] = load_bf16x8(wrow[nb] + (int64_t)c * wstep);
+  };
+  auto stage = [&](int slot, int buf) {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i)
+      if (i + 1 < PPT || (int)threadIdx.x + i * kVThreads < C::kPieces)
+        *reinterpret_cast<u32x4*>(abuf[buf] + hslot[i]) = hreg[slot][i];
+  };
+
+  f32x4 acc[MBW][NBW];
+#pragma unroll
+  for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  issue_h(0, 0);
+  issue_w(0, 0);
+  issue_h(1, 1);
+  issue_w(1, 1);
+  issue_w(2, 2);
+  stage(0, 0);
+  lds_barrier();
+  for (int c0 = 0; c0 < nchunks; c0 += 4) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int c = c0 + s;
+      issue_h(s & 1, c + 2);
+      issue_w((s + 3) & 3, c + 3);
+      bf16x8 wv[NBW];
+      const bool live = c < nchunks;
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) wv[nb] = live ? wreg[s][nb] : bf16x8{};
+#pragma unroll
+      for (int mb = 0; mb < MBW; ++mb) {
+        const bf16x8 a =
+            __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(abuf[s & 1] + (mb * 64 + lane) * 16));
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) acc[mb][nb] = mfma16x16x32(wv[nb], a, acc[mb][nb]);
       }
+      stage((s + 1) & 1, (s + 1) & 1);
+      lds_barrier();
     }
   }
-  float tmax[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    float x = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) x = (v0 + i < V) ? fmaxf(x, acc[mb][i]) : x;
-    x = fmaxf(x, __shfl_xor(x, 16));
-    x = fmaxf(x, __shfl_xor(x, 32));
-    if (lg == 0) red[wave][mb * 16 + lr] = x;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int r = mb * 16 + lr;
-    tmax[mb] = fmaxf(fmaxf(red[0][r], red[1][r]), fmaxf(red[2][r], red[3][r]));
-  }
-  __syncthreads();
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) s += (v0 + i < V) ? expf(acc[mb][i] - tmax[mb]) : 0.f;
-    s += __shfl_xor(s, 16);
-    s += __shfl_xor(s, 32);
-    if (lg == 0) red[wave][mb * 16 + lr] = s;
-  }
-  __syncthreads();
-  if (wave == 0 && lg == 0) {
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int r = mb * 16 + lr;
-      const int m = m0 + r;
-      if (m < M) {
-        const float s = (red[0][r] + red[1][r]) + (red[2][r] + red[3][r]);
-        partials[(int64_t)m * ntiles + tile] = make_float2(tmax[mb], s);
-      }
-    }
-  }
+  tile_epilogue<MBW, NBW>(acc, M, V, ntiles, tile, m0, blk0, logits, partials, red);
 }
 
 // float32 path: 64 rows x 64 vocabulary entries per workgroup, LDS-tiled FMA.
@@ -265,29 +408,47 @@ void pack_vocab_kernel(int K, int V, const uint16_t* __restrict__ w, uint16_t* _
 }
 
 template <int MB, int KC>
-hipError_t launch_mb_kc(const VocabPlan& p, int mtiles, const void* hidden, const void* w, float* logits,
-                        float2* partials, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_shallow(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
+                          hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid(p.ntiles, p.mtiles), block(kVThreads);
+  const uint16_t* h = static_cast<const uint16_t*>(hidden);
+  const uint16_t* wv = static_cast<const uint16_t*>(w);
   if (p.packed)
-    hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC, true>), dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, e0,
-                          e1, 0, p.M, p.K, p.V, p.ntiles, static_cast<const uint16_t*>(hidden),
-                          static_cast<const uint16_t*>(w), logits, partials);
+    hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC, true>), grid, block, 0, stream, e0, e1, 0, p.M, p.K, p.V,
+                          p.ntiles, h, wv, logits, partials);
   else
-    hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC, false>), dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, e0,
-                          e1, 0, p.M, p.K, p.V, p.ntiles, static_cast<const uint16_t*>(hidden),
-                          static_cast<const uint16_t*>(w), logits, partials);
+    hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC, false>), grid, block, 0, stream, e0, e1, 0, p.M, p.K, p.V,
+                          p.ntiles, h, wv, logits, partials);
   return hipGetLastError();
 }
 
-// K-chunk: as long as the double-buffered hidden chunk fits comfortably in LDS;
-// 32 (one MFMA step) whenever K is not a multiple of the preferred chunk.
 template <int MB>
-hipError_t launch_mb(const VocabPlan& p, int mtiles, const void* hidden, const void* w, float* logits,
-                     float2* partials, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  constexpr int KC = MB <= 4 ? 256 : (MB <= 8 ? 128 : (MB <= 16 ? 64 : 32));
-  if (p.K % KC == 0) return launch_mb_kc<MB, KC>(p, mtiles, hidden, w, logits, partials, stream, e0, e1);
-  if (p.K % 32 == 0) return launch_mb_kc<MB, 32>(p, mtiles, hidden, w, logits, partials, stream, e0, e1);
-  return hipErrorInvalidValue;
+hipError_t launch_shallow_mb(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
+                             hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  if (p.K % 256 == 0) return launch_shallow<MB, 256>(p, hidden, w, logits, partials, stream, e0, e1);
+  return launch_shallow<MB, 32>(p, hidden, w, logits, partials, stream, e0, e1);
 }
+
+template <int MBW, int NBW>
+hipError_t launch_deep(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
+                       hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid(p.ntiles, p.mtiles), block(kVThreads);
+  const uint16_t* h = static_cast<const uint16_t*>(hidden);
+  const uint16_t* wv = static_cast<const uint16_t*>(w);
+  if (p.packed)
+    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MBW, NBW, true>), grid, block, 0, stream, e0, e1, 0, p.M, p.K,
+                          p.V, p.ntiles, h, wv, logits, partials);
+  else
+    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MBW, NBW, false>), grid, block, 0, stream, e0, e1, 0, p.M, p.K,
+                          p.V, p.ntiles, h, wv, logits, partials);
+  return hipGetLastError();
+}
+
+// Largest row-block count per M-tile of the deep schedule: the accumulators
+// (MBW x NBW x 4 registers) stay within the 256 accumulation registers.
+constexpr int kDeepMaxBlocks2 = 20;
+constexpr int kDeepMaxBlocks4 = 16;
+constexpr int kShallowMaxBlocks = 4;
 
 }  // namespace
 
@@ -304,14 +465,33 @@ hipError_t launch_pack_vocab(int K, int V, const void* w, void* out, hipStream_t
 }
 
 VocabPlan vocab_plan(int dtype, int M, int K, int V, bool packed) {
-  (void)dtype;
   VocabPlan p;
   p.packed = packed;
   p.M = M;
   p.K = K;
   p.V = V;
-  p.tile_n = kTileN;
-  p.ntiles = (V + kTileN - 1) / kTileN;
+  const int blocks = (M + 15) / 16;
+  if (dtype == 0) {
+    p.deep = false;
+    p.mblocks = 4;
+    p.nbw = 1;
+    p.mtiles = (M + 63) / 64;
+  } else if (blocks <= kShallowMaxBlocks) {
+    p.deep = false;
+    p.mblocks = blocks;
+    p.nbw = 1;
+    p.mtiles = 1;
+  } else {
+    // Four blocks per wave once the vocabulary still gives at least one
+    // 256-wide tile per CU; two otherwise.
+    p.deep = true;
+    p.nbw = V >= 256 * 256 ? 4 : 2;
+    const int cap = p.nbw == 4 ? kDeepMaxBlocks4 : kDeepMaxBlocks2;
+    p.mtiles = (blocks + cap - 1) / cap;
+    p.mblocks = (blocks + p.mtiles - 1) / p.mtiles;
+  }
+  p.tile_n = 64 * p.nbw;
+  p.ntiles = (V + p.tile_n - 1) / p.tile_n;
   return p;
 }
 
@@ -322,25 +502,35 @@ size_t vocab_partial_bytes(const VocabPlan& p) {
 hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w, float* logits,
                         float2* partials, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   if (dtype == 0) {
-    const int mtiles = (p.M + 63) / 64;
-    hipExtLaunchKernelGGL(vocab_f32_kernel, dim3(p.ntiles, mtiles), dim3(kVThreads), 0, stream, e0, e1, 0, p.M, p.K,
+    hipExtLaunchKernelGGL(vocab_f32_kernel, dim3(p.ntiles, p.mtiles), dim3(kVThreads), 0, stream, e0, e1, 0, p.M, p.K,
                           p.V, p.ntiles, static_cast<const float*>(hidden), static_cast<const float*>(w), logits,
                           partials);
     return hipGetLastError();
   }
-  const int blocks = (p.M + 15) / 16;
-  // Rows per M-tile: up to 20 blocks of 16 (320 rows) so that W is streamed
-  // once for every pooled batch up to that size.
-  const int mtiles = (blocks + 19) / 20;
-  const int mb = (blocks + mtiles - 1) / mtiles;
-  switch (mb) {
-#define SDV_MB(n) case n: return launch_mb<n>(p, mtiles, hidden, w, logits, partials, stream, e0, e1);
-    SDV_MB(1) SDV_MB(2) SDV_MB(3) SDV_MB(4) SDV_MB(5) SDV_MB(6) SDV_MB(7) SDV_MB(8) SDV_MB(9) SDV_MB(10)
-    SDV_MB(11) SDV_MB(12) SDV_MB(13) SDV_MB(14) SDV_MB(15) SDV_MB(16) SDV_MB(17) SDV_MB(18) SDV_MB(19)
-    SDV_MB(20)
-#undef SDV_MB
+  if (!p.deep) {
+    switch (p.mblocks) {
+      case 1: return launch_shallow_mb<1>(p, hidden, w, logits, partials, stream, e0, e1);
+      case 2: return launch_shallow_mb<2>(p, hidden, w, logits, partials, stream, e0, e1);
+      case 3: return launch_shallow_mb<3>(p, hidden, w, logits, partials, stream, e0, e1);
+      case 4: return launch_shallow_mb<4>(p, hidden, w, logits, partials, stream, e0, e1);
+      default: return hipErrorInvalidValue;
+    }
+  }
+#define SDV_D(B, N) \
+  case B: return launch_deep<B, N>(p, hidden, w, logits, partials, stream, e0, e1);
+  if (p.nbw == 4) {
+    switch (p.mblocks) {
+      SDV_D(5, 4) SDV_D(6, 4) SDV_D(7, 4) SDV_D(8, 4) SDV_D(9, 4) SDV_D(10, 4) SDV_D(11, 4) SDV_D(12, 4)
+      SDV_D(13, 4) SDV_D(14, 4) SDV_D(15, 4) SDV_D(16, 4)
+      default: return hipErrorInvalidValue;
+    }
+  }
+  switch (p.mblocks) {
+    SDV_D(5, 2) SDV_D(6, 2) SDV_D(7, 2) SDV_D(8, 2) SDV_D(9, 2) SDV_D(10, 2) SDV_D(11, 2) SDV_D(12, 2)
+    SDV_D(13, 2) SDV_D(14, 2) SDV_D(15, 2) SDV_D(16, 2) SDV_D(17, 2) SDV_D(18, 2) SDV_D(19, 2) SDV_D(20, 2)
     default: return hipErrorInvalidValue;
   }
+#undef SDV_D
 }
 
 hipError_t launch_lse_combine(const VocabPlan& p, const float2* partials, float* row_lse, hipStream_t stream) {

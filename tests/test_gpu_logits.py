@@ -1,7 +1,8 @@
 """GPU parity: sd_verify_logits (vocabulary projection + row log-sum-exp)
-against the float64 oracle.  Shapes cover ragged vocabulary tiles (V not a
-multiple of 64, and not of 4), every K-chunk path, several M-tiles, and the
-tiny fp32 case."""
+against the float64 oracle.  Shapes cover both bf16 schedules (at most 64
+rows; more rows with two or four vocabulary blocks per wave), ragged
+vocabulary tiles (V not a multiple of the tile, and not of 4), K not a multiple
+of the chunk, several M-tiles, and the tiny fp32 case."""
 
 import numpy as np
 import pytest
@@ -27,6 +28,12 @@ CASES = {
                                 lengths=("fixed", 8)),
     "m336_k256_v130": _v.replace(batch=56, gamma=5, n_q_heads=2, n_kv_heads=2, hidden=256, vocab=130,
                                  lengths=("fixed", 8)),
+    # Four vocabulary blocks per wave (V >= 65536), ragged last tile.
+    "m80_k128_v65600": _v.replace(batch=16, gamma=4, n_q_heads=2, n_kv_heads=2, hidden=128, vocab=65600,
+                                  lengths=("fixed", 8)),
+    # Two M-tiles of the four-block schedule, K not a multiple of 128, V odd.
+    "m272_k96_v65537": _v.replace(batch=34, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=96, vocab=65537,
+                                  lengths=("fixed", 8)),
     "f32_m70_k128_v65": get_config("tiny").replace(batch=14, gamma=4, hidden=128, vocab=65, lengths=("fixed", 8)),
 }
 
@@ -48,7 +55,8 @@ def test_logits_match_oracle(name):
     announce(f"logits case={name} max scaled err {err:.3e} max |dlse| {np.abs(lse - ref_lse).max():.3e}")
 
 
-@pytest.mark.parametrize("name", ["m18_k512_v1000", "m18_k512_v1003", "m100_k256_v777", "m336_k256_v130"])
+@pytest.mark.parametrize("name", ["m18_k512_v1000", "m18_k512_v1003", "m100_k256_v777", "m336_k256_v130",
+                                  "m272_k96_v65537"])
 def test_packed_vocab_matches_row_major_bitwise(name):
     """The packed layout changes where W is read from, not the arithmetic:
     logits and log-sum-exp must be bit-identical to the row-major path."""
