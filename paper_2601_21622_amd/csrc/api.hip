@@ -70,7 +70,7 @@ size_t attention_ws(const sd_dims_t* d, int64_t chunks) {
 
 size_t logits_ws(const sd_dims_t* d) {
   const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab, (d->flags & SD_FLAG_PACKED_VOCAB) != 0);
-  return align_up(vocab_partial_bytes(p));
+  return align_up(vocab_workspace_bytes(p));
 }
 
 int check_kv(const sd_dims_t* d, const int64_t* kv_off, const int32_t* kv_len) {
@@ -123,7 +123,7 @@ int run_logits(const sd_dims_t* d, const void* hidden, const void* w, float* log
                hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
   const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab, (d->flags & SD_FLAG_PACKED_VOCAB) != 0);
   float2* partials = static_cast<float2*>(ws);
-  hipError_t e = launch_vocab(d->dtype, p, hidden, w, logits, partials, stream, ev_start, ev_stop);
+  hipError_t e = launch_vocab(d->dtype, p, hidden, w, logits, ws, stream, ev_start, ev_stop);
   if (e == hipSuccess) e = launch_lse_combine(p, partials, row_lse, stream);
   return hip_status(e);
 }
@@ -264,7 +264,7 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   // segment kernel writes the latter.
   const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab, (dims->flags & SD_FLAG_PACKED_VOCAB) != 0);
   float2* partials = static_cast<float2*>(workspace);
-  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, partials, stm, ev[2],
+  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, workspace, stm, ev[2],
                    ev[3]) != hipSuccess)
     return SD_ERR_HIP;
   void* acc_ws = static_cast<char*>(workspace) + logits_ws(dims);

@@ -54,17 +54,20 @@ struct VocabPlan {
   int tile_n;      // vocabulary columns per workgroup
   int ntiles;      // ceil(V / tile_n)
   int mtiles;      // workgroups along the hidden rows
-  int mblocks;     // 16-row blocks per M-tile (bf16)
+  int mblocks;     // bf16 row blocks per M-tile: of 16 rows (shallow), of 32 (deep)
   int nbw;         // 16-entry vocabulary blocks per wave (bf16)
-  bool deep;       // bf16 deep-pipelined schedule (more than 64 rows)
+  bool deep;       // bf16 deep-pipelined 32x32 schedule (more than 64 rows)
   bool packed;     // W in the fragment-order layout of launch_pack_vocab
 };
 VocabPlan vocab_plan(int dtype, int M, int K, int V, bool packed);
 size_t vocab_packed_bytes(int K, int V);
 hipError_t launch_pack_vocab(int K, int V, const void* w, void* out, hipStream_t stream);
-size_t vocab_partial_bytes(const VocabPlan& p);
+// Workspace of launch_vocab: the per-(row, tile) softmax statistics
+// (float2[M][ntiles]) at its start, then, for the deep schedule, the hidden
+// rows repacked into MFMA fragments.
+size_t vocab_workspace_bytes(const VocabPlan& p);
 hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w,
-                        float* logits, float2* partials, hipStream_t stream, hipEvent_t ev_start,
+                        float* logits, void* workspace, hipStream_t stream, hipEvent_t ev_start,
                         hipEvent_t ev_stop);
 hipError_t launch_lse_combine(const VocabPlan& p, const float2* partials, float* row_lse,
                               hipStream_t stream);

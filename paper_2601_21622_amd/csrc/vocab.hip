@@ -35,16 +35,19 @@ namespace {
 constexpr int kVThreads = 256;
 constexpr int kTileN = 64;  // vocabulary rows per workgroup (4 waves x 16)
 
-// Epilogue of one workgroup.  acc[mb][nb] of a lane holds hidden row
-// m0 + mb*16 + (lane & 15) and vocabulary entries (blk0 + nb)*16 + (lane>>4)*4
+// Epilogue of one workgroup of WM x WN waves.  Wave (wm, wn) = (wave / WN,
+// wave % WN) holds in acc[mb][nb] hidden row m0 + r0 + mb*16 + (lane & 15),
+// with r0 = wm*MBW*16, and vocabulary entries (blk0 + nb)*16 + (lane>>4)*4
 // .. +3, where blk0 is the wave's first 16-entry block.  Writes the logits,
 // then the tile's per-row maximum and sum of exponentials, combined over the
-// four waves through `red` ([4][MBW*16] floats).
-template <int MBW, int NBW>
+// WN waves that share the rows through `red` ([WN][WM*MBW*16] floats).
+template <int MBW, int NBW, int WM, int WN>
 __device__ __forceinline__ void tile_epilogue(const f32x4 (&acc)[MBW][NBW], int M, int V, int ntiles, int tile,
                                               int m0, int blk0, float* __restrict__ logits,
-                                              float2* __restrict__ partials, float (*red)[MBW * 16]) {
+                                              float2* __restrict__ partials, float (*red)[WM * MBW * 16]) {
   const int wave = threadIdx.x >> 6;
+  const int wn = wave % WN;
+  const int r0 = (wave / WN) * MBW * 16;
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15;
   const int lg = lane >> 4;
@@ -52,7 +55,7 @@ __device__ __forceinline__ void tile_epilogue(const f32x4 (&acc)[MBW][NBW], int 
   float tmax[MBW];
 #pragma unroll
   for (int mb = 0; mb < MBW; ++mb) {
-    const int m = m0 + mb * 16 + lr;
+    const int m = m0 + r0 + mb * 16 + lr;
     float x = -INFINITY;
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
@@ -72,13 +75,16 @@ __device__ __forceinline__ void tile_epilogue(const f32x4 (&acc)[MBW][NBW], int 
     }
     x = fmaxf(x, __shfl_xor(x, 16));
     x = fmaxf(x, __shfl_xor(x, 32));
-    if (lg == 0) red[wave][mb * 16 + lr] = x;
+    if (lg == 0) red[wn][r0 + mb * 16 + lr] = x;
   }
   __syncthreads();
 #pragma unroll
   for (int mb = 0; mb < MBW; ++mb) {
-    const int r = mb * 16 + lr;
-    tmax[mb] = fmaxf(fmaxf(red[0][r], red[1][r]), fmaxf(red[2][r], red[3][r]));
+    const int r = r0 + mb * 16 + lr;
+    float x = red[0][r];
+#pragma unroll
+    for (int w = 1; w < WN; ++w) x = fmaxf(x, red[w][r]);
+    tmax[mb] = x;
   }
   __syncthreads();
 #pragma unroll
@@ -92,16 +98,22 @@ __device__ __forceinline__ void tile_epilogue(const f32x4 (&acc)[MBW][NBW], int 
     }
     sm += __shfl_xor(sm, 16);
     sm += __shfl_xor(sm, 32);
-    if (lg == 0) red[wave][mb * 16 + lr] = sm;
+    if (lg == 0) red[wn][r0 + mb * 16 + lr] = sm;
   }
   __syncthreads();
-  if (wave == 0 && lg == 0) {
+  if (wn == 0 && lg == 0) {
 #pragma unroll
     for (int mb = 0; mb < MBW; ++mb) {
-      const int r = mb * 16 + lr;
+      const int r = r0 + mb * 16 + lr;
       const int m = m0 + r;
       if (m < M) {
-        const float sm = (red[0][r] + red[1][r]) + (red[2][r] + red[3][r]);
+        float sm;
+        if (WN == 4)
+          sm = (red[0][r] + red[1][r]) + (red[2][r] + red[3][r]);
+        else if (WN == 2)
+          sm = red[0][r] + red[1][r];
+        else
+          sm = red[0][r];
         partials[(int64_t)m * ntiles + tile] = make_float2(tmax[mb], sm);
       }
     }
@@ -213,123 +225,270 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
     lds_barrier();
   }
 
-  tile_epilogue<MB, 1>(acc, M, V, ntiles, tile, m0, tile * 4 + wave, logits, partials, red);
+  tile_epilogue<MB, 1, 1, 4>(acc, M, V, ntiles, tile, m0, tile * 4 + wave, logits, partials, red);
 }
 
-// Deep schedule: the workgroup's hidden rows (MBW blocks of 16) times
-// 4 waves x NBW vocabulary blocks, K in 32-wide chunks.  W fragments go
-// through a register ring of 4 slots and hidden pieces through one of 2
-// slots.  At chunk c a wave issues the hidden loads of chunk c+2 and the W
-// loads of chunk c+3, multiplies chunk c (W from the ring, hidden from LDS
-// buffer c&1) and writes hidden chunk c+1 from its ring slot into the other
-// LDS buffer.  Loads complete in issue order, so while chunk c is multiplied
-// the W of chunks c+1..c+3 and the hidden of c+1..c+2 are in flight, and the
-// wait for hidden c+1 never waits for W past c+2.  Loads past the last chunk
-// re-read the last chunk (in bounds) and chunks past the end multiply a zero
-// W, which keeps the loop free of branches around memory operations.
-template <int MBW, int NBW>
-struct DeepCfg {
-  static constexpr int kRows = MBW * 16;
-  static constexpr int kBufBytes = MBW * 1024;  // one 32-wide hidden chunk, fragment order
-  static constexpr int kPieces = kRows * 4;     // 16-byte pieces per chunk
-  static constexpr int kPiecesPerThread = (kPieces + kVThreads - 1) / kVThreads;
+// Deep schedule (more than 64 rows) on MFMA 32x32x16: the accumulators of up
+// to 448 rows pin one workgroup of four waves to a CU, and a single wave per
+// SIMD keeps the 32x32 MFMA pipe full where the 16x16 one would stall.  The
+// workgroup covers MB blocks of 32 hidden rows and 4 x NB blocks of 32
+// vocabulary entries; wave w owns blocks (tile*4 + w)*NB .. +NB, i.e.
+// MB x NB accumulators of 16 registers.  K goes in 32-wide chunks of two
+// 16-wide MFMA steps.
+//
+// Pipeline, chunk c of the loop (kStages = 6):
+//   * issue chunk c+4: its hidden chunk goes straight from global memory into
+//     LDS buffer (c+4) % 6 (LDS DMA, no registers), its W fragments into the
+//     register ring slot (c+4) % 6;
+//   * read the hidden fragments of chunk c+1 from LDS into registers;
+//   * multiply chunk c (W ring slot c % 6, fragments read one chunk earlier);
+//   * wait until this wave's DMA of chunk c+2 has landed, then barrier, so
+//     chunk c+2 is readable by every wave in the next step.
+// Memory operations complete in issue order, so the wait leaves the loads of
+// chunks c+3 and c+4 (and the W of c+2) in flight: three chunks of W and two
+// of hidden are always on the way while the MFMAs run, and no MFMA waits on
+// an LDS read issued in the same step.  Loads past the last chunk re-read the
+// last chunk (in bounds) and chunks past the end multiply a zero W, which
+// keeps the loop free of branches around memory operations.
+//
+// The hidden rows are first repacked (pack_hidden_kernel) into fragments of 32
+// rows x 16 k in lane order (lane l: row l%32, k 8*(l/32) .. +8), so every
+// DMA instruction moves 1 KB of contiguous memory into one LDS fragment.  W
+// fragments (32 vocabulary rows x 16 k, same lane order) are read either from
+// the row-major [V][K] layout or gathered from the packed 16x16x32 fragment
+// layout.
+constexpr int kStages = 6;
+
+template <int MB, int NB>
+struct Deep32Cfg {
+  static constexpr int kRows = MB * 32;
+  static constexpr int kFrags = 2 * MB;               // hidden fragments per chunk
+  static constexpr int kDmaPerWave = (kFrags + 3) / 4;  // the same count on every wave
+  static constexpr int kBufBytes = 4 * kDmaPerWave * 1024;
+  // Memory operations a wave issues per chunk, and the most that may still be
+  // outstanding once the DMA of the chunk two steps ahead has landed.
+  static constexpr int kOpsPerChunk = kDmaPerWave + 2 * NB;
+  static constexpr int kInFlight = 2 * NB + 2 * kOpsPerChunk;
 };
 
-template <int MBW, int NBW, bool PACKED>
-__global__ __launch_bounds__(kVThreads, 1)
-void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, const uint16_t* __restrict__ hidden,
-                            const uint16_t* __restrict__ w, float* __restrict__ logits,
-                            float2* __restrict__ partials) {
-  using C = DeepCfg<MBW, NBW>;
-  constexpr int PPT = C::kPiecesPerThread;
-  __shared__ __align__(16) unsigned char abuf[2][C::kBufBytes];
-  __shared__ float red[4][C::kRows];
-
-  const int tile = blockIdx.x;
-  const int m0 = blockIdx.y * C::kRows;
+template <int MB, int NB>
+__device__ __forceinline__ void tile_epilogue32(const f32x16 (&acc)[MB][NB], int M, int V, int ntiles, int tile,
+                                                int m0, int blk0, float* __restrict__ logits,
+                                                float2* __restrict__ partials, float (*red)[MB * 32]) {
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int lr = lane & 15;
-  const int lg = lane >> 4;
-  const int nblk = (V + 15) / 16;
-  const int blk0 = (tile * 4 + wave) * NBW;
-  const uint16_t* wrow[NBW];
+  const int j = lane & 31;
+  const int h = lane >> 5;
+  const bool v4 = (V % 4) == 0;
+  float tmax[MB];
 #pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    if (PACKED)
-      wrow[nb] = w + ((int64_t)min(nblk - 1, blk0 + nb) * 64 + lane) * 8;
-    else
-      wrow[nb] = w + (int64_t)min(V - 1, (blk0 + nb) * 16 + lr) * K + lg * 8;
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = m0 + mb * 32 + j;
+    float x = -INFINITY;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int v0 = (blk0 + nb) * 32 + 8 * g + 4 * h;
+        const f32x4 q = {acc[mb][nb][4 * g], acc[mb][nb][4 * g + 1], acc[mb][nb][4 * g + 2], acc[mb][nb][4 * g + 3]};
+        if (m < M) {
+          float* dst = logits + (int64_t)m * V + v0;
+          if (v4 && v0 + 3 < V) {
+            *reinterpret_cast<f32x4*>(dst) = q;
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (v0 + i < V) dst[i] = q[i];
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x = (v0 + i < V) ? fmaxf(x, q[i]) : x;
+      }
+    }
+    x = fmaxf(x, __shfl_xor(x, 32));
+    if (h == 0) red[wave][mb * 32 + j] = x;
   }
+  __syncthreads();
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int r = mb * 32 + j;
+    tmax[mb] = fmaxf(fmaxf(red[0][r], red[1][r]), fmaxf(red[2][r], red[3][r]));
+  }
+  __syncthreads();
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    float sm = 0.f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = (blk0 + nb) * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        sm += (v < V) ? expf(acc[mb][nb][r] - tmax[mb]) : 0.f;
+      }
+    sm += __shfl_xor(sm, 32);
+    if (h == 0) red[wave][mb * 32 + j] = sm;
+  }
+  __syncthreads();
+  if (wave == 0 && h == 0) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int r = mb * 32 + j;
+      const int m = m0 + r;
+      if (m < M) {
+        const float sm = (red[0][r] + red[1][r]) + (red[2][r] + red[3][r]);
+        partials[(int64_t)m * ntiles + tile] = make_float2(tmax[mb], sm);
+      }
+    }
+  }
+}
+
+template <int MB, int NB, bool PACKED>
+__global__ __launch_bounds__(kVThreads, 1)
+void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const uint16_t* __restrict__ hpacked,
+                            const uint16_t* __restrict__ w, float* __restrict__ logits,
+                            float2* __restrict__ partials) {
+  using C = Deep32Cfg<MB, NB>;
+  constexpr int ND = C::kDmaPerWave;
+  // One LDS object per stage: the compiler then sees that a fragment read
+  // and a DMA into another stage cannot alias, and leaves the ordering to the
+  // explicit vmcnt waits below.
+  __shared__ __align__(1024) unsigned char lds0[C::kBufBytes], lds1[C::kBufBytes], lds2[C::kBufBytes],
+      lds3[C::kBufBytes], lds4[C::kBufBytes], lds5[C::kBufBytes];
+  __shared__ float red[4][C::kRows];
+  auto abuf = [&](int stage) -> unsigned char* {
+    switch (stage) {
+      case 0: return lds0;
+      case 1: return lds1;
+      case 2: return lds2;
+      case 3: return lds3;
+      case 4: return lds4;
+      default: return lds5;
+    }
+  };
+
+  // Workgroup id -> (tile, M-tile): ids are dealt to the 8 XCDs round-robin,
+  // so the M-tiles of one vocabulary tile take ids 8 apart and share an XCD
+  // (and its L2), where the second reader of each W line finds it.
+  const int grp = 8 * mtiles;
+  const int tile = (blockIdx.x / grp) * 8 + (blockIdx.x & 7);
+  if (tile >= ntiles) return;
+  const int m0 = ((blockIdx.x % grp) >> 3) * C::kRows;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int nblk = (V + 15) / 16;
+  const int blk0 = (tile * 4 + wave) * NB;  // first 32-entry vocabulary block of the wave
+  // W source of this lane for 16-wide k-step ks of chunk 0; chunk c adds c*wstep.
+  const uint16_t* wsrc[NB][2];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int row = (blk0 + nb) * 32 + (lane & 31);
+      if (PACKED) {
+        // Row `row` lives in 16-row block row/16 at lane row%16 + 16*g, where
+        // g = 2*ks + lane/32 selects the 8-wide k piece of the 32-wide step.
+        const int n16 = min(nblk - 1, row >> 4);
+        const int l16 = (row & 15) + 16 * (2 * ks + (lane >> 5));
+        wsrc[nb][ks] = w + ((int64_t)n16 * 64 + l16) * 8;
+      } else {
+        wsrc[nb][ks] = w + (int64_t)min(V - 1, row) * K + ks * 16 + (lane >> 5) * 8;
+      }
+    }
   const int64_t wstep = PACKED ? (int64_t)nblk * 64 * 8 : 32;
   const int nchunks = K / 32;
 
-  // Hidden piece p of a chunk: row p/4 (clamped to M-1; such rows are never
-  // stored), 16-byte k piece p%4; pieces past kPieces repeat the last one.
-  const uint16_t* hsrc[PPT];
-  int hslot[PPT];
+  // DMA i of this wave moves fragment f = wave + 4*i (2*mb + ks) of a chunk:
+  // 1 KB contiguous in the packed hidden (lane l: row mb*32 + l%32, k
+  // 16*ks + 8*(l/32) .. +8).  Fragment numbers past the chunk's 2*MB re-read
+  // the last fragment into spare LDS space; blocks past the packed rows
+  // (last M-tile) re-read the last block, whose rows are never stored.
+  const int mbt = (M + 31) / 32;
+  const int64_t hstep = (int64_t)2 * mbt * 512;  // elements per 32-wide chunk
+  const uint16_t* hsrc[ND];
+  int hoff[ND];
 #pragma unroll
-  for (int i = 0; i < PPT; ++i) {
-    const int p = min((int)threadIdx.x + i * kVThreads, C::kPieces - 1);
-    const int row = p >> 2, kp = p & 3;
-    hsrc[i] = hidden + (int64_t)min(M - 1, m0 + row) * K + kp * 8;
-    hslot[i] = ((row >> 4) * 64 + (row & 15) + 16 * kp) * 16;
+  for (int i = 0; i < ND; ++i) {
+    const int f = wave + 4 * i;
+    const int fs = min(f, C::kFrags - 1);
+    const int mbg = min(mbt - 1, m0 / 32 + (fs >> 1));
+    hsrc[i] = hpacked + (((int64_t)(fs & 1) * mbt + mbg) * 64 + lane) * 8;
+    hoff[i] = f * 1024;
   }
 
-  u32x4 hreg[2][PPT];
-  bf16x8 wreg[4][NBW];
-  auto issue_h = [&](int slot, int c) {
+  bf16x8 wreg[kStages][NB][2];
+  bf16x8 af[2][C::kFrags];
+  auto issue = [&](int slot, int c) {
     c = min(c, nchunks - 1);
 #pragma unroll
-    for (int i = 0; i < PPT; ++i) hreg[slot][i] = *reinterpret_cast<const u32x4*>(hsrc[i] + c * 32);
-  };
-  auto issue_w = [&](int slot, int c) {
-    c = min(c, nchunks - 1);
+    for (int i = 0; i < ND; ++i)
+      dma_16B_to_lds(hsrc[i] + c * hstep, abuf(slot) + hoff[i]);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) wreg[slot][nb] = load_bf16x8(wrow[nb] + (int64_t)c * wstep);
-  };
-  auto stage = [&](int slot, int buf) {
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-    for (int i = 0; i < PPT; ++i)
-      if (i + 1 < PPT || (int)threadIdx.x + i * kVThreads < C::kPieces)
-        *reinterpret_cast<u32x4*>(abuf[buf] + hslot[i]) = hreg[slot][i];
+      for (int ks = 0; ks < 2; ++ks) wreg[slot][nb][ks] = load_bf16x8(wsrc[nb][ks] + (int64_t)c * wstep);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto read_frags = [&](int set, int slot) {
+#pragma unroll
+    for (int f = 0; f < C::kFrags; ++f)
+      af[set][f] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(abuf(slot) + f * 1024 + lane * 16));
   };
 
-  f32x4 acc[MBW][NBW];
+  f32x16 acc[MB][NB];
 #pragma unroll
-  for (int mb = 0; mb < MBW; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
-  issue_h(0, 0);
-  issue_w(0, 0);
-  issue_h(1, 1);
-  issue_w(1, 1);
-  issue_w(2, 2);
-  stage(0, 0);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) issue(c, c);
+  wait_vmcnt<2 * NB + 2 * C::kOpsPerChunk>();  // chunks 0 and 1 have landed
   lds_barrier();
-  for (int c0 = 0; c0 < nchunks; c0 += 4) {
+  read_frags(0, 0);
+  for (int c0 = 0; c0 < nchunks; c0 += kStages) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < kStages; ++s) {
       const int c = c0 + s;
-      issue_h(s & 1, c + 2);
-      issue_w((s + 3) & 3, c + 3);
-      bf16x8 wv[NBW];
+      issue((s + 4) % kStages, c + 4);
+      read_frags((s + 1) & 1, (s + 1) % kStages);
       const bool live = c < nchunks;
 #pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) wv[nb] = live ? wreg[s][nb] : bf16x8{};
+      for (int ks = 0; ks < 2; ++ks) {
+        bf16x8 wv[NB];
 #pragma unroll
-      for (int mb = 0; mb < MBW; ++mb) {
-        const bf16x8 a =
-            __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(abuf[s & 1] + (mb * 64 + lane) * 16));
+        for (int nb = 0; nb < NB; ++nb) wv[nb] = live ? wreg[s][nb][ks] : bf16x8{};
 #pragma unroll
-        for (int nb = 0; nb < NBW; ++nb) acc[mb][nb] = mfma16x16x32(wv[nb], a, acc[mb][nb]);
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma32x32x16(wv[nb], af[s & 1][2 * mb + ks], acc[mb][nb]);
       }
-      stage((s + 1) & 1, (s + 1) & 1);
+      wait_vmcnt<C::kInFlight>();
       lds_barrier();
     }
   }
-  tile_epilogue<MBW, NBW>(acc, M, V, ntiles, tile, m0, blk0, logits, partials, red);
+  tile_epilogue32<MB, NB>(acc, M, V, ntiles, tile, m0, blk0, logits, partials, red);
+}
+
+// Hidden rows [M][K] -> fragments [K/16][ceil(M/32)][64 lanes][8]: lane l of
+// fragment (k16, mb) holds row mb*32 + l%32, k 16*k16 + 8*(l/32) .. +8; rows
+// past M are zero.  One thread per 16-byte piece, writes coalesced.
+__global__ __launch_bounds__(kVThreads)
+void pack_hidden_kernel(int M, int K, const uint16_t* __restrict__ hidden, uint16_t* __restrict__ out) {
+  const int mbt = (M + 31) / 32;
+  const int64_t pieces = (int64_t)(K / 16) * mbt * 64;
+  for (int64_t i = (int64_t)blockIdx.x * kVThreads + threadIdx.x; i < pieces; i += (int64_t)gridDim.x * kVThreads) {
+    const int lane = (int)(i & 63);
+    const int64_t f = i >> 6;
+    const int mb = (int)(f % mbt);
+    const int k16 = (int)(f / mbt);
+    const int row = mb * 32 + (lane & 31);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row < M) v = *reinterpret_cast<const u32x4*>(hidden + (int64_t)row * K + k16 * 16 + (lane >> 5) * 8);
+    *reinterpret_cast<u32x4*>(out + i * 8) = v;
+  }
 }
 
 // float32 path: 64 rows x 64 vocabulary entries per workgroup, LDS-tiled FMA.
@@ -429,26 +588,30 @@ hipError_t launch_shallow_mb(const VocabPlan& p, const void* hidden, const void*
   return launch_shallow<MB, 32>(p, hidden, w, logits, partials, stream, e0, e1);
 }
 
-template <int MBW, int NBW>
+template <int MB, int NB>
 hipError_t launch_deep(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
-                       hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  const dim3 grid(p.ntiles, p.mtiles), block(kVThreads);
-  const uint16_t* h = static_cast<const uint16_t*>(hidden);
+                       uint16_t* hpacked, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  const int64_t pieces = (int64_t)(p.K / 16) * ((p.M + 31) / 32) * 64;
+  const int pblocks = (int)std::min<int64_t>((pieces + kVThreads - 1) / kVThreads, 4096);
+  hipExtLaunchKernelGGL(pack_hidden_kernel, dim3(pblocks), dim3(kVThreads), 0, stream, e0, nullptr, 0, p.M, p.K,
+                        static_cast<const uint16_t*>(hidden), hpacked);
+  const dim3 grid((p.ntiles + 7) / 8 * 8 * p.mtiles), block(kVThreads);
   const uint16_t* wv = static_cast<const uint16_t*>(w);
   if (p.packed)
-    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MBW, NBW, true>), grid, block, 0, stream, e0, e1, 0, p.M, p.K,
-                          p.V, p.ntiles, h, wv, logits, partials);
+    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, true>), grid, block, 0, stream, nullptr, e1, 0, p.M, p.K,
+                          p.V, p.ntiles, p.mtiles, hpacked, wv, logits, partials);
   else
-    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MBW, NBW, false>), grid, block, 0, stream, e0, e1, 0, p.M, p.K,
-                          p.V, p.ntiles, h, wv, logits, partials);
+    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, false>), grid, block, 0, stream, nullptr, e1, 0, p.M, p.K,
+                          p.V, p.ntiles, p.mtiles, hpacked, wv, logits, partials);
   return hipGetLastError();
 }
 
-// Largest row-block count per M-tile of the deep schedule: the accumulators
-// (MBW x NBW x 4 registers) stay within the 256 accumulation registers.
-constexpr int kDeepMaxBlocks2 = 20;
-constexpr int kDeepMaxBlocks4 = 16;
-constexpr int kShallowMaxBlocks = 4;
+// Deep schedule: 32-entry vocabulary blocks per wave (NB) and the most 32-row
+// blocks per M-tile, keeping the accumulators (MB x NB x 16 registers) within
+// 256 registers next to the load rings.
+constexpr int kDeepMaxBlocks1 = 12;
+constexpr int kDeepMaxBlocks2 = 7;
+constexpr int kShallowMaxBlocks = 4;  // 16-row blocks of the shallow schedule
 
 }  // namespace
 
@@ -482,25 +645,35 @@ VocabPlan vocab_plan(int dtype, int M, int K, int V, bool packed) {
     p.nbw = 1;
     p.mtiles = 1;
   } else {
-    // Four blocks per wave once the vocabulary still gives at least one
-    // 256-wide tile per CU; two otherwise.
+    // Two 32-entry blocks per wave (half the LDS reads per MFMA) when the
+    // vocabulary gives at least one 256-wide tile per CU, or when the rows
+    // need M-tiles anyway; one block per wave for small vocabularies.
+    const int blocks32 = (M + 31) / 32;
     p.deep = true;
-    p.nbw = V >= 256 * 256 ? 4 : 2;
-    const int cap = p.nbw == 4 ? kDeepMaxBlocks4 : kDeepMaxBlocks2;
-    p.mtiles = (blocks + cap - 1) / cap;
-    p.mblocks = (blocks + p.mtiles - 1) / p.mtiles;
+    p.nbw = (V >= 256 * 256 || blocks32 > kDeepMaxBlocks2) ? 4 : 2;  // in 16-entry blocks
+    const int cap = p.nbw == 4 ? kDeepMaxBlocks2 : kDeepMaxBlocks1;
+    p.mtiles = (blocks32 + cap - 1) / cap;
+    p.mblocks = (blocks32 + p.mtiles - 1) / p.mtiles;  // 32-row blocks
   }
   p.tile_n = 64 * p.nbw;
   p.ntiles = (V + p.tile_n - 1) / p.tile_n;
   return p;
 }
 
-size_t vocab_partial_bytes(const VocabPlan& p) {
-  return sizeof(float2) * static_cast<size_t>(p.M) * p.ntiles + 256;
+static size_t partial_bytes(const VocabPlan& p) {
+  return (sizeof(float2) * static_cast<size_t>(p.M) * p.ntiles + 255) / 256 * 256;
+}
+
+size_t vocab_workspace_bytes(const VocabPlan& p) {
+  size_t b = partial_bytes(p);
+  if (p.deep) b += sizeof(uint16_t) * static_cast<size_t>(p.K) * ((static_cast<size_t>(p.M) + 31) / 32) * 32;
+  return b;
 }
 
 hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w, float* logits,
-                        float2* partials, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+                        void* workspace, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  float2* partials = static_cast<float2*>(workspace);
+  uint16_t* hpacked = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + partial_bytes(p));
   if (dtype == 0) {
     hipExtLaunchKernelGGL(vocab_f32_kernel, dim3(p.ntiles, p.mtiles), dim3(kVThreads), 0, stream, e0, e1, 0, p.M, p.K,
                           p.V, p.ntiles, static_cast<const float*>(hidden), static_cast<const float*>(w), logits,
@@ -517,17 +690,16 @@ hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const
     }
   }
 #define SDV_D(B, N) \
-  case B: return launch_deep<B, N>(p, hidden, w, logits, partials, stream, e0, e1);
+  case B: return launch_deep<B, N>(p, hidden, w, logits, partials, hpacked, stream, e0, e1);
   if (p.nbw == 4) {
     switch (p.mblocks) {
-      SDV_D(5, 4) SDV_D(6, 4) SDV_D(7, 4) SDV_D(8, 4) SDV_D(9, 4) SDV_D(10, 4) SDV_D(11, 4) SDV_D(12, 4)
-      SDV_D(13, 4) SDV_D(14, 4) SDV_D(15, 4) SDV_D(16, 4)
+      SDV_D(2, 2) SDV_D(3, 2) SDV_D(4, 2) SDV_D(5, 2) SDV_D(6, 2) SDV_D(7, 2)
       default: return hipErrorInvalidValue;
     }
   }
   switch (p.mblocks) {
-    SDV_D(5, 2) SDV_D(6, 2) SDV_D(7, 2) SDV_D(8, 2) SDV_D(9, 2) SDV_D(10, 2) SDV_D(11, 2) SDV_D(12, 2)
-    SDV_D(13, 2) SDV_D(14, 2) SDV_D(15, 2) SDV_D(16, 2) SDV_D(17, 2) SDV_D(18, 2) SDV_D(19, 2) SDV_D(20, 2)
+    SDV_D(2, 1) SDV_D(3, 1) SDV_D(4, 1) SDV_D(5, 1) SDV_D(6, 1) SDV_D(7, 1) SDV_D(8, 1) SDV_D(9, 1)
+    SDV_D(10, 1) SDV_D(11, 1) SDV_D(12, 1)
     default: return hipErrorInvalidValue;
   }
 #undef SDV_D
