@@ -417,22 +417,20 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
 
   bf16x8 wreg[kStages][NB][2];
   bf16x8 af[2][C::kFrags];
-  auto issue = [&](int slot, int c) {
+  // Memory operation j (0 <= j < kOpsPerChunk) of chunk c: the hidden DMAs
+  // first, then the W loads, always in this order (the vmcnt accounting
+  // relies on it).
+  auto issue_op = [&](int j, int slot, int c) {
     c = min(c, nchunks - 1);
-#pragma unroll
-    for (int i = 0; i < ND; ++i)
-      dma_16B_to_lds(hsrc[i] + c * hstep, abuf(slot) + hoff[i]);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) wreg[slot][nb][ks] = load_bf16x8(wsrc[nb][ks] + (int64_t)c * wstep);
-    __builtin_amdgcn_sched_barrier(0);
+    if (j < ND) {
+      dma_16B_to_lds(hsrc[j] + c * hstep, abuf(slot) + hoff[j]);
+    } else {
+      const int nb = (j - ND) >> 1, ks = (j - ND) & 1;
+      wreg[slot][nb][ks] = load_bf16x8(wsrc[nb][ks] + (int64_t)c * wstep);
+    }
   };
-  auto read_frags = [&](int set, int slot) {
-#pragma unroll
-    for (int f = 0; f < C::kFrags; ++f)
-      af[set][f] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(abuf(slot) + f * 1024 + lane * 16));
+  auto read_frag = [&](int set, int slot, int f) {
+    af[set][f] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(abuf(slot) + f * 1024 + lane * 16));
   };
 
   f32x16 acc[MB][NB];
@@ -444,17 +442,21 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
 #pragma unroll
-  for (int c = 0; c < 4; ++c) issue(c, c);
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int j = 0; j < C::kOpsPerChunk; ++j) issue_op(j, c, c);
   wait_vmcnt<2 * NB + 2 * C::kOpsPerChunk>();  // chunks 0 and 1 have landed
   lds_barrier();
-  read_frags(0, 0);
+#pragma unroll
+  for (int f = 0; f < C::kFrags; ++f) read_frag(0, 0, f);
   for (int c0 = 0; c0 < nchunks; c0 += kStages) {
 #pragma unroll
     for (int s = 0; s < kStages; ++s) {
       const int c = c0 + s;
-      issue((s + 4) % kStages, c + 4);
-      read_frags((s + 1) & 1, (s + 1) % kStages);
       const bool live = c < nchunks;
+      // One MFMA, then one other instruction: the loads of chunk c+4 and the
+      // fragment reads of chunk c+1 fill the issue slots between MFMAs, so a
+      // single wave keeps the matrix pipe busy while they go out.
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         bf16x8 wv[NB];
@@ -463,8 +465,19 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma32x32x16(wv[nb], af[s & 1][2 * mb + ks], acc[mb][nb]);
+          for (int nb = 0; nb < NB; ++nb) {
+            const int i = (ks * MB + mb) * NB + nb;
+            acc[mb][nb] = mfma32x32x16(wv[nb], af[s & 1][2 * mb + ks], acc[mb][nb]);
+            if (i < C::kOpsPerChunk)
+              issue_op(i, (s + 4) % kStages, c + 4);
+            else if (i - C::kOpsPerChunk < C::kFrags)
+              read_frag((s + 1) & 1, (s + 1) % kStages, i - C::kOpsPerChunk);
+            __builtin_amdgcn_sched_barrier(0);
+          }
       }
+#pragma unroll
+      for (int f = 2 * MB * NB - C::kOpsPerChunk; f < C::kFrags; ++f)
+        if (f >= 0) read_frag((s + 1) & 1, (s + 1) % kStages, f);
       wait_vmcnt<C::kInFlight>();
       lds_barrier();
     }
