@@ -44,7 +44,7 @@ int check_dims(const sd_dims_t* d) {
   return SD_OK;
 }
 
-AttnShape attn_shape(const sd_dims_t* d, float scale) {
+AttnShape attn_shape(const sd_dims_t* d, float scale, const int32_t* kv_len = nullptr) {
   AttnShape s;
   s.G = d->gamma + 1;
   s.Hq = d->n_q_heads;
@@ -52,7 +52,10 @@ AttnShape attn_shape(const sd_dims_t* d, float scale) {
   s.D = d->head_dim;
   s.group = d->n_q_heads / d->n_kv_heads;
   s.rows = s.G * s.group;
-  s.chunk_keys = attn_chunk_keys(d->dtype, s.rows, s.D);
+  int64_t total = 0;
+  if (kv_len != nullptr)
+    for (int b = 0; b < d->batch; ++b) total += kv_len[b];
+  s.chunk_keys = attn_chunk_keys(d->dtype, s.rows, s.Hkv, total);
   s.scale_log2 = scale * 1.4426950408889634f;
   return s;
 }
@@ -91,7 +94,7 @@ int hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
 int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* v, const int64_t* kv_off,
                   const int32_t* kv_len, float scale, void* out, void* ws, hipStream_t stream,
                   hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
-  const AttnShape s = attn_shape(d, scale);
+  const AttnShape s = attn_shape(d, scale, kv_len);
   const int64_t chunks = total_chunks(kv_len, d->batch, s.chunk_keys);
   const AttnPartials parts = attn_carve(ws, chunks, s.Hkv, s.rows, s.D);
   int64_t chunk_base = 0;
@@ -171,8 +174,7 @@ extern "C" {
 
 size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
   if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
-  const AttnShape s = attn_shape(dims, 1.f);
-  const int64_t chunks = int64_t(dims->batch) * ((int64_t(max_kv_len) + s.chunk_keys - 1) / s.chunk_keys);
+  const int64_t chunks = attn_max_chunks(dims->dtype, dims->n_kv_heads, dims->batch, max_kv_len);
   return std::max(attention_ws(dims, chunks), logits_ws(dims) + accept_ws(dims));
 }
 
@@ -188,7 +190,7 @@ int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool
   if (!(scale == scale)) return SD_ERR_INVALID_ARGUMENT;
   st = check_kv(dims, kv_off, kv_len);
   if (st != SD_OK) return st;
-  const AttnShape s = attn_shape(dims, scale);
+  const AttnShape s = attn_shape(dims, scale, kv_len);
   if (workspace_bytes < attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)))
     return SD_ERR_WORKSPACE;
   return run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, out, workspace,
@@ -245,7 +247,7 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   if (st != SD_OK) return st;
   st = check_kv(dims, kv_off, kv_len);
   if (st != SD_OK) return st;
-  const AttnShape s = attn_shape(dims, scale);
+  const AttnShape s = attn_shape(dims, scale, kv_len);
   const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
                                logits_ws(dims) + accept_ws(dims));
   if (workspace_bytes < need) return SD_ERR_WORKSPACE;

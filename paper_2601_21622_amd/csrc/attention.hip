@@ -6,16 +6,25 @@
 // "rows" of one KV head, and every key/value vector is read from HBM once for
 // all of them.
 //
-// Work split: one workgroup per (request chunk of `chunk_keys` keys, KV head).
-// Its four waves stream interleaved 32-key tiles straight from HBM:
-//   S^T = K Q^T on MFMA 16x16x32 bf16 (K rows are the A operand, loaded in
-//       place from the [L][D] layout; the Q fragments stay in registers),
-//   online softmax in the log2 domain, each lane owning one query row,
-//   O^T += V^T P^T on MFMA, with P used straight from the S^T accumulator
-//       layout and V transposed through a wave-private LDS tile.
-// The four waves then merge their (max, sum, O) through LDS and one partial
-// per workgroup goes to the workspace; a combine kernel merges the chunks of
-// each request in fixed order and writes O in the input dtype.
+// Work split: one wave per work item (request chunk of `chunk_keys` keys, KV
+// head); a workgroup holds four independent items, so no wave waits on
+// another.  The host picks the chunk length from the total work so that the
+// items fill the GPU about twice over.  Two bf16 kernels:
+//   * one 16-row block (multi-head attention: the G queries of one head):
+//     each wave loads the next 32-key tile's K fragments and V rows into its
+//     other register set while it folds in the current tile; V goes through a
+//     wave-private LDS tile so that the transposing read ds_read_b64_tr_b16
+//     hands each lane its V^T fragment;
+//   * several 16-row blocks (grouped-query attention): K and V tiles go from
+//     HBM into wave-private LDS stages by DMA (no registers, completion
+//     tracked with explicit vmcnt waits), again one tile ahead.
+// Both compute S^T = K Q^T and O^T += V^T P^T on MFMA 16x16x32 bf16 (the Q
+// fragments stay in registers, P comes straight from the S^T accumulator
+// layout) with the online softmax in the log2 domain, each lane owning one
+// query row.  Each item writes one partial (max, sum, O) to the workspace; a
+// combine kernel merges the chunks of each request in fixed order and writes
+// O in the input dtype.  LDS tiles keep rows whole but rotate their 16-byte
+// pieces so that the fragment reads are free of bank conflicts.
 #include <hip/hip_ext.h>
 
 #include "common.h"
@@ -28,6 +37,14 @@ namespace {
 constexpr int kAttnThreads = 256;
 constexpr int kAttnWaves = 4;
 constexpr int kTile = 32;
+constexpr int kF32ChunkKeys = 128;
+constexpr int kMinChunkKeys = 512;
+constexpr int kMaxChunkKeys = 4096;
+// Work items aimed for: about one per resident wave of the one-block kernel
+// (2048 slots), about four per resident wave of the multi-block kernel
+// (1024 slots, whose row groups come with long, uneven contexts).
+constexpr int64_t kAttnTargetItemsOne = 2048;
+constexpr int64_t kAttnTargetItemsMany = 4096;
 
 
 __device__ __forceinline__ int find_request(const AttnBatch& bt, int c) {
@@ -39,34 +56,190 @@ __device__ __forceinline__ int find_request(const AttnBatch& bt, int c) {
   return lo;
 }
 
-template <int D>
-struct VStage {
-  static constexpr int kStride = D + 4;  // uint16 per staged row: 4 row groups hit distinct LDS banks
-  static constexpr int kWaveElems = kTile * kStride;
+// K or V tile of one wave in LDS: 32 keys x D, row r (D*2 bytes) holding its
+// 16-byte pieces rotated by rot(r) pieces.  K: rot(r) = r*P/16 (mod P), so a
+// piece read by 16 consecutive keys hits 16 distinct bank groups.  V:
+// rot(r) = 2*(r*P/16) (mod P), so the four rows a 16-lane group touches in one
+// transposing read fall on distinct banks.
+template <int D, bool IS_V>
+struct KVTile {
+  static constexpr int kPieces = D / 8;          // 16-byte pieces per row
+  static constexpr int kBytes = kTile * D * 2;   // one tile
+  static constexpr int kRowsPerDma = 64 / kPieces;
+  static constexpr int kDmas = kTile / kRowsPerDma;  // DMA instructions per tile
+  __device__ static constexpr int rot(int r) {
+    return ((IS_V ? 2 : 1) * ((r * kPieces) >> 4)) % kPieces;
+  }
+  // Byte offset of element d of row r.
+  __device__ static constexpr int at(int r, int d) {
+    return r * D * 2 + (((d >> 3) + rot(r)) % kPieces) * 16 + (d & 7) * 2;
+  }
+  // DMA instruction i of a tile: lane l brings row r = i*kRowsPerDma +
+  // l/kPieces, the global piece that belongs in LDS slot l%kPieces.
+  __device__ static void load(const uint16_t* rows, int k0, int L, unsigned char* tile, int lane) {
+#pragma unroll
+    for (int i = 0; i < kDmas; ++i) {
+      const int r = i * kRowsPerDma + lane / kPieces;
+      const int piece = (lane % kPieces - rot(r) + kPieces) % kPieces;
+      const int key = min(k0 + r, L - 1);
+      dma_16B_to_lds_opaque(rows + (int64_t)key * D + piece * 8, tile + i * 1024);
+    }
+  }
 };
 
+// Per-wave running state of the online softmax over its query rows.
 template <int RB, int D>
-struct AttnSmem {
-  static constexpr int kRowsPad = 16 * RB;
-  static constexpr int kOStride = D + 4;
-  static constexpr size_t kStage = sizeof(uint16_t) * kAttnWaves * VStage<D>::kWaveElems;
-  static constexpr size_t kMerge = sizeof(float) * (2 * kRowsPad + kRowsPad * kOStride);
-  static constexpr size_t kBytes = kStage > kMerge ? kStage : kMerge;
+struct AttnRows {
+  bf16x8 qf[RB][D / 32];  // Q fragments, B operand of S^T = K Q^T
+  int lim[RB];            // last visible key of the lane's row (-1: padding row)
+  float m[RB], lsum[RB];  // running maximum (log2 domain) and sum
+  f32x4 o[RB][D / 16];    // running O^T blocks
 };
 
+// One step of a wave's software pipeline: start the DMAs of the next tile
+// (keys from k0_next) into (kdst, vdst), wait until only those are in flight,
+// then fold the current tile (keys from k0, staged in ksrc/vsrc) into the
+// running state.  The stage pointers are restrict-qualified, so the compiler
+// knows the new DMAs cannot write what this step reads and leaves the
+// ordering to the explicit wait.  A tile with live == false (past the wave's
+// last one) contributes nothing: all of its scores are masked.
 template <int RB, int D>
-__global__ __launch_bounds__(kAttnThreads, (RB >= 3 ? 1 : 2))
+__device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2, const uint16_t* Kb,
+                                          const uint16_t* Vb, int L, int k0_next, int k0, bool live,
+                                          unsigned char* __restrict__ kdst, unsigned char* __restrict__ vdst,
+                                          const unsigned char* __restrict__ ksrc,
+                                          const unsigned char* __restrict__ vsrc) {
+  constexpr int DS = D / 32;
+  constexpr int DB = D / 16;
+  using KT = KVTile<D, false>;
+  using VT = KVTile<D, true>;
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15;
+  const int lg = lane >> 4;
+  KT::load(Kb, k0_next, L, kdst, lane);
+  VT::load(Vb, k0_next, L, vdst, lane);
+  wait_vmcnt<KT::kDmas + VT::kDmas>();
+
+  // K fragments (A operand): lane holds key kb*16 + lr, d = ds*32 + lg*8 .. +8.
+  bf16x8 kf[2][DS];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds)
+      kf[kb][ds] = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(ksrc + KT::at(kb * 16 + lr, ds * 32 + lg * 8)));
+  f32x4 sc[RB][2];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) acc = mfma16x16x32(kf[kb][ds], st.qf[rb][ds], acc);
+      sc[rb][kb] = acc;
+    }
+
+  // Online softmax: lane owns row rb*16+lr and keys k0 + kb*16 + lg*4 + e.
+  bf16x8 pf[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    float sv[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int key = k0 + kb * 16 + lg * 4 + e;
+        float x = sc[rb][kb][e] * scale_log2;
+        x = (key > st.lim[rb] || !live) ? -INFINITY : x;
+        sv[kb * 4 + e] = x;
+        mx = fmaxf(mx, x);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mn = fmaxf(st.m[rb], mx);
+    const float alpha = exp2f(st.m[rb] - mn);
+    st.m[rb] = mn;
+    float ps = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const __bf16 pb = (__bf16)exp2f(sv[e] - mn);
+      pf[rb][e] = pb;
+      ps += (float)pb;
+    }
+    st.lsum[rb] = st.lsum[rb] * alpha + ps;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) st.o[rb][db] *= alpha;
+  }
+
+  // V^T fragments (A operand of O^T += V^T P^T): lane (lg, lr) needs
+  // d = db*16 + lr and keys {lg*4 .. +3} then {16 + lg*4 .. +3}, the
+  // P fragment's k-slots.  Lane j of the 16-lane group lg points at row
+  // 4*lg + j/4 (+16), d = db*16 + 4*(j%4) .. +3.
+  const int jr = 4 * lg + (lr >> 2);
+  const int jd = 4 * (lr & 3);
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const s16x4 lo = lds_read_tr16(vsrc + VT::at(jr, db * 16 + jd));
+    const s16x4 hi = lds_read_tr16(vsrc + VT::at(16 + jr, db * 16 + jd));
+    const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) st.o[rb][db] = mfma16x16x32(vf, pf[rb], st.o[rb][db]);
+  }
+}
+
+// Item of wave `wave` in workgroup blockIdx.x: (chunk, KV head), KV head
+// fastest.  Returns false past the last item.
+__device__ __forceinline__ bool attn_item(const AttnShape& s, const AttnBatch& bt, int& c_local, int& g) {
+  const int item = blockIdx.x * kAttnWaves + (threadIdx.x >> 6);
+  c_local = item / s.Hkv;
+  g = item - c_local * s.Hkv;
+  return c_local < bt.chunk_prefix[bt.nreq];
+}
+
+// Partial of one item: row r of slot (chunk_base + c_local)*Hkv + g.
+template <int RB, int D>
+__device__ __forceinline__ void write_partial(const AttnShape& s, const AttnBatch& bt, AttnPartials parts, int c_local,
+                                              int g, const float (&m)[RB], float (&lsum)[RB],
+                                              const f32x4 (&o)[RB][D / 16]) {
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int64_t slot = (int64_t)(bt.chunk_base + c_local) * s.Hkv + g;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    lsum[rb] += __shfl_xor(lsum[rb], 16);
+    lsum[rb] += __shfl_xor(lsum[rb], 32);
+    const int row = rb * 16 + lr;
+    if (row < s.rows) {
+      if (lg == 0) {
+        parts.m[slot * s.rows + row] = m[rb];
+        parts.l[slot * s.rows + row] = lsum[rb];
+      }
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db)
+        *reinterpret_cast<f32x4*>(parts.o + (slot * s.rows + row) * D + db * 16 + lg * 4) = o[rb][db];
+    }
+  }
+}
+
+template <int RB, int D>
+__global__ __launch_bounds__(kAttnThreads, 1)
 void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
                       const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
                       AttnPartials parts) {
   constexpr int DS = D / 32;  // 32-wide steps of the q.k contraction
   constexpr int DB = D / 16;  // 16-wide blocks of the output
-  constexpr int VS = VStage<D>::kStride;
-  using SM = AttnSmem<RB, D>;
-  __shared__ __align__(16) unsigned char smem[SM::kBytes];
+  using KT = KVTile<D, false>;
+  using VT = KVTile<D, true>;
+  constexpr size_t kStage = (size_t)kAttnWaves * kTile * D * 2;  // one stage of K or V, all waves
+  // Two stages of K and V tiles, each its own object.
+  __shared__ __align__(16) unsigned char ks0[kStage];
+  __shared__ __align__(16) unsigned char ks1[kStage];
+  __shared__ __align__(16) unsigned char vs0[kStage];
+  __shared__ __align__(16) unsigned char vs1[kStage];
 
-  const int c_local = blockIdx.x;
-  const int g = blockIdx.y;
+  int c_local, g;
+  if (!attn_item(s, bt, c_local, g)) return;
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15;  // row (or column) within a 16-block
@@ -82,8 +255,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   const uint16_t* Vb = vp + off + (int64_t)g * L * D;
 
   // Q fragments (B operand of S^T = K Q^T): lane holds row rb*16+lr, d = ds*32 + lg*8 .. +8.
-  bf16x8 qf[RB][DS];
-  int lim[RB];
+  AttnRows<RB, D> st;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int row = rb * 16 + lr;
@@ -92,179 +264,188 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
       const int h = g * s.group + (row - j * s.group);
       const uint16_t* qrow = q + (((int64_t)req * s.G + j) * s.Hq + h) * D;
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) qf[rb][ds] = load_bf16x8(qrow + ds * 32 + lg * 8);
-      lim[rb] = L - s.G + j;
+      for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = load_bf16x8(qrow + ds * 32 + lg * 8);
+      st.lim[rb] = L - s.G + j;
     } else {
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) qf[rb][ds] = bf16x8{};
-      lim[rb] = -1;
+      for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = bf16x8{};
+      st.lim[rb] = -1;
     }
+    st.m[rb] = kNegBig;
+    st.lsum[rb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) st.o[rb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  float m[RB], lsum[RB];
-  f32x4 o[RB][DB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    m[rb] = kNegBig;
-    lsum[rb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[rb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  uint16_t* vst = reinterpret_cast<uint16_t*>(smem) + wave * VStage<D>::kWaveElems;
+  // Tile i of the item starts at key k_begin + 32i; the load past the last
+  // tile re-reads it (in bounds, never folded in).  Tile i+1 loads while
+  // tile i is folded in; the two stages swap after every tile.
   const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
-  constexpr int LPR = D / 8;      // lanes per staged V row (16 bytes each)
-  constexpr int KPI = 64 / LPR;   // V rows per wave-wide load
+  unsigned char* k0s = ks0 + wave * KT::kBytes;
+  unsigned char* k1s = ks1 + wave * KT::kBytes;
+  unsigned char* v0s = vs0 + wave * VT::kBytes;
+  unsigned char* v1s = vs1 + wave * VT::kBytes;
+  auto key0 = [&](int i) { return k_begin + min(i, ntiles - 1) * kTile; };
+  KT::load(Kb, key0(0), L, k0s, lane);
+  VT::load(Vb, key0(0), L, v0s, lane);
+  for (int i = 0; i < ntiles; ++i) {
+    attn_step<RB, D>(st, s.scale_log2, Kb, Vb, L, key0(i + 1), key0(i), true, k1s, v1s, k0s, v0s);
+    unsigned char* t = k0s;
+    k0s = k1s;
+    k1s = t;
+    t = v0s;
+    v0s = v1s;
+    v1s = t;
+  }
+  wait_vmcnt<0>();
+  write_partial<RB, D>(s, bt, parts, c_local, g, st.m, st.lsum, st.o);
+}
 
-  constexpr int NV = kTile / KPI;
-  for (int t = wave; t < ntiles; t += kAttnWaves) {
-    const int k0 = k_begin + t * kTile;
-    // K fragments (A operand): lane holds key k0 + kb*16 + lr; keys past L are clamped and masked.
-    bf16x8 kf[2][DS];
+// Register-staged variant for one 16-row block (multi-head attention, where
+// each KV head serves only the G queries of its own head).  The work per
+// tile is small there, so the kernel keeps two workgroups per CU and stages
+// through registers: whole K and V rows go register -> wave-private LDS tiles
+// (rotated rows) -> MFMA fragments.  All loads land in registers, so the
+// compiler's own vmcnt accounting covers the pipeline.
+template <int D>
+__global__ __launch_bounds__(kAttnThreads, 2)
+void attn_bf16_mha_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
+                          const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
+                          AttnPartials parts) {
+  constexpr int DS = D / 32;
+  constexpr int DB = D / 16;
+  constexpr int LPR = D / 8;       // lanes per V row (16 bytes each)
+  constexpr int KPI = 64 / LPR;    // V rows per wave-wide load
+  constexpr int NV = kTile / KPI;  // V loads per tile
+  using VT = KVTile<D, true>;
+  using KT = KVTile<D, false>;
+  __shared__ __align__(16) unsigned char vsm[kAttnWaves * VT::kBytes];
+  __shared__ __align__(16) unsigned char ksm[kAttnWaves * KT::kBytes];
+
+  int c_local, g;
+  if (!attn_item(s, bt, c_local, g)) return;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15;
+  const int lg = lane >> 4;
+
+  const int b = find_request(bt, c_local);
+  const int L = bt.kv_len[b];
+  const int64_t off = bt.kv_off[b];
+  const int req = bt.req0 + b;
+  const int k_begin = (c_local - bt.chunk_prefix[b]) * s.chunk_keys;
+  const int k_end = min(L, k_begin + s.chunk_keys);
+  const uint16_t* Kb = kp + off + (int64_t)g * L * D;
+  const uint16_t* Vb = vp + off + (int64_t)g * L * D;
+
+  bf16x8 qf[DS];
+  int lim;
+  if (lr < s.rows) {
+    const int j = lr / s.group;
+    const int h = g * s.group + (lr - j * s.group);
+    const uint16_t* qrow = q + (((int64_t)req * s.G + j) * s.Hq + h) * D;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) qf[ds] = load_bf16x8(qrow + ds * 32 + lg * 8);
+    lim = L - s.G + j;
+  } else {
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) qf[ds] = bf16x8{};
+    lim = -1;
+  }
+  float m[1] = {kNegBig}, lsum[1] = {0.f};
+  f32x4 o[1][DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) o[0][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
+  unsigned char* vt = vsm + wave * VT::kBytes;
+  unsigned char* kt = ksm + wave * KT::kBytes;
+  auto key0 = [&](int i) { return k_begin + min(i, ntiles - 1) * kTile; };
+
+  // Whole K and V rows, KPI rows per wave-wide load (full cache lines),
+  // streamed with the nontemporal hint: every row is read once.
+  u32x4 kr[2][NV], vr[2][NV];
+  auto issue = [&](int set, int k0) {
+#pragma unroll
+    for (int it = 0; it < NV; ++it) {
+      const int64_t row = (int64_t)min(k0 + it * KPI + lane / LPR, L - 1) * D + (lane % LPR) * 8;
+      kr[set][it] = load_u32x4_stream(Kb + row);
+      vr[set][it] = load_u32x4_stream(Vb + row);
+    }
+  };
+  // Fold tile (set, k0) into the running state; live == false masks it.
+  auto fold = [&](int set, int k0, bool live) {
+#pragma unroll
+    for (int it = 0; it < NV; ++it) {
+      const int r = it * KPI + lane / LPR, d = (lane % LPR) * 8;
+      *reinterpret_cast<u32x4*>(kt + KT::at(r, d)) = kr[set][it];
+      *reinterpret_cast<u32x4*>(vt + VT::at(r, d)) = vr[set][it];
+    }
+    // K fragments (A operand): lane holds key kb*16 + lr, d = ds*32 + lg*8 .. +8.
+    f32x4 sc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      const int key = min(k0 + kb * 16 + lr, L - 1);
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = load_bf16x8(Kb + (int64_t)key * D + ds * 32 + lg * 8);
-    }
-    // V rows of the tile, coalesced 16-byte loads, staged row-major in LDS below.
-    u32x4 vreg[NV];
-#pragma unroll
-    for (int it = 0; it < NV; ++it) {
-      const int key = min(k0 + it * KPI + lane / LPR, L - 1);
-      vreg[it] = *reinterpret_cast<const u32x4*>(Vb + (int64_t)key * D + (lane % LPR) * 8);
-    }
-
-    f32x4 st[RB][2];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds) acc = mfma16x16x32(kf[kb][ds], qf[rb][ds], acc);
-        st[rb][kb] = acc;
+      for (int ds = 0; ds < DS; ++ds) {
+        const bf16x8 kf =
+            __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kt + KT::at(kb * 16 + lr, ds * 32 + lg * 8)));
+        acc = mfma16x16x32(kf, qf[ds], acc);
       }
-
-#pragma unroll
-    for (int it = 0; it < NV; ++it) {
-      uint16_t* dst = vst + (it * KPI + lane / LPR) * VS + (lane % LPR) * 8;
-      reinterpret_cast<u32x2*>(dst)[0] = u32x2{vreg[it][0], vreg[it][1]};
-      reinterpret_cast<u32x2*>(dst)[1] = u32x2{vreg[it][2], vreg[it][3]};
+      sc[kb] = acc;
     }
-
-    // Online softmax: lane owns row rb*16+lr and keys k0 + kb*16 + lg*4 + i.
-    bf16x8 pf[RB];
+    float sv[8];
+    float mx = -INFINITY;
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      float sv[8];
-      float mx = -INFINITY;
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = k0 + kb * 16 + lg * 4 + i;
-          float x = st[rb][kb][i] * s.scale_log2;
-          x = key > lim[rb] ? -INFINITY : x;
-          sv[kb * 4 + i] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mn = fmaxf(m[rb], mx);
-      const float alpha = exp2f(m[rb] - mn);
-      m[rb] = mn;
-      float ps = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const __bf16 pb = (__bf16)exp2f(sv[e] - mn);
-        pf[rb][e] = pb;
-        ps += (float)pb;
+      for (int e = 0; e < 4; ++e) {
+        const int key = k0 + kb * 16 + lg * 4 + e;
+        float x = sc[kb][e] * s.scale_log2;
+        x = (key > lim || !live) ? -INFINITY : x;
+        sv[kb * 4 + e] = x;
+        mx = fmaxf(mx, x);
       }
-      lsum[rb] = lsum[rb] * alpha + ps;
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mn = fmaxf(m[0], mx);
+    const float alpha = exp2f(m[0] - mn);
+    m[0] = mn;
+    bf16x8 pf;
+    float ps = 0.f;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+    for (int e = 0; e < 8; ++e) {
+      const __bf16 pb = (__bf16)exp2f(sv[e] - mn);
+      pf[e] = pb;
+      ps += (float)pb;
     }
-
-    lds_wait();
-    // V^T fragments (A operand of O^T += V^T P^T): lane holds d = db*16 + lr and the
-    // 8 keys {lg*4 .. lg*4+3, 16+lg*4 .. 16+lg*4+3} matching the P fragment's k-slots.
+    lsum[0] = lsum[0] * alpha + ps;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[0][db] *= alpha;
+    const int jr = 4 * lg + (lr >> 2);
+    const int jd = 4 * (lr & 3);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      bf16x8 vf;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int kl = (e < 4) ? (lg * 4 + e) : (16 + lg * 4 + e - 4);
-        vf[e] = __builtin_bit_cast(__bf16, vst[kl * VS + db * 16 + lr]);
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) o[rb][db] = mfma16x16x32(vf, pf[rb], o[rb][db]);
+      const s16x4 lo = lds_read_tr16(vt + VT::at(jr, db * 16 + jd));
+      const s16x4 hi = lds_read_tr16(vt + VT::at(16 + jr, db * 16 + jd));
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      o[0][db] = mfma16x16x32(vf, pf, o[0][db]);
     }
-    lds_wait();
-  }
+  };
 
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    lsum[rb] += __shfl_xor(lsum[rb], 16);
-    lsum[rb] += __shfl_xor(lsum[rb], 32);
+  // Tile i+1 loads while tile i is folded in; the body always folds two
+  // tiles (the second masked when the count is odd), so no branch separates
+  // a load from its use.
+  issue(0, key0(0));
+  for (int i = 0; i < ntiles; i += 2) {
+    issue(1, key0(i + 1));
+    __builtin_amdgcn_sched_barrier(0);  // keep the next tile's loads ahead of this tile's work
+    fold(0, key0(i), true);
+    issue(0, key0(i + 2));
+    __builtin_amdgcn_sched_barrier(0);
+    fold(1, key0(i + 1), i + 1 < ntiles);
   }
-
-  // Merge the four waves through LDS, one after the other (fixed order).
-  float* mm = reinterpret_cast<float*>(smem);
-  float* ml = mm + SM::kRowsPad;
-  float* mo = ml + SM::kRowsPad;
-  __syncthreads();
-  for (int turn = 0; turn < kAttnWaves; ++turn) {
-    if (wave == turn) {
-      if (turn > 0) {
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const int row = rb * 16 + lr;
-          const float m2 = mm[row], l2 = ml[row];
-          const float mn = fmaxf(m[rb], m2);
-          const float a1 = exp2f(m[rb] - mn), a2 = exp2f(m2 - mn);
-          m[rb] = mn;
-          lsum[rb] = lsum[rb] * a1 + l2 * a2;
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const f32x4 o2 = *reinterpret_cast<const f32x4*>(mo + row * SM::kOStride + db * 16 + lg * 4);
-            o[rb][db] = o[rb][db] * a1 + o2 * a2;
-          }
-        }
-      }
-      if (turn < kAttnWaves - 1) {
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const int row = rb * 16 + lr;
-          if (lg == 0) {
-            mm[row] = m[rb];
-            ml[row] = lsum[rb];
-          }
-#pragma unroll
-          for (int db = 0; db < DB; ++db)
-            *reinterpret_cast<f32x4*>(mo + row * SM::kOStride + db * 16 + lg * 4) = o[rb][db];
-        }
-      }
-    }
-    __syncthreads();
-  }
-
-  if (wave == kAttnWaves - 1) {
-    const int64_t slot = (int64_t)(bt.chunk_base + c_local) * s.Hkv + g;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int row = rb * 16 + lr;
-      if (row < s.rows) {
-        if (lg == 0) {
-          parts.m[slot * s.rows + row] = m[rb];
-          parts.l[slot * s.rows + row] = lsum[rb];
-        }
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-          *reinterpret_cast<f32x4*>(parts.o + (slot * s.rows + row) * D + db * 16 + lg * 4) = o[rb][db];
-      }
-    }
-  }
+  write_partial<1, D>(s, bt, parts, c_local, g, m, lsum, o);
 }
 
 // float32 path (small shapes): one workgroup per (chunk, KV head); scores and
@@ -381,8 +562,9 @@ void attn_combine_kernel(const AttnShape s, const AttnBatch bt, AttnPartials par
 template <int RB, int D>
 hipError_t launch_bf16(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                        const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  hipExtLaunchKernelGGL((attn_bf16_kernel<RB, D>), dim3(nchunks, s.Hkv), dim3(kAttnThreads), 0, stream, e0, e1, 0,
-                        s, bt, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+  const int items = nchunks * s.Hkv;
+  hipExtLaunchKernelGGL((attn_bf16_kernel<RB, D>), dim3((items + kAttnWaves - 1) / kAttnWaves), dim3(kAttnThreads), 0,
+                        stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                         static_cast<const uint16_t*>(v), parts);
   return hipGetLastError();
 }
@@ -391,7 +573,11 @@ template <int D>
 hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                        const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   switch (rb) {
-    case 1: return launch_bf16<1, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 1:
+      hipExtLaunchKernelGGL(attn_bf16_mha_kernel<D>, dim3((nchunks * s.Hkv + kAttnWaves - 1) / kAttnWaves),
+                            dim3(kAttnThreads), 0, stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q),
+                            static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), parts);
+      return hipGetLastError();
     case 2: return launch_bf16<2, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     case 3: return launch_bf16<3, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     case 4: return launch_bf16<4, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
@@ -405,13 +591,25 @@ hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchu
 
 }  // namespace
 
-int attn_chunk_keys(int dtype, int rows, int head_dim) {
-  (void)head_dim;
-  if (dtype == 0) return 128;
-  // Larger row groups write larger partials; longer chunks amortise them.
-  if (rows <= 16) return 512;
-  if (rows <= 32) return 1024;
-  return 2048;
+int attn_chunk_keys(int dtype, int rows, int Hkv, int64_t total_keys) {
+  if (dtype == 0) return kF32ChunkKeys;
+  // A whole number of 32-key tiles; never so short that an item's start-up
+  // (query rows, first tile) outweighs its streaming.
+  const int64_t target = rows <= 16 ? kAttnTargetItemsOne : kAttnTargetItemsMany;
+  const int64_t per = (total_keys * Hkv + target - 1) / target;
+  const int64_t c = (per + kTile - 1) / kTile * kTile;
+  return (int)std::min<int64_t>(kMaxChunkKeys, std::max<int64_t>(kMinChunkKeys, c));
+}
+
+int64_t attn_max_chunks(int dtype, int Hkv, int B, int64_t max_kv_len) {
+  if (dtype == 0) return (int64_t)B * ((max_kv_len + kF32ChunkKeys - 1) / kF32ChunkKeys);
+  // chunks = sum_b ceil(L_b / C) <= sum(L)/C + B, with C >= sum(L)*Hkv/target
+  // unless C is capped at kMaxChunkKeys, and never more than with C at its floor.
+  const int64_t by_floor = (int64_t)B * ((max_kv_len + kMinChunkKeys - 1) / kMinChunkKeys);
+  const int64_t target = std::max(kAttnTargetItemsOne, kAttnTargetItemsMany);
+  const int64_t by_target = std::max<int64_t>((target + Hkv - 1) / Hkv,
+                                              (int64_t)B * ((max_kv_len + kMaxChunkKeys - 1) / kMaxChunkKeys)) + B;
+  return std::min(by_floor, by_target);
 }
 
 size_t attn_partial_bytes(int64_t total_chunks, int Hkv, int rows, int D) {

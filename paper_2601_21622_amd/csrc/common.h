@@ -44,6 +44,29 @@ __device__ __forceinline__ void dma_16B_to_lds(const void* g, void* lds) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
+// Transposing LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
+// lane j supplies the address of 4 consecutive 16-bit elements x_j[0..3];
+// lane i receives {x_{i/4}[i%4], x_{4+i/4}[i%4], x_{8+i/4}[i%4], x_{12+i/4}[i%4]}.
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4;
+__device__ __forceinline__ s16x4 lds_read_tr16(const void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+}
+
+// The same DMA issued from inline assembly: the compiler neither tracks it
+// nor inserts waits for it, so the kernel's own vmcnt waits alone order it
+// against the LDS reads (the compiler's conservative handling of tracked LDS
+// DMA can otherwise drain every load in flight before an unrelated LDS read).
+// It sets M0 itself: use it only in kernels that leave M0 to it (no other LDS
+// DMA, no indexed register moves).
+// The load carries the nontemporal hint: the data is read once.
+__device__ __forceinline__ void dma_16B_to_lds_opaque(const void* g, void* lds) {
+  const uint32_t l = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(l)), "v"(g)
+               : "memory");
+}
+
 // s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {

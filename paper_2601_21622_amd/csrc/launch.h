@@ -25,7 +25,7 @@ struct AttnShape {
   int Hq, Hkv, D;
   int group;        // Hq / Hkv
   int rows;         // G * group query rows per KV head
-  int chunk_keys;   // keys per partial (one workgroup)
+  int chunk_keys;   // keys per partial (one work item)
   float scale_log2; // softmax scale * log2(e)
 };
 
@@ -37,7 +37,10 @@ struct AttnPartials {
   float* o;  // [slots][rows][D]
 };
 
-int attn_chunk_keys(int dtype, int rows, int head_dim);
+// Keys per work item (chunk), from the total number of keys over the batch;
+// attn_max_chunks bounds the chunk count for any lengths up to max_kv_len.
+int attn_chunk_keys(int dtype, int rows, int Hkv, int64_t total_keys);
+int64_t attn_max_chunks(int dtype, int Hkv, int B, int64_t max_kv_len);
 size_t attn_partial_bytes(int64_t total_chunks, int Hkv, int rows, int D);
 AttnPartials attn_carve(void* ws, int64_t total_chunks, int Hkv, int rows, int D);
 
