@@ -257,7 +257,7 @@ def main() -> int:
         "accepted_tokens_per_s": accepted / (ms_step * 1e-3),
         "emitted_per_step": emitted,
         "kernel_ms": {"attention": float(st_mean[0]), "vocab_projection": float(st_mean[1]),
-                      "accept_segments": float(st_mean[2])},
+                      "accept": float(st_mean[2])},
         "ms_per_step_with_kernel_events": ms_step_ev,
         "attention_hbm_gbps": attn_gbps,
         "vocab_hbm_gbps": vocab_gbps,

@@ -179,11 +179,12 @@ SD_API int sd_accept_resample(const sd_dims_t* dims, const float* logits_or_prob
  * sd_accept_resample on the logits and row_lse it produced.  Arguments as in
  * the three calls; attn_out, logits, row_lse are outputs the caller owns.
  *   kernel_events  (host) NULL, or 6 hipEvent_t handles (created with timing
- *                  enabled): start/stop of the attention kernel, of the
- *                  vocabulary-projection kernel and of the acceptance
- *                  segment kernel.  They are recorded by the kernel launches
- *                  themselves (no extra work on the stream), so the elapsed
- *                  time of each pair is that kernel's execution time.
+ *                  enabled): start/stop of the attention kernel (without its
+ *                  combine), of the vocabulary projection (for more than 64
+ *                  rows: hidden repacking through the projection kernel) and
+ *                  of the acceptance kernel.  They are recorded by the kernel
+ *                  launches themselves (no extra work on the stream), so the
+ *                  elapsed time of each pair is that span's execution time.
  */
 SD_API int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
                    const int64_t* kv_off, const int32_t* kv_len, float scale,

@@ -1,20 +1,22 @@
 // Acceptance test, first rejection, residual resampling and output assembly.
 //
-// Three short kernels, so that no single workgroup walks a whole vocabulary
-// row and each has one or two dependent memory round trips:
-//  accept_prepare: one workgroup per request.  Optionally folds the
-//     vocabulary kernel's per-tile statistics into the row log-sum-exp of the
-//     request's rows (one wave per row); then lanes 0..gamma-1 run the ratio
-//     tests in float64 (lane i: u < p_i(x_i) / q_i(x_i)) and a ballot gives
-//     the accept length l.
-//  accept_segments: one wave per (512-entry vocabulary segment, request) sums,
-//     in float64, the unnormalised continuation distribution over its segment:
-//     r = max(0, p_{l+1} - q_{l+1}) after a rejection, p_{gamma+1} after a
-//     full accept.
-//  accept_finalize: one wave per request prefix-sums the segment totals (Z is
-//     the last), finds the segment holding u * Z and scans it in token order
-//     for the first entry whose running sum exceeds u * Z; then writes the
-//     accept length, the emitted tokens and the new cache length.
+// Two launches.  The sums kernel runs S workgroups of 8 waves per request;
+// each workgroup
+//  1. gathers the ratio-test operands (draft token, its logit or probability,
+//     its draft probability, the draw) and, with the vocabulary kernel's
+//     per-tile statistics, folds the log-sum-exp of each of the request's rows
+//     (one wave per row; the first workgroup writes them out);
+//  2. runs the ratio tests in float64 on wave 0 (lane i: u < p_i(x_i) / q_i(x_i))
+//     and a ballot gives the accept length l (the first workgroup writes it);
+//  3. sums, per 512-entry vocabulary segment of its slice and in float64, the
+//     unnormalised continuation distribution: r = max(0, p_{l+1} - q_{l+1})
+//     after a rejection, p_{gamma+1} after a full accept; each wave issues the
+//     loads of several segments before reducing them.
+// Steps 1 and 2 are repeated by every workgroup of a request: they read a few
+// kilobytes, far less than the slice.  The pick kernel (one wave per request)
+// prefix-sums the segment totals (Z is the last), finds the segment holding
+// u * Z, scans it in token order for the first entry whose running sum
+// exceeds u * Z, and writes the emitted tokens and the new cache length.
 // p(v) = exp(logit - lse) keeps the difference exact (TwoSum) so its error is
 // a few float32 ulp, far below the 1e-6 decision band.
 #include <hip/hip_ext.h>
@@ -26,9 +28,6 @@ namespace sdv {
 
 namespace {
 
-constexpr int kSeg = 512;
-constexpr int kPerLane = kSeg / kWave;
-constexpr int kMaxSeg = 4096;  // vocabularies up to 2,097,152 entries
 
 // exp(a - b), with a - b carried exactly as s + err.
 __device__ __forceinline__ float exp_diff(float a, float b) {
@@ -40,14 +39,13 @@ __device__ __forceinline__ float exp_diff(float a, float b) {
 }
 
 struct AcceptArgs {
-  int gamma, V, nseg;
+  int gamma, V, nseg, segs_per_group;
   const float* x;        // [M][V] logits (lse != nullptr) or probabilities
   const float* lse;      // [M] or nullptr
   const float* q;        // [B][gamma][V]
   const int32_t* draft;  // [B][gamma]
   const float* u;        // [B][G]
-  double* segsum;        // [B][nseg]
-  int2* desc;            // [B] (accept length l, bits of the log-sum-exp of row l) from prepare
+  double* segsum;        // [B][nseg] segment totals
 };
 
 __device__ __forceinline__ float r_of(const AcceptArgs& a, const float* xrow, const float* qrow, float lse,
@@ -58,19 +56,116 @@ __device__ __forceinline__ float r_of(const AcceptArgs& a, const float* xrow, co
   return d > 0.f ? d : 0.f;
 }
 
-// One workgroup per request.  The ratio-test operands (draft token, its logit
-// or probability, its draft probability, the draw) are gathered first, so
-// their latency overlaps the log-sum-exp fold; with `partials` the fold of the
-// request's rows (one wave per row) writes row_lse; then wave 0 runs the tests
-// in float64 and stores (l, lse of row l) for the next two kernels.
-__global__ __launch_bounds__(512)
-void accept_prepare_kernel(const AcceptArgs a, int req0, const float2* __restrict__ partials, int ntiles) {
+constexpr int kSumWaves = 8;            // waves per workgroup of the sums kernel
+constexpr int kSeg = 512;               // vocabulary entries per segment
+constexpr int kPerLane = kSeg / kWave;  // lane holds entries sg*512 + e*64 + lane
+constexpr int kMaxSeg = 4096;           // vocabularies up to 2,097,152 entries
+constexpr int kSegBatch = 4;            // segments whose loads a wave issues together
+constexpr int kTargetGroups = 512;      // sums-kernel workgroups aimed for per launch
+
+// r over one segment, per lane (entries sg*512 + e*64 + lane): the raw loads
+// (indexes past the vocabulary clamped), then r from them.
+template <bool LSE, bool RES>
+__device__ __forceinline__ void segment_issue(const float* xrow, const float* qrow, int V, int sg,
+                                              float (&xs)[kPerLane], float (&qs)[kPerLane]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int e = 0; e < kPerLane; ++e) {
+    const int v = min(sg * kSeg + e * kWave + lane, V - 1);
+    xs[e] = __builtin_nontemporal_load(xrow + v);
+    if (RES) qs[e] = __builtin_nontemporal_load(qrow + v);
+  }
+}
+
+template <bool LSE, bool RES>
+__device__ __forceinline__ void segment_finish(float lse, int V, int sg, const float (&xs)[kPerLane],
+                                               const float (&qs)[kPerLane], float (&r)[kPerLane]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int e = 0; e < kPerLane; ++e) {
+    float v = LSE ? exp_diff(xs[e], lse) : xs[e];
+    if (RES) {
+      const float d = v - qs[e];
+      v = d > 0.f ? d : 0.f;
+    }
+    r[e] = sg * kSeg + e * kWave + lane < V ? v : 0.f;
+  }
+}
+
+template <bool LSE, bool RES>
+__device__ __forceinline__ void segment_r(const float* xrow, const float* qrow, float lse, int V, int sg,
+                                          float (&r)[kPerLane]) {
+  float xs[kPerLane], qs[kPerLane];
+  segment_issue<LSE, RES>(xrow, qrow, V, sg, xs, qs);
+  segment_finish<LSE, RES>(lse, V, sg, xs, qs, r);
+}
+
+__device__ __forceinline__ void segment_load(const AcceptArgs& a, const float* xrow, const float* qrow, float lse,
+                                             bool residual, int sg, float (&r)[kPerLane]) {
+  if (a.lse != nullptr) {
+    if (residual) segment_r<true, true>(xrow, qrow, lse, a.V, sg, r);
+    else segment_r<true, false>(xrow, qrow, lse, a.V, sg, r);
+  } else {
+    if (residual) segment_r<false, true>(xrow, qrow, lse, a.V, sg, r);
+    else segment_r<false, false>(xrow, qrow, lse, a.V, sg, r);
+  }
+}
+
+// Float64 sum of one segment: per lane in order of e, then across the lanes.
+__device__ __forceinline__ double segment_total(const float (&r)[kPerLane]) {
+  double acc = 0.0;
+#pragma unroll
+  for (int e = 0; e < kPerLane; ++e) acc += (double)r[e];
+  return wave_sum_f64(acc);
+}
+
+// Totals of segments [sg0, sg1) into out[]: wave w takes sg0 + w, sg0 + w +
+// nwaves, ..., issuing the loads of kSegBatch segments before reducing any.
+template <bool LSE, bool RES>
+__device__ __forceinline__ void segment_totals_t(const float* xrow, const float* qrow, float lse, int V, int sg0,
+                                                 int sg1, int nwaves, double* out) {
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  for (int s0 = sg0 + wave; s0 < sg1; s0 += nwaves * kSegBatch) {
+    float xs[kSegBatch][kPerLane], qs[kSegBatch][kPerLane];
+#pragma unroll
+    for (int k = 0; k < kSegBatch; ++k)
+      segment_issue<LSE, RES>(xrow, qrow, V, min(s0 + k * nwaves, sg1 - 1), xs[k], qs[k]);
+#pragma unroll
+    for (int k = 0; k < kSegBatch; ++k) {
+      const int sg = s0 + k * nwaves;
+      float r[kPerLane];
+      segment_finish<LSE, RES>(lse, V, sg, xs[k], qs[k], r);
+      const double t = segment_total(r);
+      if (lane == 0 && sg < sg1) out[sg] = t;
+    }
+  }
+}
+
+__device__ __forceinline__ void segment_totals(const AcceptArgs& a, const float* xrow, const float* qrow, float lse,
+                                               bool residual, int sg0, int sg1, int nwaves, double* out) {
+  if (a.lse != nullptr) {
+    if (residual) segment_totals_t<true, true>(xrow, qrow, lse, a.V, sg0, sg1, nwaves, out);
+    else segment_totals_t<true, false>(xrow, qrow, lse, a.V, sg0, sg1, nwaves, out);
+  } else {
+    if (residual) segment_totals_t<false, true>(xrow, qrow, lse, a.V, sg0, sg1, nwaves, out);
+    else segment_totals_t<false, false>(xrow, qrow, lse, a.V, sg0, sg1, nwaves, out);
+  }
+}
+
+// Grid (S, requests); workgroup s covers segments [s * segs_per_group, ...).
+__global__ __launch_bounds__(kSumWaves * kWave)
+void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* __restrict__ partials, int ntiles,
+                        int32_t* __restrict__ accept_len) {
   __shared__ float s_lse[kWave];
-  const int req = req0 + blockIdx.x;
+  __shared__ int s_l;
+  const int s = blockIdx.x;
+  const int req = bt.req0 + blockIdx.y;
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int G = a.gamma + 1;
 
+  // 1. Test operands first, then the row log-sum-exp fold.
   float xv = 0.f, qv = 0.f, uv = 0.f;
   bool valid = false;
   if (wave == 0 && lane < a.gamma) {
@@ -83,17 +178,19 @@ void accept_prepare_kernel(const AcceptArgs a, int req0, const float2* __restric
     uv = a.u[(int64_t)req * G + lane];
   }
   if (partials != nullptr) {
-    for (int j = wave; j < G; j += 8) {
+    for (int j = wave; j < G; j += kSumWaves) {
       const float v = row_lse_from_partials(partials + ((int64_t)req * G + j) * ntiles, ntiles);
       if (lane == 0) {
         s_lse[j] = v;
-        const_cast<float*>(a.lse)[(int64_t)req * G + j] = v;
+        if (s == 0) const_cast<float*>(a.lse)[(int64_t)req * G + j] = v;
       }
     }
   } else if (a.lse != nullptr && threadIdx.x < G) {
     s_lse[threadIdx.x] = a.lse[(int64_t)req * G + threadIdx.x];
   }
   __syncthreads();
+
+  // 2. Ratio tests in float64; l = number of leading accepts.
   if (wave == 0) {
     bool fail = false;
     if (lane < a.gamma) {
@@ -107,75 +204,62 @@ void accept_prepare_kernel(const AcceptArgs a, int req0, const float2* __restric
     }
     const unsigned long long fails = __ballot(fail);
     const int l = fails ? (__ffsll(fails) - 1) : a.gamma;
-    if (lane == 0) a.desc[req] = make_int2(l, __float_as_int(a.lse != nullptr ? s_lse[l] : 0.f));
+    if (lane == 0) {
+      s_l = l;
+      if (s == 0) accept_len[req] = l;
+    }
   }
-}
-
-__global__ __launch_bounds__(kWave)
-void accept_segments_kernel(const AcceptArgs a, int req0) {
-  const int sg = blockIdx.x;
-  const int req = req0 + blockIdx.y;
-  const int lane = threadIdx.x;
-  const int G = a.gamma + 1;
-  const int2 d = a.desc[req];
-  const int l = d.x;
-  const float lse = __int_as_float(d.y);
+  __syncthreads();
+  const int l = s_l;
+  const float lse = a.lse != nullptr ? s_lse[l] : 0.f;
   const bool residual = l < a.gamma;
-  const int64_t row = (int64_t)req * G + l;
-  const float* xrow = a.x + row * a.V;
+  const float* xrow = a.x + ((int64_t)req * G + l) * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
-  float r[kPerLane];
-#pragma unroll
-  for (int e = 0; e < kPerLane; ++e) {
-    const int v = sg * kSeg + e * kWave + lane;
-    r[e] = v < a.V ? r_of(a, xrow, qrow, lse, residual, v) : 0.f;
-  }
-  double acc = 0.0;
-#pragma unroll
-  for (int e = 0; e < kPerLane; ++e) acc += (double)r[e];
-  acc = wave_sum_f64(acc);
-  if (lane == 0) a.segsum[(int64_t)req * a.nseg + sg] = acc;
+
+  // 3. This workgroup's segment totals.
+  const int sg0 = s * a.segs_per_group;
+  const int sg1 = min(a.nseg, sg0 + a.segs_per_group);
+  segment_totals(a, xrow, qrow, lse, residual, sg0, sg1, kSumWaves, a.segsum + (int64_t)req * a.nseg);
 }
 
-// Sum of r over one segment, recomputed (used only on the rare fallback path).
-__device__ double segment_sum(const AcceptArgs& a, const float* xrow, const float* qrow, float lse, bool residual,
-                              int sg) {
-  const int lane = threadIdx.x & 63;
-  double acc = 0.0;
-  for (int e = 0; e < kPerLane; ++e) {
-    const int v = sg * kSeg + e * kWave + lane;
-    if (v < a.V) acc += (double)r_of(a, xrow, qrow, lse, residual, v);
-  }
-  return wave_sum_f64(acc);
-}
-
+// One wave per request: prefix of the segment totals, the segment holding
+// u * Z, and the scan of that segment in token order.
 __global__ __launch_bounds__(kWave)
-void accept_finalize_kernel(const AcceptArgs a, const AcceptBatch bt, int32_t* __restrict__ accept_len,
-                            int32_t* __restrict__ out_tok, int32_t* __restrict__ new_kv_len) {
+void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t* __restrict__ accept_len,
+                        int32_t* __restrict__ out_tok, int32_t* __restrict__ new_kv_len) {
+  __shared__ double seg[kMaxSeg];
   const int b = blockIdx.x;
   const int req = bt.req0 + b;
   const int lane = threadIdx.x;
   const int G = a.gamma + 1;
-  __shared__ double seg[kMaxSeg];
-  for (int i = lane; i < a.nseg; i += kWave) seg[i] = a.segsum[(int64_t)req * a.nseg + i];
-  const int2 d = a.desc[req];
-  const int l = d.x;
-  const float lse = __int_as_float(d.y);
-  bool residual = l < a.gamma;
-  const int64_t row = (int64_t)req * G + l;
-  const float* xrow = a.x + row * a.V;
-  const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
-  lds_wait();
+  const int nseg = a.nseg;
+  const double* tot = a.segsum + (int64_t)req * nseg;
 
-  // Inclusive prefix of the segment totals, in place (LDS, one wave).
+  // Segment totals into LDS, 8 loads per lane in flight; l and u alongside.
+  const int l = accept_len[req];
+  const float uu = a.u[(int64_t)req * G + a.gamma];
+  for (int base = 0; base < nseg; base += 8 * kWave) {
+    double v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = tot[min(base + k * kWave + lane, nseg - 1)];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (base + k * kWave + lane < nseg) seg[base + k * kWave + lane] = v[k];
+  }
+  const float lse = a.lse != nullptr ? a.lse[(int64_t)req * G + l] : 0.f;
+  bool residual = l < a.gamma;
+  const float* xrow = a.x + ((int64_t)req * G + l) * a.V;
+  const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
+
+  // Inclusive prefix of the segment totals, in place.
   auto prefix = [&]() -> double {
     lds_wait();
     double carry = 0.0;
-    for (int base = 0; base < a.nseg; base += kWave) {
+    for (int base = 0; base < nseg; base += kWave) {
       const int i = base + lane;
-      const double v = i < a.nseg ? seg[i] : 0.0;
+      const double v = i < nseg ? seg[i] : 0.0;
       const double c = wave_inclusive_scan_f64(v) + carry;
-      if (i < a.nseg) seg[i] = c;
+      if (i < nseg) seg[i] = c;
       carry = __shfl(c, 63);
     }
     lds_wait();
@@ -185,28 +269,21 @@ void accept_finalize_kernel(const AcceptArgs a, const AcceptBatch bt, int32_t* _
   if (!(z > 0.0) && residual) {
     // The residual vanished (possible only through rounding): sample from p_{l+1}.
     residual = false;
-    for (int sg = 0; sg < a.nseg; ++sg) {
-      const double s = segment_sum(a, xrow, qrow, lse, false, sg);
-      if (lane == 0) seg[sg] = s;
-    }
+    segment_totals(a, xrow, qrow, lse, false, 0, nseg, 1, seg);
     z = prefix();
   }
 
-  const double thr = (double)a.u[(int64_t)req * G + a.gamma] * z;
+  const double thr = (double)uu * z;
   int found = -1;
-  for (int base = 0; base < a.nseg && found < 0; base += kWave) {
+  for (int base = 0; base < nseg && found < 0; base += kWave) {
     const int i = base + lane;
-    const unsigned long long hit = __ballot(i < a.nseg && seg[i] > thr);
+    const unsigned long long hit = __ballot(i < nseg && seg[i] > thr);
     if (hit) found = base + __ffsll(hit) - 1;
   }
   int t = -1;
   if (found >= 0) {
     float rv[kPerLane];
-#pragma unroll
-    for (int e = 0; e < kPerLane; ++e) {
-      const int v = found * kSeg + e * kWave + lane;
-      rv[e] = v < a.V ? r_of(a, xrow, qrow, lse, residual, v) : 0.f;
-    }
+    segment_load(a, xrow, qrow, lse, residual, found, rv);
     double c = found > 0 ? seg[found - 1] : 0.0;
     int last_pos = -1;
 #pragma unroll
@@ -224,10 +301,11 @@ void accept_finalize_kernel(const AcceptArgs a, const AcceptBatch bt, int32_t* _
   }
   if (t < 0) {
     // No prefix sum exceeds u * Z: the largest token with mass.
-    for (int sg = a.nseg - 1; sg >= 0 && t < 0; --sg) {
+    for (int sg = nseg - 1; sg >= 0 && t < 0; --sg) {
+      float rv[kPerLane];
+      segment_load(a, xrow, qrow, lse, residual, sg, rv);
       for (int e = kPerLane - 1; e >= 0 && t < 0; --e) {
-        const int v = sg * kSeg + e * kWave + lane;
-        const unsigned long long pos = __ballot(v < a.V && r_of(a, xrow, qrow, lse, residual, v) > 0.f);
+        const unsigned long long pos = __ballot(rv[e] > 0.f);
         if (pos) t = sg * kSeg + e * kWave + 63 - __clzll(pos);
       }
     }
@@ -240,44 +318,44 @@ void accept_finalize_kernel(const AcceptArgs a, const AcceptBatch bt, int32_t* _
     else if (lane == l) v = t;
     out_tok[(int64_t)req * G + lane] = v;
   }
-  if (lane == 0) {
-    accept_len[req] = l;
-    if (new_kv_len != nullptr && bt.has_kv_len) new_kv_len[req] = bt.kv_len[b] - a.gamma + l;
-  }
+  if (lane == 0 && new_kv_len != nullptr && bt.has_kv_len) new_kv_len[req] = bt.kv_len[b] - a.gamma + l;
 }
 
 }  // namespace
 
 size_t accept_workspace_bytes(int B, int V) {
   const int nseg = (V + kSeg - 1) / kSeg;
-  return sizeof(double) * static_cast<size_t>(B) * nseg + sizeof(int2) * static_cast<size_t>(B) + 512;
+  return sizeof(double) * static_cast<size_t>(B) * nseg;
 }
 
 hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
                          const float2* partials, int ntiles, const float* q_draft, const int32_t* draft_tok,
                          const float* u, void* ws, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
                          hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+  (void)B;
   if (bt.nreq <= 0) return hipSuccess;
   AcceptArgs a;
   a.gamma = gamma;
   a.V = V;
   a.nseg = (V + kSeg - 1) / kSeg;
+  if (a.nseg > kMaxSeg || gamma + 1 > kWave) return hipErrorInvalidValue;
+  // Segments per workgroup: a multiple of the wave count, enough workgroups
+  // to cover the chip about twice.
+  const int64_t want = ((int64_t)a.nseg * bt.nreq + kTargetGroups - 1) / kTargetGroups;
+  a.segs_per_group = (int)std::min<int64_t>(a.nseg, std::max<int64_t>(kSumWaves, (want + kSumWaves - 1) / kSumWaves * kSumWaves));
   a.x = x;
   a.lse = row_lse;
   a.q = q_draft;
   a.draft = draft_tok;
   a.u = u;
   a.segsum = static_cast<double*>(ws);
-  a.desc = reinterpret_cast<int2*>(static_cast<char*>(ws) + sizeof(double) * static_cast<size_t>(B) * a.nseg);
-  hipLaunchKernelGGL(accept_prepare_kernel, dim3(bt.nreq), dim3(512), 0, stream, a, bt.req0, partials, ntiles);
+  const int S = (a.nseg + a.segs_per_group - 1) / a.segs_per_group;
+  hipExtLaunchKernelGGL(accept_sums_kernel, dim3(S, bt.nreq), dim3(kSumWaves * kWave), 0, stream, ev_start, nullptr,
+                        0, a, bt, partials, ntiles, accept_len);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL(accept_segments_kernel, dim3(a.nseg, bt.nreq), dim3(kWave), 0, stream, ev_start, ev_stop,
-                        0, a, bt.req0);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_finalize_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, a, bt, accept_len, out_tok,
-                     new_kv_len);
+  hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, nullptr, ev_stop, 0, a, bt,
+                        accept_len, out_tok, new_kv_len);
   return hipGetLastError();
 }
 

@@ -127,31 +127,34 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // Row log-sum-exp from per-tile (maximum, sum of exp(x - maximum)) pairs, one
-// wave, two passes over registers: the row maximum m, then
-// sum_t S_t * exp(M_t - m) accumulated in float64, lse = m + log(sum).  Each
-// lane holds tiles lane, lane + 64, ...; the lane sums are added by a fixed
-// butterfly and lane 0's value is broadcast, so the result is deterministic
-// and every lane returns the same bits.
+// wave: the row maximum m, then sum_t S_t * exp(M_t - m) accumulated in
+// float64, lse = m + log(sum).  Each lane holds tiles lane, lane + 64, ...;
+// loads take clamped indexes and masks so a round of kR per lane is in flight
+// at once (rows of up to kR * 64 tiles are read once), the lane sums are added
+// by a fixed butterfly and lane 0's value is broadcast, so the result is
+// deterministic and every lane returns the same bits.  ntiles >= 1.
 __device__ __forceinline__ float row_lse_from_partials(const float2* p, int ntiles) {
   const int lane = threadIdx.x & 63;
-  constexpr int kR = 8;  // tiles per lane held in registers per round
+  constexpr int kR = 16;  // tiles per lane held in registers per round
+  float2 v[kR];
+  auto load = [&](int base) {
+#pragma unroll
+    for (int j = 0; j < kR; ++j) v[j] = p[min(base + j * kWave + lane, ntiles - 1)];
+#pragma unroll
+    for (int j = 0; j < kR; ++j)
+      if (base + j * kWave + lane >= ntiles) v[j] = make_float2(-INFINITY, 0.f);
+  };
   float mx = -INFINITY;
   for (int base = 0; base < ntiles; base += kR * kWave) {
+    load(base);
 #pragma unroll
-    for (int j = 0; j < kR; ++j) {
-      const int t = base + j * kWave + lane;
-      if (t < ntiles) mx = fmaxf(mx, p[t].x);
-    }
+    for (int j = 0; j < kR; ++j) mx = fmaxf(mx, v[j].x);
   }
   mx = wave_max(mx);
+  const bool one_round = ntiles <= kR * kWave;
   double s = 0.0;
   for (int base = 0; base < ntiles; base += kR * kWave) {
-    float2 v[kR];
-#pragma unroll
-    for (int j = 0; j < kR; ++j) {
-      const int t = base + j * kWave + lane;
-      v[j] = t < ntiles ? p[t] : make_float2(-INFINITY, 0.f);
-    }
+    if (!one_round) load(base);
 #pragma unroll
     for (int j = 0; j < kR; ++j) s += (double)v[j].y * (double)expf(v[j].x - mx);
   }
