@@ -102,7 +102,8 @@ SD_API size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len);
  *   kv_off   (host) [B] element offsets; kv_off[b] * sizeof(dtype) % 16 == 0
  *   kv_len   (host) [B] cached length L_b INCLUDING this step's G positions,
  *            G <= L_b <= 2^30; query j attends to keys 0 .. L_b - G + j
- *   scale    softmax scale (1/sqrt(head_dim) for the usual definition)
+ *   scale    softmax scale, finite and > 0 (SD_ERR_INVALID_ARGUMENT otherwise);
+ *            1/sqrt(head_dim) for the usual definition
  *   out      [B][G][Hq][D] in dtype: softmax(q k^T * scale) v per (request, head, query)
  * Requires G * (n_q_heads / n_kv_heads) <= 128 (SD_ERR_UNSUPPORTED otherwise).
  */
@@ -182,7 +183,8 @@ SD_API int sd_accept_resample(const sd_dims_t* dims, const float* logits_or_prob
  *                  enabled): start/stop of the attention kernel (without its
  *                  combine), of the vocabulary projection (for more than 64
  *                  rows: hidden repacking through the projection kernel) and
- *                  of the acceptance kernel.  They are recorded by the kernel
+ *                  of the acceptance (segment sums through the pick kernel).
+ *                  They are recorded by the kernel
  *                  launches themselves (no extra work on the stream), so the
  *                  elapsed time of each pair is that span's execution time.
  */

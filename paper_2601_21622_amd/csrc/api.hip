@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 
 #include "sdverify.h"
 #include "launch.h"
@@ -187,7 +188,7 @@ int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool
   if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(out, 16) ||
       !aligned(workspace, 16))
     return SD_ERR_INVALID_ARGUMENT;
-  if (!(scale == scale)) return SD_ERR_INVALID_ARGUMENT;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return SD_ERR_INVALID_ARGUMENT;
   st = check_kv(dims, kv_off, kv_len);
   if (st != SD_OK) return st;
   const AttnShape s = attn_shape(dims, scale, kv_len);
@@ -242,7 +243,7 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
       (hidden != nullptr && !aligned(hidden, 16)))
     return SD_ERR_INVALID_ARGUMENT;
   if (hidden == nullptr && dims->hidden != dims->n_q_heads * dims->head_dim) return SD_ERR_INVALID_ARGUMENT;
-  if (!(scale == scale)) return SD_ERR_INVALID_ARGUMENT;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return SD_ERR_INVALID_ARGUMENT;
   st = check_accept_args(logits, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok, new_kv_len);
   if (st != SD_OK) return st;
   st = check_kv(dims, kv_off, kv_len);

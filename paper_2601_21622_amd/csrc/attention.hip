@@ -21,7 +21,8 @@
 // Both compute S^T = K Q^T and O^T += V^T P^T on MFMA 16x16x32 bf16 (the Q
 // fragments stay in registers, P comes straight from the S^T accumulator
 // layout) with the online softmax in the log2 domain, each lane owning one
-// query row.  Each item writes one partial (max, sum, O) to the workspace; a
+// query row (for up to two row blocks the reference maximum moves lazily, so
+// most tiles skip the rescale of O).  Each item writes one partial (max, sum, O) to the workspace; a
 // combine kernel merges the chunks of each request in fixed order and writes
 // O in the input dtype.  LDS tiles keep rows whole but rotate their 16-byte
 // pieces so that the fragment reads are free of bank conflicts.
@@ -54,6 +55,68 @@ __device__ __forceinline__ int find_request(const AttnBatch& bt, int c) {
     if (bt.chunk_prefix[mid] <= c) lo = mid; else hi = mid - 1;
   }
   return lo;
+}
+
+// Online softmax of one 16-row block over a 32-key tile, in the log2 domain:
+// the lane owns row lr of the block and keys k0 + kb*16 + lg*4 + e.  With
+// LAZY the reference maximum m of the rows moves lazily: only when some row's
+// tile maximum exceeds it by more than kLazyLog2 does the wave move m to the
+// new maxima and rescale the sums and O (rows whose maximum did not grow get
+// alpha = 1).  Otherwise p = 2^(s*scale - m) stays below 2^kLazyLog2, well
+// inside float32 and bfloat16 range, and O and the sum share the same m, so
+// the normalised result is unchanged.  Masking (keys past the row's causal
+// limit lim) applies only when `masked` (always without LAZY, which keeps the
+// step one branch-free block); a fully masked row gives p = 0.
+// Requires scale_log2 > 0 (the row maximum is taken before scaling).
+constexpr float kLazyLog2 = 8.f;
+// Up to this many row blocks the rescale branch costs nothing; with more, the
+// output accumulators no longer fit beside the rest in plain registers and
+// the branch makes the compiler move them every tile, so the rescale runs on
+// every tile instead (alpha is 1 whenever the maximum did not grow).
+constexpr int kLazyMaxBlocks = 2;
+
+__device__ __forceinline__ float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <int DB, bool LAZY>
+__device__ __forceinline__ bf16x8 softmax_tile(const f32x4 (&sc)[2], float scale_log2, bool masked, int k0, int lim,
+                                               float& m, float& lsum, f32x4 (&o)[DB]) {
+  const int lg = (threadIdx.x & 63) >> 4;
+  float raw[8];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) raw[kb * 4 + e] = sc[kb][e];
+  if (!LAZY || masked) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (k0 + kb * 16 + lg * 4 + e > lim) raw[kb * 4 + e] = -INFINITY;
+  }
+  float mx = fmaxf(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])),
+                   fmaxf(fmaxf(raw[4], raw[5]), fmaxf(raw[6], raw[7])));
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  mx *= scale_log2;
+  if (!LAZY || __ballot(mx > m + kLazyLog2) != 0) {
+    const float mn = fmaxf(m, mx);
+    const float alpha = exp2_raw(m - mn);
+    m = mn;
+    lsum *= alpha;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] *= alpha;
+  }
+  const float mneg = -m;
+  bf16x8 pf;
+  float ps = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 pb = (__bf16)exp2_raw(fmaf(raw[e], scale_log2, mneg));
+    pf[e] = pb;
+    ps += (float)pb;
+  }
+  lsum += ps;
+  return pf;
 }
 
 // K or V tile of one wave in LDS: 32 keys x D, row r (D*2 bytes) holding its
@@ -96,19 +159,15 @@ struct AttnRows {
   f32x4 o[RB][D / 16];    // running O^T blocks
 };
 
-// One step of a wave's software pipeline: start the DMAs of the next tile
-// (keys from k0_next) into (kdst, vdst), wait until only those are in flight,
-// then fold the current tile (keys from k0, staged in ksrc/vsrc) into the
-// running state.  The stage pointers are restrict-qualified, so the compiler
-// knows the new DMAs cannot write what this step reads and leaves the
-// ordering to the explicit wait.  A tile with live == false (past the wave's
-// last one) contributes nothing: all of its scores are masked.
+// Fold one staged 32-key tile (keys from k0, K in ksrc, V in vsrc) into the
+// running state of a wave's rows: S^T = K Q^T, online softmax, O^T += V^T P^T.
+// `masked` says whether some key of the tile may lie past a row's causal
+// limit (only then are the limits applied); a tile with live == false
+// contributes nothing (all of its keys are masked).
 template <int RB, int D>
-__device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2, const uint16_t* Kb,
-                                          const uint16_t* Vb, int L, int k0_next, int k0, bool live,
-                                          unsigned char* __restrict__ kdst, unsigned char* __restrict__ vdst,
+__device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2, int k0, bool masked,
                                           const unsigned char* __restrict__ ksrc,
-                                          const unsigned char* __restrict__ vsrc) {
+                                          const unsigned char* __restrict__ vsrc, bool live = true) {
   constexpr int DS = D / 32;
   constexpr int DB = D / 16;
   using KT = KVTile<D, false>;
@@ -116,9 +175,6 @@ __device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2,
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15;
   const int lg = lane >> 4;
-  KT::load(Kb, k0_next, L, kdst, lane);
-  VT::load(Vb, k0_next, L, vdst, lane);
-  wait_vmcnt<KT::kDmas + VT::kDmas>();
 
   // K fragments (A operand): lane holds key kb*16 + lr, d = ds*32 + lg*8 .. +8.
   bf16x8 kf[2][DS];
@@ -139,38 +195,11 @@ __device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2,
       sc[rb][kb] = acc;
     }
 
-  // Online softmax: lane owns row rb*16+lr and keys k0 + kb*16 + lg*4 + e.
   bf16x8 pf[RB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    float sv[8];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = k0 + kb * 16 + lg * 4 + e;
-        float x = sc[rb][kb][e] * scale_log2;
-        x = (key > st.lim[rb] || !live) ? -INFINITY : x;
-        sv[kb * 4 + e] = x;
-        mx = fmaxf(mx, x);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mn = fmaxf(st.m[rb], mx);
-    const float alpha = exp2f(st.m[rb] - mn);
-    st.m[rb] = mn;
-    float ps = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const __bf16 pb = (__bf16)exp2f(sv[e] - mn);
-      pf[rb][e] = pb;
-      ps += (float)pb;
-    }
-    st.lsum[rb] = st.lsum[rb] * alpha + ps;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) st.o[rb][db] *= alpha;
-  }
+  for (int rb = 0; rb < RB; ++rb)
+    pf[rb] = softmax_tile<DB, (RB <= kLazyMaxBlocks)>(sc[rb], scale_log2, masked || !live, k0,
+                                                      live ? st.lim[rb] : -1, st.m[rb], st.lsum[rb], st.o[rb]);
 
   // V^T fragments (A operand of O^T += V^T P^T): lane (lg, lr) needs
   // d = db*16 + lr and keys {lg*4 .. +3} then {16 + lg*4 .. +3}, the
@@ -188,6 +217,26 @@ __device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2,
   }
 }
 
+// One step of a wave's software pipeline: start the DMAs of the next tile
+// (keys from k0_next) into (kdst, vdst), wait until only those are in flight,
+// then fold the current tile.  The stage pointers are restrict-qualified, so
+// the compiler knows the new DMAs cannot write what this step reads and
+// leaves the ordering to the explicit wait.
+template <int RB, int D>
+__device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2, const uint16_t* Kb,
+                                          const uint16_t* Vb, int L, int k0_next, int k0, bool masked,
+                                          unsigned char* __restrict__ kdst, unsigned char* __restrict__ vdst,
+                                          const unsigned char* __restrict__ ksrc,
+                                          const unsigned char* __restrict__ vsrc) {
+  using KT = KVTile<D, false>;
+  using VT = KVTile<D, true>;
+  const int lane = threadIdx.x & 63;
+  KT::load(Kb, k0_next, L, kdst, lane);
+  VT::load(Vb, k0_next, L, vdst, lane);
+  wait_vmcnt<KT::kDmas + VT::kDmas>();
+  attn_fold<RB, D>(st, scale_log2, k0, masked, ksrc, vsrc);
+}
+
 // Item of wave `wave` in workgroup blockIdx.x: (chunk, KV head), KV head
 // fastest.  Returns false past the last item.
 __device__ __forceinline__ bool attn_item(const AttnShape& s, const AttnBatch& bt, int& c_local, int& g) {
@@ -201,7 +250,7 @@ __device__ __forceinline__ bool attn_item(const AttnShape& s, const AttnBatch& b
 template <int RB, int D>
 __device__ __forceinline__ void write_partial(const AttnShape& s, const AttnBatch& bt, AttnPartials parts, int c_local,
                                               int g, const float (&m)[RB], float (&lsum)[RB],
-                                              const f32x4 (&o)[RB][D / 16]) {
+                                              const f32x4 (&o)[RB][D / 16], int row0 = 0) {
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15, lg = lane >> 4;
   const int64_t slot = (int64_t)(bt.chunk_base + c_local) * s.Hkv + g;
@@ -209,7 +258,7 @@ __device__ __forceinline__ void write_partial(const AttnShape& s, const AttnBatc
   for (int rb = 0; rb < RB; ++rb) {
     lsum[rb] += __shfl_xor(lsum[rb], 16);
     lsum[rb] += __shfl_xor(lsum[rb], 32);
-    const int row = rb * 16 + lr;
+    const int row = row0 + rb * 16 + lr;
     if (row < s.rows) {
       if (lg == 0) {
         parts.m[slot * s.rows + row] = m[rb];
@@ -219,6 +268,39 @@ __device__ __forceinline__ void write_partial(const AttnShape& s, const AttnBatc
       for (int db = 0; db < D / 16; ++db)
         *reinterpret_cast<f32x4*>(parts.o + (slot * s.rows + row) * D + db * 16 + lg * 4) = o[rb][db];
     }
+  }
+}
+
+// Running state of rows row0 .. row0 + 16*RB - 1 of KV head g: Q fragments
+// (B operand of S^T = K Q^T; lane holds row row0 + rb*16 + lr, d = ds*32 +
+// lg*8 .. +8), causal limits, empty sums.  Rows past s.rows are padding.
+template <int RB, int D>
+__device__ __forceinline__ void init_rows(AttnRows<RB, D>& st, const AttnShape& s, const uint16_t* __restrict__ q,
+                                          int req, int g, int L, int row0) {
+  constexpr int DS = D / 32;
+  constexpr int DB = D / 16;
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15;
+  const int lg = lane >> 4;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int row = row0 + rb * 16 + lr;
+    if (row < s.rows) {
+      const int j = row / s.group;
+      const int h = g * s.group + (row - j * s.group);
+      const uint16_t* qrow = q + (((int64_t)req * s.G + j) * s.Hq + h) * D;
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = load_bf16x8(qrow + ds * 32 + lg * 8);
+      st.lim[rb] = L - s.G + j;
+    } else {
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = bf16x8{};
+      st.lim[rb] = -1;
+    }
+    st.m[rb] = kNegBig;
+    st.lsum[rb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) st.o[rb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 }
 
@@ -254,28 +336,8 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   const uint16_t* Kb = kp + off + (int64_t)g * L * D;
   const uint16_t* Vb = vp + off + (int64_t)g * L * D;
 
-  // Q fragments (B operand of S^T = K Q^T): lane holds row rb*16+lr, d = ds*32 + lg*8 .. +8.
   AttnRows<RB, D> st;
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int row = rb * 16 + lr;
-    if (row < s.rows) {
-      const int j = row / s.group;
-      const int h = g * s.group + (row - j * s.group);
-      const uint16_t* qrow = q + (((int64_t)req * s.G + j) * s.Hq + h) * D;
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = load_bf16x8(qrow + ds * 32 + lg * 8);
-      st.lim[rb] = L - s.G + j;
-    } else {
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = bf16x8{};
-      st.lim[rb] = -1;
-    }
-    st.m[rb] = kNegBig;
-    st.lsum[rb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) st.o[rb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+  init_rows<RB, D>(st, s, q, req, g, L, 0);
 
   // Tile i of the item starts at key k_begin + 32i; the load past the last
   // tile re-reads it (in bounds, never folded in).  Tile i+1 loads while
@@ -289,7 +351,8 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   KT::load(Kb, key0(0), L, k0s, lane);
   VT::load(Vb, key0(0), L, v0s, lane);
   for (int i = 0; i < ntiles; ++i) {
-    attn_step<RB, D>(st, s.scale_log2, Kb, Vb, L, key0(i + 1), key0(i), true, k1s, v1s, k0s, v0s);
+    attn_step<RB, D>(st, s.scale_log2, Kb, Vb, L, key0(i + 1), key0(i), key0(i) + kTile - 1 > L - s.G, k1s, v1s,
+                     k0s, v0s);
     unsigned char* t = k0s;
     k0s = k1s;
     k1s = t;
@@ -301,22 +364,19 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   write_partial<RB, D>(s, bt, parts, c_local, g, st.m, st.lsum, st.o);
 }
 
-// Register-staged variant for one 16-row block (multi-head attention, where
-// each KV head serves only the G queries of its own head).  The work per
-// tile is small there, so the kernel keeps two workgroups per CU and stages
-// through registers: whole K and V rows go register -> wave-private LDS tiles
-// (rotated rows) -> MFMA fragments.  All loads land in registers, so the
-// compiler's own vmcnt accounting covers the pipeline.
-template <int D>
-__global__ __launch_bounds__(kAttnThreads, 2)
-void attn_bf16_mha_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
+// Register-staged variant: whole K and V rows go HBM -> registers ->
+// wave-private LDS tiles (rotated rows) -> MFMA fragments.  All loads land in
+// registers, so the compiler's own vmcnt accounting covers the pipeline, and
+// two tiles of each wave are in flight while it folds.  With one 16-row block
+// (multi-head attention) two workgroups share a CU.
+template <int RB, int D>
+__global__ __launch_bounds__(kAttnThreads, (RB == 1 ? 2 : 1))
+void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
                           const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
                           AttnPartials parts) {
-  constexpr int DS = D / 32;
-  constexpr int DB = D / 16;
-  constexpr int LPR = D / 8;       // lanes per V row (16 bytes each)
-  constexpr int KPI = 64 / LPR;    // V rows per wave-wide load
-  constexpr int NV = kTile / KPI;  // V loads per tile
+  constexpr int LPR = D / 8;       // lanes per row (16 bytes each)
+  constexpr int KPI = 64 / LPR;    // rows per wave-wide load
+  constexpr int NV = kTile / KPI;  // loads of K (and of V) per tile
   using VT = KVTile<D, true>;
   using KT = KVTile<D, false>;
   __shared__ __align__(16) unsigned char vsm[kAttnWaves * VT::kBytes];
@@ -326,8 +386,6 @@ void attn_bf16_mha_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
   if (!attn_item(s, bt, c_local, g)) return;
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int lr = lane & 15;
-  const int lg = lane >> 4;
 
   const int b = find_request(bt, c_local);
   const int L = bt.kv_len[b];
@@ -338,24 +396,8 @@ void attn_bf16_mha_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
   const uint16_t* Kb = kp + off + (int64_t)g * L * D;
   const uint16_t* Vb = vp + off + (int64_t)g * L * D;
 
-  bf16x8 qf[DS];
-  int lim;
-  if (lr < s.rows) {
-    const int j = lr / s.group;
-    const int h = g * s.group + (lr - j * s.group);
-    const uint16_t* qrow = q + (((int64_t)req * s.G + j) * s.Hq + h) * D;
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) qf[ds] = load_bf16x8(qrow + ds * 32 + lg * 8);
-    lim = L - s.G + j;
-  } else {
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) qf[ds] = bf16x8{};
-    lim = -1;
-  }
-  float m[1] = {kNegBig}, lsum[1] = {0.f};
-  f32x4 o[1][DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) o[0][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  AttnRows<RB, D> st;
+  init_rows<RB, D>(st, s, q, req, g, L, 0);
 
   const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
   unsigned char* vt = vsm + wave * VT::kBytes;
@@ -381,56 +423,7 @@ void attn_bf16_mha_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
       *reinterpret_cast<u32x4*>(kt + KT::at(r, d)) = kr[set][it];
       *reinterpret_cast<u32x4*>(vt + VT::at(r, d)) = vr[set][it];
     }
-    // K fragments (A operand): lane holds key kb*16 + lr, d = ds*32 + lg*8 .. +8.
-    f32x4 sc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) {
-        const bf16x8 kf =
-            __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kt + KT::at(kb * 16 + lr, ds * 32 + lg * 8)));
-        acc = mfma16x16x32(kf, qf[ds], acc);
-      }
-      sc[kb] = acc;
-    }
-    float sv[8];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = k0 + kb * 16 + lg * 4 + e;
-        float x = sc[kb][e] * s.scale_log2;
-        x = (key > lim || !live) ? -INFINITY : x;
-        sv[kb * 4 + e] = x;
-        mx = fmaxf(mx, x);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mn = fmaxf(m[0], mx);
-    const float alpha = exp2f(m[0] - mn);
-    m[0] = mn;
-    bf16x8 pf;
-    float ps = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const __bf16 pb = (__bf16)exp2f(sv[e] - mn);
-      pf[e] = pb;
-      ps += (float)pb;
-    }
-    lsum[0] = lsum[0] * alpha + ps;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[0][db] *= alpha;
-    const int jr = 4 * lg + (lr >> 2);
-    const int jd = 4 * (lr & 3);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const s16x4 lo = lds_read_tr16(vt + VT::at(jr, db * 16 + jd));
-      const s16x4 hi = lds_read_tr16(vt + VT::at(16 + jr, db * 16 + jd));
-      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-      o[0][db] = mfma16x16x32(vf, pf, o[0][db]);
-    }
+    attn_fold<RB, D>(st, s.scale_log2, k0, k0 + kTile - 1 > L - s.G, kt, vt, live);
   };
 
   // Tile i+1 loads while tile i is folded in; the body always folds two
@@ -445,7 +438,7 @@ void attn_bf16_mha_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
     __builtin_amdgcn_sched_barrier(0);
     fold(1, key0(i + 1), i + 1 < ntiles);
   }
-  write_partial<1, D>(s, bt, parts, c_local, g, m, lsum, o);
+  write_partial<RB, D>(s, bt, parts, c_local, g, st.m, st.lsum, st.o);
 }
 
 // float32 path (small shapes): one workgroup per (chunk, KV head); scores and
@@ -569,15 +562,20 @@ hipError_t launch_bf16(const AttnShape& s, const AttnBatch& bt, int nchunks, con
   return hipGetLastError();
 }
 
+template <int RB, int D>
+hipError_t launch_reg(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
+                      const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+  hipExtLaunchKernelGGL((attn_bf16_reg_kernel<RB, D>), dim3((nchunks * s.Hkv + kAttnWaves - 1) / kAttnWaves),
+                        dim3(kAttnThreads), 0, stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q),
+                        static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), parts);
+  return hipGetLastError();
+}
+
 template <int D>
 hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                        const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   switch (rb) {
-    case 1:
-      hipExtLaunchKernelGGL(attn_bf16_mha_kernel<D>, dim3((nchunks * s.Hkv + kAttnWaves - 1) / kAttnWaves),
-                            dim3(kAttnThreads), 0, stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q),
-                            static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), parts);
-      return hipGetLastError();
+    case 1: return launch_reg<1, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     case 2: return launch_bf16<2, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     case 3: return launch_bf16<3, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     case 4: return launch_bf16<4, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);

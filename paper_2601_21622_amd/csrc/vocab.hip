@@ -236,16 +236,17 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
 // MB x NB accumulators of 16 registers.  K goes in 32-wide chunks of two
 // 16-wide MFMA steps.
 //
-// Pipeline, chunk c of the loop (kStages = 6):
-//   * issue chunk c+4: its hidden chunk goes straight from global memory into
-//     LDS buffer (c+4) % 6 (LDS DMA, no registers), its W fragments into the
-//     register ring slot (c+4) % 6;
+// Pipeline, chunk c of the loop (kStages = 6, kAhead = 5):
+//   * issue chunk c+5: its hidden chunk goes straight from global memory into
+//     LDS buffer (c+5) % 6 (LDS DMA, no registers), its W fragments into the
+//     register ring slot (c+5) % 6; both slots last served chunk c-1, whose
+//     fragments every wave read before the previous step's barrier;
 //   * read the hidden fragments of chunk c+1 from LDS into registers;
 //   * multiply chunk c (W ring slot c % 6, fragments read one chunk earlier);
 //   * wait until this wave's DMA of chunk c+2 has landed, then barrier, so
 //     chunk c+2 is readable by every wave in the next step.
 // Memory operations complete in issue order, so the wait leaves the loads of
-// chunks c+3 and c+4 (and the W of c+2) in flight: three chunks of W and two
+// chunks c+3 .. c+5 (and the W of c+2) in flight: four chunks of W and three
 // of hidden are always on the way while the MFMAs run, and no MFMA waits on
 // an LDS read issued in the same step.  Loads past the last chunk re-read the
 // last chunk (in bounds) and chunks past the end multiply a zero W, which
@@ -258,6 +259,7 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
 // the row-major [V][K] layout or gathered from the packed 16x16x32 fragment
 // layout.
 constexpr int kStages = 6;
+constexpr int kAhead = kStages - 1;  // chunks issued ahead of the one multiplied
 
 template <int MB, int NB>
 struct Deep32Cfg {
@@ -266,9 +268,11 @@ struct Deep32Cfg {
   static constexpr int kDmaPerWave = (kFrags + 3) / 4;  // the same count on every wave
   static constexpr int kBufBytes = 4 * kDmaPerWave * 1024;
   // Memory operations a wave issues per chunk, and the most that may still be
-  // outstanding once the DMA of the chunk two steps ahead has landed.
+  // outstanding once the DMA of the chunk two steps ahead has landed (its W,
+  // then chunks c+3 .. c+kAhead).
   static constexpr int kOpsPerChunk = kDmaPerWave + 2 * NB;
-  static constexpr int kInFlight = 2 * NB + 2 * kOpsPerChunk;
+  static constexpr int kInFlight = 2 * NB + (kAhead - 2) * kOpsPerChunk;
+  static_assert(kInFlight <= 63, "vmcnt holds 6 bits");
 };
 
 template <int MB, int NB>
@@ -399,9 +403,11 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
 
   // DMA i of this wave moves fragment f = wave + 4*i (2*mb + ks) of a chunk:
   // 1 KB contiguous in the packed hidden (lane l: row mb*32 + l%32, k
-  // 16*ks + 8*(l/32) .. +8).  Fragment numbers past the chunk's 2*MB re-read
-  // the last fragment into spare LDS space; blocks past the packed rows
-  // (last M-tile) re-read the last block, whose rows are never stored.
+  // 16*ks + 8*(l/32) .. +8).  Fragment numbers past the chunk's 2*MB keep
+  // every wave's operation count equal: all their lanes read the same 16
+  // bytes of the last fragment (one cache line, one request) into spare LDS
+  // space.  Blocks past the packed rows (last M-tile) re-read the last
+  // block, whose rows are never stored.
   const int mbt = (M + 31) / 32;
   const int64_t hstep = (int64_t)2 * mbt * 512;  // elements per 32-wide chunk
   const uint16_t* hsrc[ND];
@@ -411,7 +417,7 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
     const int f = wave + 4 * i;
     const int fs = min(f, C::kFrags - 1);
     const int mbg = min(mbt - 1, m0 / 32 + (fs >> 1));
-    hsrc[i] = hpacked + (((int64_t)(fs & 1) * mbt + mbg) * 64 + lane) * 8;
+    hsrc[i] = hpacked + (((int64_t)(fs & 1) * mbt + mbg) * 64 + (f < C::kFrags ? lane : 0)) * 8;
     hoff[i] = f * 1024;
   }
 
@@ -442,10 +448,10 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
+  for (int c = 0; c < kAhead; ++c)
 #pragma unroll
     for (int j = 0; j < C::kOpsPerChunk; ++j) issue_op(j, c, c);
-  wait_vmcnt<2 * NB + 2 * C::kOpsPerChunk>();  // chunks 0 and 1 have landed
+  wait_vmcnt<2 * NB + (kAhead - 2) * C::kOpsPerChunk>();  // chunks 0 and 1 have landed
   lds_barrier();
 #pragma unroll
   for (int f = 0; f < C::kFrags; ++f) read_frag(0, 0, f);
@@ -469,7 +475,7 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
             const int i = (ks * MB + mb) * NB + nb;
             acc[mb][nb] = mfma32x32x16(wv[nb], af[s & 1][2 * mb + ks], acc[mb][nb]);
             if (i < C::kOpsPerChunk)
-              issue_op(i, (s + 4) % kStages, c + 4);
+              issue_op(i, (s + kAhead) % kStages, c + kAhead);
             else if (i - C::kOpsPerChunk < C::kFrags)
               read_frag((s + 1) & 1, (s + 1) % kStages, i - C::kOpsPerChunk);
             __builtin_amdgcn_sched_barrier(0);

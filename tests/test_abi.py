@@ -82,6 +82,9 @@ def test_attention_rejects_bad_pointers_lengths_and_workspace():
     assert _attn(d, kv_off=(-8, 0)) == sd.SD_ERR_INVALID_ARGUMENT
     assert _attn(d, ws_bytes=16) == sd.SD_ERR_WORKSPACE
     assert _attn(d, scale=float("nan")) == sd.SD_ERR_INVALID_ARGUMENT
+    assert _attn(d, scale=0.0) == sd.SD_ERR_INVALID_ARGUMENT
+    assert _attn(d, scale=-0.088) == sd.SD_ERR_INVALID_ARGUMENT
+    assert _attn(d, scale=float("inf")) == sd.SD_ERR_INVALID_ARGUMENT
     lib = sd.library()
     assert lib.sd_verify_attention(ctypes.byref(d), P, P, P, None, None, 0.1, P, P, 1 << 30, None) == \
         sd.SD_ERR_INVALID_ARGUMENT
