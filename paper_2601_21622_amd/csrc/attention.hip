@@ -138,14 +138,17 @@ struct KVTile {
     return r * D * 2 + (((d >> 3) + rot(r)) % kPieces) * 16 + (d & 7) * 2;
   }
   // DMA instruction i of a tile: lane l brings row r = i*kRowsPerDma +
-  // l/kPieces, the global piece that belongs in LDS slot l%kPieces.
-  __device__ static void load(const uint16_t* rows, int k0, int L, unsigned char* tile, int lane) {
+  // l/kPieces, the global piece that belongs in LDS slot l%kPieces.  A dead
+  // tile (past the item's last, issued only to keep the pipeline shape) has
+  // every lane read the same 16 bytes: one cache line per instruction.
+  __device__ static void load(const uint16_t* rows, int k0, int L, unsigned char* tile, int lane, bool dead = false) {
 #pragma unroll
     for (int i = 0; i < kDmas; ++i) {
       const int r = i * kRowsPerDma + lane / kPieces;
       const int piece = (lane % kPieces - rot(r) + kPieces) % kPieces;
       const int key = min(k0 + r, L - 1);
-      dma_16B_to_lds_opaque(rows + (int64_t)key * D + piece * 8, tile + i * 1024);
+      const int64_t src = dead ? (int64_t)min(k0, L - 1) * D : (int64_t)key * D + piece * 8;
+      dma_16B_to_lds_opaque(rows + src, tile + i * 1024);
     }
   }
 };
@@ -224,15 +227,15 @@ __device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2,
 // leaves the ordering to the explicit wait.
 template <int RB, int D>
 __device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2, const uint16_t* Kb,
-                                          const uint16_t* Vb, int L, int k0_next, int k0, bool masked,
-                                          unsigned char* __restrict__ kdst, unsigned char* __restrict__ vdst,
-                                          const unsigned char* __restrict__ ksrc,
+                                          const uint16_t* Vb, int L, int k0_next, bool next_dead, int k0,
+                                          bool masked, unsigned char* __restrict__ kdst,
+                                          unsigned char* __restrict__ vdst, const unsigned char* __restrict__ ksrc,
                                           const unsigned char* __restrict__ vsrc) {
   using KT = KVTile<D, false>;
   using VT = KVTile<D, true>;
   const int lane = threadIdx.x & 63;
-  KT::load(Kb, k0_next, L, kdst, lane);
-  VT::load(Vb, k0_next, L, vdst, lane);
+  KT::load(Kb, k0_next, L, kdst, lane, next_dead);
+  VT::load(Vb, k0_next, L, vdst, lane, next_dead);
   wait_vmcnt<KT::kDmas + VT::kDmas>();
   attn_fold<RB, D>(st, scale_log2, k0, masked, ksrc, vsrc);
 }
@@ -340,7 +343,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   init_rows<RB, D>(st, s, q, req, g, L, 0);
 
   // Tile i of the item starts at key k_begin + 32i; the load past the last
-  // tile re-reads it (in bounds, never folded in).  Tile i+1 loads while
+  // tile is dead (one cache line per instruction, never folded in).  Tile i+1 loads while
   // tile i is folded in; the two stages swap after every tile.
   const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
   unsigned char* k0s = ks0 + wave * KT::kBytes;
@@ -351,8 +354,8 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   KT::load(Kb, key0(0), L, k0s, lane);
   VT::load(Vb, key0(0), L, v0s, lane);
   for (int i = 0; i < ntiles; ++i) {
-    attn_step<RB, D>(st, s.scale_log2, Kb, Vb, L, key0(i + 1), key0(i), key0(i) + kTile - 1 > L - s.G, k1s, v1s,
-                     k0s, v0s);
+    attn_step<RB, D>(st, s.scale_log2, Kb, Vb, L, key0(i + 1), i + 1 >= ntiles, key0(i),
+                     key0(i) + kTile - 1 > L - s.G, k1s, v1s, k0s, v0s);
     unsigned char* t = k0s;
     k0s = k1s;
     k1s = t;
@@ -407,10 +410,13 @@ void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
   // Whole K and V rows, KPI rows per wave-wide load (full cache lines),
   // streamed with the nontemporal hint: every row is read once.
   u32x4 kr[2][NV], vr[2][NV];
-  auto issue = [&](int set, int k0) {
+  // A dead tile (past the item's last) has every lane read one cache line.
+  auto issue = [&](int set, int i) {
+    const int k0 = key0(i);
+    const bool dead = i >= ntiles;
 #pragma unroll
     for (int it = 0; it < NV; ++it) {
-      const int64_t row = (int64_t)min(k0 + it * KPI + lane / LPR, L - 1) * D + (lane % LPR) * 8;
+      const int64_t row = dead ? (int64_t)k0 * D : (int64_t)min(k0 + it * KPI + lane / LPR, L - 1) * D + (lane % LPR) * 8;
       kr[set][it] = load_u32x4_stream(Kb + row);
       vr[set][it] = load_u32x4_stream(Vb + row);
     }
@@ -429,12 +435,12 @@ void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
   // Tile i+1 loads while tile i is folded in; the body always folds two
   // tiles (the second masked when the count is odd), so no branch separates
   // a load from its use.
-  issue(0, key0(0));
+  issue(0, 0);
   for (int i = 0; i < ntiles; i += 2) {
-    issue(1, key0(i + 1));
+    issue(1, i + 1);
     __builtin_amdgcn_sched_barrier(0);  // keep the next tile's loads ahead of this tile's work
     fold(0, key0(i), true);
-    issue(0, key0(i + 2));
+    issue(0, i + 2);
     __builtin_amdgcn_sched_barrier(0);
     fold(1, key0(i + 1), i + 1 < ntiles);
   }

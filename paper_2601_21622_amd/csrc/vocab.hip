@@ -1,26 +1,31 @@
 // Vocabulary projection with a fused softmax-statistics epilogue (gfx950).
 //
-// logits^T = W hidden^T on MFMA 16x16x32 bf16: a W fragment (16 vocabulary
-// rows x 32 k) is the A operand and a hidden fragment (16 rows x 32 k) the B
-// operand.  Each lane then holds four consecutive vocabulary entries of one
-// hidden row, which is what the logits store and the row statistics want.
+// logits^T = W hidden^T: a W fragment (vocabulary rows x k) is the MFMA A
+// operand and a hidden fragment the B operand, so each lane ends up holding
+// four consecutive vocabulary entries of one hidden row, which is what the
+// logits store and the row statistics want.
 //
 // A workgroup (4 waves) owns a tile of vocabulary rows for all hidden rows of
 // its M-tile, so W (the dominant stream, K*V*2 bytes) is read from HBM once.
-// Every wave streams its own W fragments straight into registers; the hidden
-// rows, shared by every workgroup and L2-resident, are staged per K-chunk in
-// LDS in MFMA-fragment order and read by all four waves.  Two schedules:
-//   * shallow (at most 64 hidden rows): one 16-entry vocabulary block per
-//     wave, 256-wide K-chunks, one chunk of prefetch; several workgroups per
-//     CU keep enough W in flight.
-//   * deep (more rows): the accumulators of up to 320 rows pin one workgroup
-//     to a CU, so W and hidden are prefetched through a 4-deep register ring
-//     of 32-wide K-chunks (three chunks in flight while one is multiplied),
-//     and each wave owns 2 or 4 vocabulary blocks, so that one LDS read of a
-//     hidden fragment feeds 2 or 4 MFMAs.
+// Every wave streams its own W fragments straight into registers, either from
+// the [V][K] layout or from the fragment-ordered copy sd_pack_vocab makes at
+// weight-load time (1 KB contiguous per fragment).  The hidden rows, shared by
+// every workgroup and L2-resident, are staged per K-chunk in LDS in
+// fragment order and read by all four waves.  Two schedules:
+//   * shallow (at most 64 hidden rows), MFMA 16x16x32: one 16-entry
+//     vocabulary block per wave, 256-wide K-chunks, one chunk of prefetch;
+//     several workgroups per CU keep enough W in flight.
+//   * deep (more rows), MFMA 32x32x16: the hidden rows are first repacked
+//     (pack_hidden_kernel) into 32-row fragments that LDS DMA moves 1 KB at a
+//     time; the accumulators of up to 384 rows pin one workgroup to a CU; W
+//     goes through a 6-slot register ring and hidden through 6 LDS stages,
+//     five 32-wide K-chunks ahead of the one multiplied, and each wave owns
+//     1 or 2 blocks of 32 vocabulary entries.  Workgroups that share a
+//     vocabulary tile (several M-tiles) are dealt to the same XCD.
 // The epilogue writes the float32 logits and, per (row, tile), the tile
-// maximum and the sum of exp(logit - maximum); a second kernel combines the
-// tiles of each row in fixed order into the row's log-sum-exp.
+// maximum and the sum of exp(logit - maximum); the row log-sum-exp is folded
+// from those in fixed order (lse_combine_kernel, or the acceptance kernel in
+// a whole step).
 #include <hip/hip_ext.h>
 
 #include <algorithm>
