@@ -1,8 +1,9 @@
 """GPU parity: sd_verify_attention against the float64 oracle (tolerance rule:
 |gpu - oracle| <= rtol * max(|oracle|, rms of the oracle row); rtol 2e-2 for
 bf16, 1e-4 for fp32).  Shapes span several 32-key tiles and 512+-key chunks,
-ragged tails, the shortest cache (L = G), GQA groups 1/4/8, head_dim 64/128,
-and more requests than one launch carries."""
+ragged tails, the shortest cache (L = G), GQA groups 1/4/8/16 (1 to 8 blocks
+of 16 query rows per KV head), head_dim 64/128, and more requests than one
+launch carries."""
 
 import numpy as np
 import pytest
@@ -28,6 +29,18 @@ CASES = {
                                            vocab=256, lengths=("explicit", (5, 70, 300))),
     "many_requests_bf16": get_config("pooled").replace(batch=70, n_q_heads=2, n_kv_heads=2, hidden=256,
                                                        vocab=128, lengths=("uniform", 5, 700)),
+    # Query rows per KV head = G * group: 40 (3 blocks of 16), 56 (4, head_dim 64), 88 (6), 112 (7), 128 (8).
+    "rows40_bf16": get_config("llama70b_share").replace(batch=2, gamma=4, n_q_heads=16, n_kv_heads=2, hidden=2048,
+                                                        vocab=256, lengths=("explicit", (5, 777))),
+    "rows56_d64_bf16": get_config("llama70b_share").replace(batch=2, gamma=6, n_q_heads=16, n_kv_heads=2,
+                                                            head_dim=64, hidden=1024, vocab=256,
+                                                            lengths=("explicit", (600, 7))),
+    "rows88_bf16": get_config("llama70b_share").replace(batch=2, gamma=10, n_q_heads=16, n_kv_heads=2,
+                                                        hidden=2048, vocab=256, lengths=("explicit", (11, 1030))),
+    "rows112_bf16": get_config("llama70b_share").replace(batch=2, gamma=6, n_q_heads=32, n_kv_heads=2,
+                                                         hidden=4096, vocab=256, lengths=("explicit", (700, 33))),
+    "rows128_bf16": get_config("llama70b_share").replace(batch=2, gamma=7, n_q_heads=32, n_kv_heads=2,
+                                                         hidden=4096, vocab=256, lengths=("explicit", (8, 2200))),
 }
 
 
