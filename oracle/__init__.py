@@ -21,6 +21,9 @@ What it computes (StarSD, "One-for-Many Speculative Decoding"):
   Algorithm 2, with the ratio rule of the Leviathan et al. formulation the
   paper adopts in Sec. 2 and whose acceptance probability is Eq. (1) of
   Sec. 3.2.  Followed step by step.
+* :mod:`oracle.warp` -- warped target distributions for sampled verification
+  (temperature, top-k, top-p, greedy), with which the same test and
+  correction stay lossless with respect to the warped target.  By definition.
 * :mod:`oracle.step` -- the composition of the three for one pooled batch.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against closed forms,
@@ -30,7 +33,8 @@ see those files for which pin covers which function.
 
 from .attention import verify_attention
 from .logits import verify_logits, probabilities
-from .accept import accept_request, accept_resample, near_threshold
+from .accept import accept_request, accept_resample, accept_resample_sampled, near_threshold
+from .warp import order_keys, warp_row, warped_from_cut
 from .step import verify_step
 
 __all__ = [
@@ -39,6 +43,10 @@ __all__ = [
     "probabilities",
     "accept_request",
     "accept_resample",
+    "accept_resample_sampled",
     "near_threshold",
+    "order_keys",
+    "warp_row",
+    "warped_from_cut",
     "verify_step",
 ]

@@ -153,6 +153,43 @@ def accept_resample(logits_or_probs, row_lse, q_draft, draft, u, kv_len=None):
     return {"accept_len": accept_len, "out_tok": out_tok, "new_kv_len": new_kv_len, "traces": traces}
 
 
+def accept_resample_sampled(logits, q_draft, draft, u, temperature, top_k=0, top_p=1.0, kv_len=None, cut=None):
+    """Verification against the warped target (``oracle.warp``): each row of
+    float32 logits becomes p' (temperature, top-k, top-p, or greedy when
+    temperature is 0) and the same test and correction run on p'.
+
+    ``cut`` = (theta_keys [B*G], lse [B*G], argmax [B*G]) makes p' the exact
+    distribution another implementation's cut and normaliser define, so that
+    acceptance decisions can be compared on identical p'; without it the cut
+    is computed here.  Returns the dict of ``accept_resample`` plus per-row
+    WarpedRow records (``rows``, only when ``cut`` is None) and ``near_cut``
+    [B] (a row of the request has its top-p cut within the decision band).
+    """
+    from .warp import warp_row, warped_from_cut
+
+    x = np.asarray(logits, dtype=np.float32)
+    draft = np.asarray(draft)
+    B, gamma = draft.shape
+    G = gamma + 1
+    if x.shape[0] != B * G:
+        raise ValueError("logits must have B * (gamma + 1) rows")
+    rows = []
+    pw = np.empty(x.shape, dtype=np.float64)
+    near_cut = np.zeros(B, dtype=bool)
+    for r in range(B * G):
+        if cut is None:
+            wr = warp_row(x[r], temperature, top_k, top_p)
+            rows.append(wr)
+            pw[r] = wr.p
+            near_cut[r // G] |= wr.near
+        else:
+            pw[r] = warped_from_cut(x[r], temperature, int(cut[0][r]), float(cut[1][r]), int(cut[2][r]))
+    out = accept_resample(pw, None, q_draft, draft, u, kv_len)
+    out["rows"] = rows
+    out["near_cut"] = near_cut
+    return out
+
+
 def near_threshold(trace: AcceptTrace, band: float = 1e-6) -> bool:
     """True when a draw lies within ``band`` of a decision boundary: an evaluated
     test with |u - ratio| < band, or a final draw with u*Z within band*Z of the
