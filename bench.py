@@ -101,6 +101,9 @@ def main() -> int:
                     help="LM-head weight layout: repacked once before timing (sd_pack_vocab), or [V][hidden]")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sampling", default=None, metavar="T,K,P",
+                    help="time sd_verify_step_sampled with temperature T, top-k K (0: off), top-p P (1: off) "
+                         "instead of the plain step (T = 0: greedy)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -152,11 +155,22 @@ def main() -> int:
         t["acc"] = torch.full((B,), -7, dtype=torch.int32, device="cuda")
         t["tok"] = torch.empty((B, G), dtype=torch.int32, device="cuda")
         t["new"] = torch.empty((B,), dtype=torch.int32, device="cuda")
+        t["rmin"] = torch.empty((M,), dtype=torch.float32, device="cuda")
         t["ws"] = torch.empty((ws_bytes,), dtype=torch.uint8, device="cuda")
         copies.append(t)
     log(f"{ncopies} input copies of {big_bytes / 1e6:.0f} MB each")
 
+    sampling = None
+    if args.sampling is not None:
+        s_t, s_k, s_p = args.sampling.split(",")
+        sampling = sd.Sampling(float(s_t), int(s_k), float(s_p))
+
     def prepared(t, events=None):
+        if sampling is not None:
+            return sd.prepare_verify_step_sampled(dims, sampling, t["q"], t["k_pool"], t["v_pool"], x.kv_off,
+                                                  x.kv_len, scale, t["hidden"], t["w"], t["q_draft"], t["draft"],
+                                                  t["u"], t["attn"], t["logits"], t["lse"], t["rmin"], t["acc"],
+                                                  t["tok"], t["new"], t["ws"], kernel_events=events)
         return sd.prepare_verify_step(dims, t["q"], t["k_pool"], t["v_pool"], x.kv_off, x.kv_len, scale, t["hidden"],
                                       t["w"], t["q_draft"], t["draft"], t["u"], t["attn"], t["logits"], t["lse"],
                                       t["acc"], t["tok"], t["new"], t["ws"], kernel_events=events)
@@ -256,6 +270,8 @@ def main() -> int:
             "head_dim": cfg.head_dim, "hidden": K, "vocab": V,
             "kv_len": list(cfg.lengths), "kv_tokens": int(x.kv_len.sum()), "draft": list(cfg.draft),
             "input_copies": ncopies, "vocab_layout": "packed" if packed else "row-major",
+            **({"sampling": {"temperature": sampling.temperature, "top_k": sampling.top_k, "top_p": sampling.top_p}}
+               if sampling is not None else {}),
         },
         "roofline": roof,
         "scored_tokens_per_s": B * G / (ms_step * 1e-3),
@@ -270,7 +286,7 @@ def main() -> int:
         "vocab_attainable_frac": vocab_tflops / min(BF16_MFMA_PEAK_TFLOPS, vocab_flops / vocab_bytes * HBM_PEAK_GBPS / 1e3),
         "wall_ms_per_step": wall * 1e3 / args.steps,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and sampling is None:  # the CPU leg times the plain step
         log("timing the CPU oracle on the same batch")
         result["cpu_baseline"] = cpu_baseline(x, args.cpu_seconds)
     print(json.dumps(result), flush=True)

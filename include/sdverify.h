@@ -196,6 +196,68 @@ SD_API int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_po
                    void* workspace, size_t workspace_bytes, sd_stream_t stream,
                    void* const* kernel_events);
 
+/*
+ * Sampled verification.  The test and correction of sd_accept_resample run on
+ * a warped target p' instead of p (the Leviathan test of Sec. 2 is lossless
+ * with respect to whichever target it is given).  q_draft must then hold the
+ * distributions the drafts were actually drawn from, i.e. the draft model's
+ * distributions warped the same way.  Warps of one row of target logits, in
+ * this order:
+ *   temperature T > 0     z = logit / T (T = 0 selects greedy, below);
+ *   top_k >= 1 (0: off)   keep every token whose logit is >= the k-th largest
+ *                         logit (ties of the k-th all kept; k >= V: off);
+ *   top_p in (0, 1)       of the kept tokens, keep the smallest set
+ *   (1: off)              {logit >= c} whose mass sum exp(z) reaches top_p
+ *                         times the kept total;
+ *   p'(v) = exp(z(v) - row_lse) on the kept set, 0 elsewhere.
+ * Greedy (T = 0): p' is one-hot on the first (smallest id) largest logit, so
+ * a draft is accepted iff it equals its row's argmax and the emitted token is
+ * the argmax of row l + 1; u and q do not change the result.
+ * "Order" is the order of float32 values with -0 below +0.  Logits must be
+ * finite.  Masses are evaluated in float32 and summed as 64-bit fixed point
+ * (2^(62 - ceil(log2 V)) per unit), so the cut is deterministic; it may differ
+ * from a float64 evaluation only when top_p lies within about 1e-6 of a
+ * cumulative mass.
+ */
+typedef struct {
+  float temperature;  /* >= 0, finite */
+  int32_t top_k;      /* >= 0 */
+  float top_p;        /* in (0, 1] */
+} sd_sampling_t;
+
+/*
+ * sd_accept_resample with a warped target.  Arguments as there, except:
+ *   logits         [M][V] float32 target logits (never probabilities)
+ *   row_lse        [M] float32 output: log sum over the kept set of exp(logit / T)
+ *                  (greedy rows: 0)
+ *   row_min_logit  [M] float32 output: the smallest kept logit; -inf when no cut
+ *                  applies, +inf for greedy rows.  Together with row_lse it
+ *                  defines p' exactly (see above).
+ *   workspace      sd_workspace_bytes(dims, ...) bytes suffice.
+ * The drafts' tests use p'(x_i) in float64 from the row's float32 cut and
+ * normaliser; the correction uses the float32 p' with float64 sums, as in
+ * sd_accept_resample.
+ */
+SD_API int sd_accept_resample_sampled(const sd_dims_t* dims, const sd_sampling_t* sampling, const float* logits,
+                                      const float* q_draft, const int32_t* draft_tok, const float* u,
+                                      const int32_t* kv_len, float* row_lse, float* row_min_logit,
+                                      int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
+                                      void* workspace, size_t workspace_bytes, sd_stream_t stream);
+
+/*
+ * sd_verify_step with a warped target: attention, projection, then
+ * sd_accept_resample_sampled on the logits it produced.  Arguments as in
+ * sd_verify_step and sd_accept_resample_sampled; kernel_events' last pair
+ * spans the warp kernel through the pick kernel.
+ */
+SD_API int sd_verify_step_sampled(const sd_dims_t* dims, const sd_sampling_t* sampling, const void* q,
+                                  const void* k_pool, const void* v_pool, const int64_t* kv_off,
+                                  const int32_t* kv_len, float scale, const void* hidden, const void* w_vocab,
+                                  const float* q_draft, const int32_t* draft_tok, const float* u, void* attn_out,
+                                  float* logits, float* row_lse, float* row_min_logit, int32_t* accept_len,
+                                  int32_t* out_tok, int32_t* new_kv_len, void* workspace, size_t workspace_bytes,
+                                  sd_stream_t stream, void* const* kernel_events);
+
 /* Static description of a status code. */
 SD_API const char* sd_status_string(int status);
 

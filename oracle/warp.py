@@ -77,8 +77,9 @@ def warp_row(row32, temperature: float, top_k: int = 0, top_p: float = 1.0, band
     if 0.0 < top_p < 1.0:
         total = float(w[keep].sum())
         target = top_p * total
-        levels = np.unique(keys[keep])[::-1]             # distinct kept keys, largest first
-        mass = np.array([w[keep & (keys == lv)].sum() for lv in levels])
+        levels, inv = np.unique(keys[keep], return_inverse=True)   # distinct kept keys, ascending
+        mass = np.bincount(inv, weights=w[keep], minlength=len(levels))
+        levels, mass = levels[::-1], mass[::-1]                       # largest first
         cum = np.cumsum(mass)
         j = int(np.nonzero(cum >= target)[0][0])
         near = abs(cum[j] - target) < band * total or (j > 0 and abs(cum[j - 1] - target) < band * total)
@@ -103,5 +104,5 @@ def warped_from_cut(row32, temperature: float, theta_key: int, lse: float, argma
         p[int(argmax)] = 1.0
         return p
     keys = order_keys(row32)
-    z = row32.astype(np.float64) * np.float64(np.float32(1.0 / np.float32(temperature)))
+    z = row32.astype(np.float64) * np.float64(np.float32(1.0) / np.float32(temperature))
     return np.where(keys >= theta_key, np.exp(z - np.float64(lse)), 0.0)

@@ -19,17 +19,21 @@ from ._binding import (  # noqa: F401
     SD_OK,
     Dims,
     PreparedCall,
+    Sampling,
     SdError,
     exported_symbols,
     library,
     library_path,
     prepare_verify_step,
+    prepare_verify_step_sampled,
     sd_accept_resample,
+    sd_accept_resample_sampled,
     sd_pack_vocab,
     sd_status_string,
     sd_verify_attention,
     sd_verify_logits,
     sd_verify_step,
+    sd_verify_step_sampled,
     sd_version,
     sd_vocab_packed_bytes,
     sd_workspace_bytes,

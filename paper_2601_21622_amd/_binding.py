@@ -55,6 +55,15 @@ class Dims(ctypes.Structure):
                     self.vocab, self.dtype, flags)
 
 
+class Sampling(ctypes.Structure):
+    """sd_sampling_t: temperature (0 = greedy), top_k (0 = off), top_p (1 = off)."""
+    _fields_ = [
+        ("temperature", ctypes.c_float),
+        ("top_k", ctypes.c_int32),
+        ("top_p", ctypes.c_float),
+    ]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -84,6 +93,11 @@ def library() -> ctypes.CDLL:
     lib.sd_accept_resample.restype = ctypes.c_int
     lib.sd_verify_step.argtypes = [DP, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
     lib.sd_verify_step.restype = ctypes.c_int
+    SP = ctypes.POINTER(Sampling)
+    lib.sd_accept_resample_sampled.argtypes = [DP, SP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.sd_accept_resample_sampled.restype = ctypes.c_int
+    lib.sd_verify_step_sampled.argtypes = [DP, SP, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
+    lib.sd_verify_step_sampled.restype = ctypes.c_int
     lib.sd_vocab_packed_bytes.argtypes = [DP]
     lib.sd_vocab_packed_bytes.restype = SZ
     lib.sd_pack_vocab.argtypes = [DP, P, P, P]
@@ -192,6 +206,17 @@ def sd_accept_resample(dims: Dims, logits_or_probs, row_lse, q_draft, draft_tok,
     _check(st, "sd_accept_resample")
 
 
+def sd_accept_resample_sampled(dims: Dims, sampling: Sampling, logits, q_draft, draft_tok, u, kv_len, row_lse,
+                               row_min_logit, accept_len, out_tok, new_kv_len, workspace, stream=None) -> None:
+    _len, len_p = _host(kv_len, np.int32)
+    st = library().sd_accept_resample_sampled(ctypes.byref(dims), ctypes.byref(sampling), _ptr(logits),
+                                              _ptr(q_draft), _ptr(draft_tok), _ptr(u), len_p, _ptr(row_lse),
+                                              _ptr(row_min_logit), _ptr(accept_len), _ptr(out_tok),
+                                              _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace),
+                                              _stream(stream))
+    _check(st, "sd_accept_resample_sampled")
+
+
 def _event_handles(events):
     if events is None:
         return None
@@ -241,6 +266,34 @@ def sd_verify_step(dims: Dims, q, k_pool, v_pool, kv_off, kv_len, scale: float, 
                              u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace, stream,
                              kernel_events)
     _check(library().sd_verify_step(*args), "sd_verify_step")
+
+
+def _step_sampled_args(dims, sampling, q, k_pool, v_pool, kv_off, kv_len, scale, hidden, w_vocab, q_draft,
+                       draft_tok, u, attn_out, logits, row_lse, row_min_logit, accept_len, out_tok, new_kv_len,
+                       workspace, stream=None, kernel_events=None):
+    off, off_p = _host(kv_off, np.int64)
+    ln, len_p = _host(kv_len, np.int32)
+    ev = _event_handles(kernel_events)
+    args = (ctypes.byref(dims), ctypes.byref(sampling), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p,
+            float(scale), _ptr(hidden), _ptr(w_vocab), _ptr(q_draft), _ptr(draft_tok), _ptr(u), _ptr(attn_out),
+            _ptr(logits), _ptr(row_lse), _ptr(row_min_logit), _ptr(accept_len), _ptr(out_tok), _ptr(new_kv_len),
+            _ptr(workspace), _nbytes(workspace), _stream(stream), ev)
+    return args, (dims, sampling, off, ln, ev)
+
+
+def sd_verify_step_sampled(dims: Dims, sampling: Sampling, q, k_pool, v_pool, kv_off, kv_len, scale: float, hidden,
+                           w_vocab, q_draft, draft_tok, u, attn_out, logits, row_lse, row_min_logit, accept_len,
+                           out_tok, new_kv_len, workspace, stream=None, kernel_events=None) -> None:
+    args, _keep = _step_sampled_args(dims, sampling, q, k_pool, v_pool, kv_off, kv_len, scale, hidden, w_vocab,
+                                     q_draft, draft_tok, u, attn_out, logits, row_lse, row_min_logit, accept_len,
+                                     out_tok, new_kv_len, workspace, stream, kernel_events)
+    _check(library().sd_verify_step_sampled(*args), "sd_verify_step_sampled")
+
+
+def prepare_verify_step_sampled(*a, **kw) -> PreparedCall:
+    """sd_verify_step_sampled with the same arguments, converted once (see PreparedCall)."""
+    args, keep = _step_sampled_args(*a, **kw)
+    return PreparedCall(library().sd_verify_step_sampled, args, (keep, a, kw), "sd_verify_step_sampled")
 
 
 def prepare_verify_step(*a, **kw) -> PreparedCall:

@@ -40,20 +40,43 @@ __device__ __forceinline__ float exp_diff(float a, float b) {
 
 struct AcceptArgs {
   int gamma, V, nseg, segs_per_group;
-  const float* x;        // [M][V] logits (lse != nullptr) or probabilities
+  const float* x;        // [M][V] logits (lse != nullptr or warp != nullptr) or probabilities
   const float* lse;      // [M] or nullptr
+  const WarpRow* warp;   // [M] or nullptr: warped target (sampled verification)
   const float* q;        // [B][gamma][V]
   const int32_t* draft;  // [B][gamma]
   const float* u;        // [B][G]
   double* segsum;        // [B][nseg] segment totals
 };
 
-__device__ __forceinline__ float r_of(const AcceptArgs& a, const float* xrow, const float* qrow, float lse,
-                                      bool residual, int v) {
-  const float p = a.lse != nullptr ? exp_diff(xrow[v], lse) : xrow[v];
-  if (!residual) return p;
-  const float d = p - qrow[v];
-  return d > 0.f ? d : 0.f;
+// How a row's p is evaluated: from probabilities, from logits and the row
+// log-sum-exp, or from logits and the row's warp (sampled verification).
+enum { kProbs = 0, kLogits = 1, kWarped = 2 };
+
+struct RowP {
+  float lse, inv_t;
+  uint32_t theta;
+  int argmax;
+};
+
+template <int PM>
+__device__ __forceinline__ float p_of(const RowP& rp, float x, int v) {
+  if (PM == kProbs) return x;
+  if (PM == kLogits) return exp_diff(x, rp.lse);
+  const float w = order_key(x) >= rp.theta ? exp_diff(x * rp.inv_t, rp.lse) : 0.f;
+  return v == rp.argmax ? 1.f : w;
+}
+
+__device__ __forceinline__ RowP row_p(const AcceptArgs& a, int64_t row, float lse) {
+  RowP rp{lse, 1.f, 0u, -1};
+  if (a.warp != nullptr) {
+    const WarpRow w = a.warp[row];
+    rp.lse = w.lse;
+    rp.inv_t = w.inv_t;
+    rp.theta = w.theta;
+    rp.argmax = w.argmax;
+  }
+  return rp;
 }
 
 constexpr int kSumWaves = 8;            // waves per workgroup of the sums kernel
@@ -65,7 +88,7 @@ constexpr int kTargetGroups = 512;      // sums-kernel workgroups aimed for per 
 
 // r over one segment, per lane (entries sg*512 + e*64 + lane): the raw loads
 // (indexes past the vocabulary clamped), then r from them.
-template <bool LSE, bool RES>
+template <bool RES>
 __device__ __forceinline__ void segment_issue(const float* xrow, const float* qrow, int V, int sg,
                                               float (&xs)[kPerLane], float (&qs)[kPerLane]) {
   const int lane = threadIdx.x & 63;
@@ -77,37 +100,48 @@ __device__ __forceinline__ void segment_issue(const float* xrow, const float* qr
   }
 }
 
-template <bool LSE, bool RES>
-__device__ __forceinline__ void segment_finish(float lse, int V, int sg, const float (&xs)[kPerLane],
+template <int PM, bool RES>
+__device__ __forceinline__ void segment_finish(const RowP& rp, int V, int sg, const float (&xs)[kPerLane],
                                                const float (&qs)[kPerLane], float (&r)[kPerLane]) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int e = 0; e < kPerLane; ++e) {
-    float v = LSE ? exp_diff(xs[e], lse) : xs[e];
+    const int v = sg * kSeg + e * kWave + lane;
+    float pv = p_of<PM>(rp, xs[e], v);
     if (RES) {
-      const float d = v - qs[e];
-      v = d > 0.f ? d : 0.f;
+      const float d = pv - qs[e];
+      pv = d > 0.f ? d : 0.f;
     }
-    r[e] = sg * kSeg + e * kWave + lane < V ? v : 0.f;
+    r[e] = v < V ? pv : 0.f;
   }
 }
 
-template <bool LSE, bool RES>
-__device__ __forceinline__ void segment_r(const float* xrow, const float* qrow, float lse, int V, int sg,
+template <int PM, bool RES>
+__device__ __forceinline__ void segment_r(const float* xrow, const float* qrow, const RowP& rp, int V, int sg,
                                           float (&r)[kPerLane]) {
   float xs[kPerLane], qs[kPerLane];
-  segment_issue<LSE, RES>(xrow, qrow, V, sg, xs, qs);
-  segment_finish<LSE, RES>(lse, V, sg, xs, qs, r);
+  segment_issue<RES>(xrow, qrow, V, sg, xs, qs);
+  segment_finish<PM, RES>(rp, V, sg, xs, qs, r);
 }
 
-__device__ __forceinline__ void segment_load(const AcceptArgs& a, const float* xrow, const float* qrow, float lse,
+__device__ __forceinline__ int p_mode(const AcceptArgs& a) {
+  return a.warp != nullptr ? kWarped : (a.lse != nullptr ? kLogits : kProbs);
+}
+
+__device__ __forceinline__ void segment_load(const AcceptArgs& a, const float* xrow, const float* qrow, const RowP& rp,
                                              bool residual, int sg, float (&r)[kPerLane]) {
-  if (a.lse != nullptr) {
-    if (residual) segment_r<true, true>(xrow, qrow, lse, a.V, sg, r);
-    else segment_r<true, false>(xrow, qrow, lse, a.V, sg, r);
-  } else {
-    if (residual) segment_r<false, true>(xrow, qrow, lse, a.V, sg, r);
-    else segment_r<false, false>(xrow, qrow, lse, a.V, sg, r);
+  switch (p_mode(a)) {
+    case kWarped:
+      if (residual) segment_r<kWarped, true>(xrow, qrow, rp, a.V, sg, r);
+      else segment_r<kWarped, false>(xrow, qrow, rp, a.V, sg, r);
+      break;
+    case kLogits:
+      if (residual) segment_r<kLogits, true>(xrow, qrow, rp, a.V, sg, r);
+      else segment_r<kLogits, false>(xrow, qrow, rp, a.V, sg, r);
+      break;
+    default:
+      if (residual) segment_r<kProbs, true>(xrow, qrow, rp, a.V, sg, r);
+      else segment_r<kProbs, false>(xrow, qrow, rp, a.V, sg, r);
   }
 }
 
@@ -121,35 +155,41 @@ __device__ __forceinline__ double segment_total(const float (&r)[kPerLane]) {
 
 // Totals of segments [sg0, sg1) into out[]: wave w takes sg0 + w, sg0 + w +
 // nwaves, ..., issuing the loads of kSegBatch segments before reducing any.
-template <bool LSE, bool RES>
-__device__ __forceinline__ void segment_totals_t(const float* xrow, const float* qrow, float lse, int V, int sg0,
+template <int PM, bool RES>
+__device__ __forceinline__ void segment_totals_t(const float* xrow, const float* qrow, const RowP& rp, int V, int sg0,
                                                  int sg1, int nwaves, double* out) {
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   for (int s0 = sg0 + wave; s0 < sg1; s0 += nwaves * kSegBatch) {
     float xs[kSegBatch][kPerLane], qs[kSegBatch][kPerLane];
 #pragma unroll
-    for (int k = 0; k < kSegBatch; ++k)
-      segment_issue<LSE, RES>(xrow, qrow, V, min(s0 + k * nwaves, sg1 - 1), xs[k], qs[k]);
+    for (int k = 0; k < kSegBatch; ++k) segment_issue<RES>(xrow, qrow, V, min(s0 + k * nwaves, sg1 - 1), xs[k], qs[k]);
 #pragma unroll
     for (int k = 0; k < kSegBatch; ++k) {
       const int sg = s0 + k * nwaves;
       float r[kPerLane];
-      segment_finish<LSE, RES>(lse, V, sg, xs[k], qs[k], r);
+      segment_finish<PM, RES>(rp, V, sg, xs[k], qs[k], r);
       const double t = segment_total(r);
       if (lane == 0 && sg < sg1) out[sg] = t;
     }
   }
 }
 
-__device__ __forceinline__ void segment_totals(const AcceptArgs& a, const float* xrow, const float* qrow, float lse,
-                                               bool residual, int sg0, int sg1, int nwaves, double* out) {
-  if (a.lse != nullptr) {
-    if (residual) segment_totals_t<true, true>(xrow, qrow, lse, a.V, sg0, sg1, nwaves, out);
-    else segment_totals_t<true, false>(xrow, qrow, lse, a.V, sg0, sg1, nwaves, out);
-  } else {
-    if (residual) segment_totals_t<false, true>(xrow, qrow, lse, a.V, sg0, sg1, nwaves, out);
-    else segment_totals_t<false, false>(xrow, qrow, lse, a.V, sg0, sg1, nwaves, out);
+__device__ __forceinline__ void segment_totals(const AcceptArgs& a, const float* xrow, const float* qrow,
+                                               const RowP& rp, bool residual, int sg0, int sg1, int nwaves,
+                                               double* out) {
+  switch (p_mode(a)) {
+    case kWarped:
+      if (residual) segment_totals_t<kWarped, true>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
+      else segment_totals_t<kWarped, false>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
+      break;
+    case kLogits:
+      if (residual) segment_totals_t<kLogits, true>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
+      else segment_totals_t<kLogits, false>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
+      break;
+    default:
+      if (residual) segment_totals_t<kProbs, true>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
+      else segment_totals_t<kProbs, false>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
   }
 }
 
@@ -196,7 +236,16 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
     if (lane < a.gamma) {
       double ratio = 0.0;
       if (valid) {
-        const double px = a.lse != nullptr ? exp((double)xv - (double)s_lse[lane]) : (double)xv;
+        double px;
+        if (a.warp != nullptr) {
+          // Warped target: the row's cut and normaliser (greedy: one-hot).
+          const WarpRow w = a.warp[(int64_t)req * G + lane];
+          const int tok = a.draft[(int64_t)req * a.gamma + lane];
+          px = tok == w.argmax ? 1.0
+                               : (order_key(xv) >= w.theta ? exp((double)xv * (double)w.inv_t - (double)w.lse) : 0.0);
+        } else {
+          px = a.lse != nullptr ? exp((double)xv - (double)s_lse[lane]) : (double)xv;
+        }
         const double qx = (double)qv;
         ratio = (px <= 0.0) ? 0.0 : (qx <= 0.0 ? (double)INFINITY : px / qx);
       }
@@ -211,7 +260,7 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
   }
   __syncthreads();
   const int l = s_l;
-  const float lse = a.lse != nullptr ? s_lse[l] : 0.f;
+  const RowP rp = row_p(a, (int64_t)req * G + l, a.lse != nullptr ? s_lse[l] : 0.f);
   const bool residual = l < a.gamma;
   const float* xrow = a.x + ((int64_t)req * G + l) * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
@@ -219,7 +268,7 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
   // 3. This workgroup's segment totals.
   const int sg0 = s * a.segs_per_group;
   const int sg1 = min(a.nseg, sg0 + a.segs_per_group);
-  segment_totals(a, xrow, qrow, lse, residual, sg0, sg1, kSumWaves, a.segsum + (int64_t)req * a.nseg);
+  segment_totals(a, xrow, qrow, rp, residual, sg0, sg1, kSumWaves, a.segsum + (int64_t)req * a.nseg);
 }
 
 // One wave per request: prefix of the segment totals, the segment holding
@@ -246,7 +295,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
     for (int k = 0; k < 8; ++k)
       if (base + k * kWave + lane < nseg) seg[base + k * kWave + lane] = v[k];
   }
-  const float lse = a.lse != nullptr ? a.lse[(int64_t)req * G + l] : 0.f;
+  const RowP rp = row_p(a, (int64_t)req * G + l, a.lse != nullptr ? a.lse[(int64_t)req * G + l] : 0.f);
   bool residual = l < a.gamma;
   const float* xrow = a.x + ((int64_t)req * G + l) * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
@@ -269,7 +318,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   if (!(z > 0.0) && residual) {
     // The residual vanished (possible only through rounding): sample from p_{l+1}.
     residual = false;
-    segment_totals(a, xrow, qrow, lse, false, 0, nseg, 1, seg);
+    segment_totals(a, xrow, qrow, rp, false, 0, nseg, 1, seg);
     z = prefix();
   }
 
@@ -283,7 +332,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   int t = -1;
   if (found >= 0) {
     float rv[kPerLane];
-    segment_load(a, xrow, qrow, lse, residual, found, rv);
+    segment_load(a, xrow, qrow, rp, residual, found, rv);
     double c = found > 0 ? seg[found - 1] : 0.0;
     int last_pos = -1;
 #pragma unroll
@@ -303,7 +352,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
     // No prefix sum exceeds u * Z: the largest token with mass.
     for (int sg = nseg - 1; sg >= 0 && t < 0; --sg) {
       float rv[kPerLane];
-      segment_load(a, xrow, qrow, lse, residual, sg, rv);
+      segment_load(a, xrow, qrow, rp, residual, sg, rv);
       for (int e = kPerLane - 1; e >= 0 && t < 0; --e) {
         const unsigned long long pos = __ballot(rv[e] > 0.f);
         if (pos) t = sg * kSeg + e * kWave + 63 - __clzll(pos);
@@ -331,7 +380,7 @@ size_t accept_workspace_bytes(int B, int V) {
 hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
                          const float2* partials, int ntiles, const float* q_draft, const int32_t* draft_tok,
                          const float* u, void* ws, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
-                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop, const WarpRow* warp) {
   (void)B;
   if (bt.nreq <= 0) return hipSuccess;
   AcceptArgs a;
@@ -344,14 +393,15 @@ hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const f
   const int64_t want = ((int64_t)a.nseg * bt.nreq + kTargetGroups - 1) / kTargetGroups;
   a.segs_per_group = (int)std::min<int64_t>(a.nseg, std::max<int64_t>(kSumWaves, (want + kSumWaves - 1) / kSumWaves * kSumWaves));
   a.x = x;
-  a.lse = row_lse;
+  a.lse = warp != nullptr ? nullptr : row_lse;
+  a.warp = warp;
   a.q = q_draft;
   a.draft = draft_tok;
   a.u = u;
   a.segsum = static_cast<double*>(ws);
   const int S = (a.nseg + a.segs_per_group - 1) / a.segs_per_group;
   hipExtLaunchKernelGGL(accept_sums_kernel, dim3(S, bt.nreq), dim3(kSumWaves * kWave), 0, stream, ev_start, nullptr,
-                        0, a, bt, partials, ntiles, accept_len);
+                        0, a, bt, warp != nullptr ? nullptr : partials, ntiles, accept_len);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, nullptr, ev_stop, 0, a, bt,

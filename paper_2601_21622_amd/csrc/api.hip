@@ -138,7 +138,7 @@ int run_logits(const sd_dims_t* d, const void* hidden, const void* w, float* log
 int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const float2* partials, int ntiles,
                const float* q_draft, const int32_t* draft_tok, const float* u, const int32_t* kv_len,
                int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len, void* ws, hipStream_t stream,
-               hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
+               hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const WarpRow* warp = nullptr) {
   for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
     AcceptBatch bt;
     memset(&bt, 0, sizeof(bt));
@@ -150,13 +150,24 @@ int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const f
     const bool first = r0 == 0, last = r0 + kMaxReqPerLaunch >= d->batch;
     hipError_t e = launch_accept(d->gamma, d->vocab, d->batch, bt, x, row_lse, partials, ntiles, q_draft, draft_tok,
                                  u, ws, accept_len, out_tok, new_kv_len, stream, first ? ev_start : nullptr,
-                                 last ? ev_stop : nullptr);
+                                 last ? ev_stop : nullptr, warp);
     if (e != hipSuccess) return SD_ERR_HIP;
   }
   return SD_OK;
 }
 
 size_t accept_ws(const sd_dims_t* d) { return align_up(accept_workspace_bytes(d->batch, d->vocab)); }
+
+// Warped target rows of sampled verification, after the acceptance sums.
+size_t warp_ws(const sd_dims_t* d) { return align_up(sizeof(WarpRow) * static_cast<size_t>(d->batch) * (d->gamma + 1)); }
+
+int check_sampling(const sd_sampling_t* sp) {
+  if (sp == nullptr) return SD_ERR_INVALID_ARGUMENT;
+  if (!std::isfinite(sp->temperature) || sp->temperature < 0.f) return SD_ERR_INVALID_ARGUMENT;
+  if (sp->top_k < 0) return SD_ERR_INVALID_ARGUMENT;
+  if (!(sp->top_p > 0.f && sp->top_p <= 1.f)) return SD_ERR_INVALID_ARGUMENT;
+  return SD_OK;
+}
 
 int check_accept_args(const float* x, const float* row_lse, const float* q_draft, const int32_t* draft_tok,
                       const float* u, const int32_t* kv_len, const int32_t* accept_len, const int32_t* out_tok,
@@ -176,7 +187,7 @@ extern "C" {
 size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
   if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
   const int64_t chunks = attn_max_chunks(dims->dtype, dims->n_kv_heads, dims->batch, max_kv_len);
-  return std::max(attention_ws(dims, chunks), logits_ws(dims) + accept_ws(dims));
+  return std::max(attention_ws(dims, chunks), logits_ws(dims) + accept_ws(dims) + warp_ws(dims));
 }
 
 int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
@@ -250,7 +261,7 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   if (st != SD_OK) return st;
   const AttnShape s = attn_shape(dims, scale, kv_len);
   const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
-                               logits_ws(dims) + accept_ws(dims));
+                               logits_ws(dims) + accept_ws(dims) + warp_ws(dims));
   if (workspace_bytes < need) return SD_ERR_WORKSPACE;
 
   hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
@@ -273,6 +284,78 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   void* acc_ws = static_cast<char*>(workspace) + logits_ws(dims);
   return run_accept(dims, logits, row_lse, partials, vp.ntiles, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
                     new_kv_len, acc_ws, stm, ev[4], ev[5]);
+}
+
+int sd_accept_resample_sampled(const sd_dims_t* dims, const sd_sampling_t* sampling, const float* logits,
+                               const float* q_draft, const int32_t* draft_tok, const float* u, const int32_t* kv_len,
+                               float* row_lse, float* row_min_logit, int32_t* accept_len, int32_t* out_tok,
+                               int32_t* new_kv_len, void* workspace, size_t workspace_bytes, sd_stream_t stream) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  st = check_sampling(sampling);
+  if (st != SD_OK) return st;
+  st = check_accept_args(logits, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok, new_kv_len);
+  if (st != SD_OK) return st;
+  if (!row_lse || !row_min_logit || !aligned(row_min_logit, 4)) return SD_ERR_INVALID_ARGUMENT;
+  if (workspace == nullptr || !aligned(workspace, 16)) return SD_ERR_INVALID_ARGUMENT;
+  if (kv_len != nullptr)
+    for (int b = 0; b < dims->batch; ++b)
+      if (kv_len[b] < dims->gamma + 1 || kv_len[b] > kMaxKvLen) return SD_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < accept_ws(dims) + warp_ws(dims)) return SD_ERR_WORKSPACE;
+  hipStream_t stm = static_cast<hipStream_t>(stream);
+  WarpRow* warp = reinterpret_cast<WarpRow*>(static_cast<char*>(workspace) + accept_ws(dims));
+  if (launch_warp(dims->batch * (dims->gamma + 1), dims->vocab, logits, sampling->temperature, sampling->top_k,
+                  sampling->top_p, warp, row_lse, row_min_logit, stm, nullptr) != hipSuccess)
+    return SD_ERR_HIP;
+  return run_accept(dims, logits, nullptr, nullptr, 0, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
+                    new_kv_len, workspace, stm, nullptr, nullptr, warp);
+}
+
+int sd_verify_step_sampled(const sd_dims_t* dims, const sd_sampling_t* sampling, const void* q, const void* k_pool,
+                           const void* v_pool, const int64_t* kv_off, const int32_t* kv_len, float scale,
+                           const void* hidden, const void* w_vocab, const float* q_draft, const int32_t* draft_tok,
+                           const float* u, void* attn_out, float* logits, float* row_lse, float* row_min_logit,
+                           int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len, void* workspace,
+                           size_t workspace_bytes, sd_stream_t stream, void* const* kernel_events) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  st = check_sampling(sampling);
+  if (st != SD_OK) return st;
+  if (!q || !k_pool || !v_pool || !attn_out || !w_vocab || !logits || !row_lse || !row_min_logit || !workspace)
+    return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(attn_out, 16) ||
+      !aligned(w_vocab, 16) || !aligned(logits, 16) || !aligned(row_lse, 4) || !aligned(row_min_logit, 4) ||
+      !aligned(workspace, 16) || (hidden != nullptr && !aligned(hidden, 16)))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (hidden == nullptr && dims->hidden != dims->n_q_heads * dims->head_dim) return SD_ERR_INVALID_ARGUMENT;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return SD_ERR_INVALID_ARGUMENT;
+  st = check_accept_args(logits, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok, new_kv_len);
+  if (st != SD_OK) return st;
+  st = check_kv(dims, kv_off, kv_len);
+  if (st != SD_OK) return st;
+  const AttnShape s = attn_shape(dims, scale, kv_len);
+  const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
+                               logits_ws(dims) + accept_ws(dims) + warp_ws(dims));
+  if (workspace_bytes < need) return SD_ERR_WORKSPACE;
+
+  hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  if (kernel_events != nullptr)
+    for (int i = 0; i < 6; ++i) ev[i] = static_cast<hipEvent_t>(kernel_events[i]);
+  hipStream_t stm = static_cast<hipStream_t>(stream);
+  st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out, workspace, stm, ev[0], ev[1]);
+  if (st != SD_OK) return st;
+  const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab,
+                                  (dims->flags & SD_FLAG_PACKED_VOCAB) != 0);
+  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, workspace, stm, ev[2],
+                   ev[3]) != hipSuccess)
+    return SD_ERR_HIP;
+  void* acc_ws = static_cast<char*>(workspace) + logits_ws(dims);
+  WarpRow* warp = reinterpret_cast<WarpRow*>(static_cast<char*>(acc_ws) + accept_ws(dims));
+  if (launch_warp(dims->batch * (dims->gamma + 1), dims->vocab, logits, sampling->temperature, sampling->top_k,
+                  sampling->top_p, warp, row_lse, row_min_logit, stm, ev[4]) != hipSuccess)
+    return SD_ERR_HIP;
+  return run_accept(dims, logits, nullptr, nullptr, 0, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
+                    new_kv_len, acc_ws, stm, nullptr, ev[5], warp);
 }
 
 size_t sd_vocab_packed_bytes(const sd_dims_t* dims) {

@@ -119,6 +119,13 @@ __device__ __forceinline__ void lds_wait() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
+// 32-bit key whose unsigned order is the order of the float32 values (-0
+// below +0): negative values bit-inverted, the others with the sign bit set.
+__device__ __forceinline__ uint32_t order_key(float f) {
+  const uint32_t b = __float_as_uint(f);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
 // Workgroup barrier that orders LDS traffic only.  __syncthreads() also waits
 // for every outstanding global load (vmcnt(0) on gfx9-family parts), which
 // would drain the prefetch pipeline of the streaming kernels.

@@ -75,6 +75,22 @@ hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const
 hipError_t launch_lse_combine(const VocabPlan& p, const float2* partials, float* row_lse,
                               hipStream_t stream);
 
+// Warped target rows for sampled verification: p'(v) = exp(logit(v) * inv_t
+// - lse) where order_key(logit(v)) >= theta, else 0; greedy rows (argmax >= 0)
+// are one-hot on argmax and have theta = 0xffffffff.
+struct WarpRow {
+  float inv_t;
+  uint32_t theta;
+  float lse;
+  int32_t argmax;
+};
+// temperature 0 selects greedy; top_k 0 or >= V and top_p >= 1 switch the cuts off.
+// Also writes each row's normaliser and smallest kept logit (-inf: no cut,
+// +inf: greedy) to row_lse / row_min_logit.  ev_start (may be null) is
+// recorded as the kernel starts.
+hipError_t launch_warp(int M, int V, const float* logits, float temperature, int top_k, float top_p, WarpRow* out,
+                       float* row_lse, float* row_min_logit, hipStream_t stream, hipEvent_t ev_start);
+
 // Acceptance and resampling.
 struct AcceptBatch {
   int32_t nreq;
@@ -88,10 +104,13 @@ size_t accept_workspace_bytes(int B, int V);
 // row log-sum-exp is folded first and written to row_lse.  ws holds
 // accept_workspace_bytes(B, V).  ev_start/ev_stop (may be null) time the
 // segment-sum kernel.
+// With `warp` (one WarpRow per row, from launch_warp) x holds logits and the
+// test and correction use the warped p'; row_lse and partials are then unused.
 hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& batch, const float* x,
                          const float* row_lse, const float2* partials, int ntiles,
                          const float* q_draft, const int32_t* draft_tok, const float* u, void* ws,
                          int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
-                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop);
+                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop,
+                         const WarpRow* warp = nullptr);
 
 }  // namespace sdv

@@ -1,0 +1,317 @@
+// Warped target rows for sampled verification (gfx950).
+//
+// Sampled decoding replaces the target p of the acceptance test (the
+// Leviathan test of Sec. 2) by a warped p': logits scaled by 1/T, then the
+// top-k cut (every token tied with the k-th largest logit kept), then the
+// top-p cut (the smallest set {logit >= theta} of the top-k-kept tokens whose
+// mass reaches top_p of their total), or, at T = 0, one-hot on the first
+// largest logit (greedy).  For each row this kernel finds the cut and the
+// normaliser; the acceptance kernels then evaluate
+//   p'(v) = [key(v) >= theta] exp(logit(v) / T - lse)   (greedy: [v == argmax]).
+//
+// One workgroup of 1024 threads per row:
+//   1. the largest logit and the first index holding it (one pass);
+//   2. top-k: a radix descent over the 32-bit order keys of the logits, 11, 11
+//      and 10 bits per level, with per-bucket counts and masses in LDS; the
+//      bucket where the running count from the top reaches k holds the cut;
+//   3. top-p: the same descent over the kept tokens, on masses, against
+//      ceil(top_p * kept mass);
+//   4. lse = max / T + log(kept mass).
+// Masses are exp((logit - max) / T) in float32, scaled by 2^S and truncated to
+// 64-bit integers (S = 62 - ceil(log2 V), so a whole row cannot overflow);
+// integer sums make every histogram and total independent of the order of
+// the atomic adds, so the cut is deterministic.
+#include <hip/hip_ext.h>
+
+#include <cmath>
+
+#include "common.h"
+#include "launch.h"
+
+namespace sdv {
+
+namespace {
+
+constexpr int kWarpThreads = 1024;
+constexpr int kWarpWaves = kWarpThreads / kWave;
+constexpr int kBuckets = 2048;
+
+__device__ __forceinline__ float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+__device__ __forceinline__ unsigned long long fixed_mass(float x, float m, float inv_t, double scale) {
+  const float w = expf((x - m) * inv_t);
+  return (unsigned long long)((double)w * scale);
+}
+
+__device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int mask) {
+  const uint32_t lo = __shfl_xor((uint32_t)v, mask);
+  const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), mask);
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+// Calls f(v, x[v]) for every element of the row, this thread's share, with
+// several loads in flight per thread (4 x float4 when the row is 16-byte
+// aligned, else 8 scalars).  The order in which a thread sees its elements is
+// unspecified; every reduction built on it is order-independent.
+template <typename F>
+__device__ __forceinline__ void row_pass(const float* __restrict__ x, int V, F&& f) {
+  const int tid = threadIdx.x;
+  if ((V & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) {
+    constexpr int U = 4;
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    const int V4 = V >> 2;
+    int i = tid;
+    for (; i + (U - 1) * kWarpThreads < V4; i += U * kWarpThreads) {
+      float4 r[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) r[u] = x4[i + u * kWarpThreads];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int v = 4 * (i + u * kWarpThreads);
+        f(v, r[u].x);
+        f(v + 1, r[u].y);
+        f(v + 2, r[u].z);
+        f(v + 3, r[u].w);
+      }
+    }
+    for (; i < V4; i += kWarpThreads) {
+      const float4 r = x4[i];
+      f(4 * i, r.x);
+      f(4 * i + 1, r.y);
+      f(4 * i + 2, r.z);
+      f(4 * i + 3, r.w);
+    }
+  } else {
+    constexpr int U = 8;
+    int v = tid;
+    for (; v + (U - 1) * kWarpThreads < V; v += U * kWarpThreads) {
+      float r[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) r[u] = x[v + u * kWarpThreads];
+#pragma unroll
+      for (int u = 0; u < U; ++u) f(v + u * kWarpThreads, r[u]);
+    }
+    for (; v < V; v += kWarpThreads) f(v, x[v]);
+  }
+}
+
+struct Level {
+  int shift, nb;
+  uint32_t hmask;  // bits above this level's digit
+};
+
+__device__ __forceinline__ Level level_of(int level) {
+  Level l;
+  l.shift = level == 0 ? 21 : (level == 1 ? 10 : 0);
+  l.nb = level == 2 ? 1024 : 2048;
+  l.hmask = level == 0 ? 0u : (0xffffffffu << (l.shift + (level == 2 ? 10 : 11)));
+  return l;
+}
+
+// Wave 0: scanning the buckets from the top, the first bucket at which the
+// running total (of counts, or of masses with BY_MASS) reaches `need`, and the
+// count and mass of the buckets above it.  need >= 1 and the buckets hold at
+// least `need` in total.
+template <bool BY_MASS>
+__device__ void select_bucket(const uint32_t* hcnt, const unsigned long long* hmass, int nb, unsigned long long need,
+                              uint32_t* lcnt, unsigned long long* lmass, uint32_t* s_bucket, uint32_t* s_cnt_above,
+                              unsigned long long* s_mass_above) {
+  const int lane = threadIdx.x & 63;
+  const int per = nb / kWave;
+  const int top = nb - 1 - lane * per;
+  uint32_t c = 0;
+  unsigned long long ms = 0;
+  for (int i = 0; i < per; ++i) {
+    c += hcnt[top - i];
+    ms += hmass[top - i];
+  }
+  lcnt[lane] = c;
+  lmass[lane] = ms;
+  lds_wait();
+  if (lane == 0) {
+    uint32_t cnt_run = 0;
+    unsigned long long mass_run = 0;
+    int L = 0;
+    for (; L < kWave - 1; ++L) {
+      const unsigned long long v = BY_MASS ? lmass[L] : (unsigned long long)lcnt[L];
+      const unsigned long long run = BY_MASS ? mass_run : (unsigned long long)cnt_run;
+      if (run + v >= need) break;
+      cnt_run += lcnt[L];
+      mass_run += lmass[L];
+    }
+    int b = nb - 1 - L * per;
+    for (int i = 0; i < per - 1; ++i, --b) {
+      const unsigned long long v = BY_MASS ? hmass[b] : (unsigned long long)hcnt[b];
+      const unsigned long long run = BY_MASS ? mass_run : (unsigned long long)cnt_run;
+      if (run + v >= need) break;
+      cnt_run += hcnt[b];
+      mass_run += hmass[b];
+    }
+    *s_bucket = (uint32_t)b;
+    *s_cnt_above = cnt_run;
+    *s_mass_above = mass_run;
+  }
+}
+
+__global__ __launch_bounds__(kWarpThreads)
+void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greedy, int top_k, float top_p,
+                 double scale, WarpRow* __restrict__ out, float* __restrict__ row_lse,
+                 float* __restrict__ row_min_logit) {
+  __shared__ uint32_t hcnt[kBuckets];
+  __shared__ unsigned long long hmass[kBuckets];
+  __shared__ uint32_t lcnt[kWave];
+  __shared__ unsigned long long lmass[kWave];
+  __shared__ uint32_t w_key[kWarpWaves];
+  __shared__ int w_idx[kWarpWaves];
+  __shared__ unsigned long long w_sum[kWarpWaves];
+  __shared__ uint32_t s_kmax, s_bucket, s_cnt_above;
+  __shared__ int s_amax;
+  __shared__ unsigned long long s_mass_above, s_total;
+
+  const int row = blockIdx.x;
+  const float* x = logits + (int64_t)row * V;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+
+  // 1. Largest key; among equal keys the smallest index.
+  auto merge = [](uint32_t& k, int& i, uint32_t ok, int oi) {
+    if (ok > k || (ok == k && oi < i)) {
+      k = ok;
+      i = oi;
+    }
+  };
+  uint32_t bk = 0;
+  int bi = 0x7fffffff;
+  row_pass(x, V, [&](int v, float xv) { merge(bk, bi, order_key(xv), v); });
+  for (int off = 32; off >= 1; off >>= 1) merge(bk, bi, __shfl_xor(bk, off), __shfl_xor(bi, off));
+  if (lane == 0) {
+    w_key[wave] = bk;
+    w_idx[wave] = bi;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t k = w_key[0];
+    int i = w_idx[0];
+    for (int w = 1; w < kWarpWaves; ++w) merge(k, i, w_key[w], w_idx[w]);
+    s_kmax = k;
+    s_amax = i;
+  }
+  __syncthreads();
+  const int amax = s_amax;
+  if (greedy) {
+    if (tid == 0) {
+      out[row] = WarpRow{0.f, 0xffffffffu, 0.f, amax};
+      row_lse[row] = 0.f;
+      row_min_logit[row] = INFINITY;
+    }
+    return;
+  }
+  const float m = key_value(s_kmax);
+
+  // Mass of the whole row (no top-k), or of the top-k set.
+  uint32_t theta = 0;
+  unsigned long long W = 0;
+  if (top_k >= 1 && top_k < V) {
+    uint32_t prefix = 0, krem = (uint32_t)top_k;
+    unsigned long long above = 0;
+    for (int level = 0; level < 3; ++level) {
+      const Level lv = level_of(level);
+      for (int i = tid; i < lv.nb; i += kWarpThreads) {
+        hcnt[i] = 0;
+        hmass[i] = 0;
+      }
+      __syncthreads();
+      row_pass(x, V, [&](int, float xv) {
+        const uint32_t k = order_key(xv);
+        if ((k & lv.hmask) == prefix) {
+          const int b = (k >> lv.shift) & (lv.nb - 1);
+          atomicAdd(&hcnt[b], 1u);
+          atomicAdd(&hmass[b], fixed_mass(xv, m, inv_t, scale));
+        }
+      });
+      __syncthreads();
+      if (wave == 0) select_bucket<false>(hcnt, hmass, lv.nb, krem, lcnt, lmass, &s_bucket, &s_cnt_above, &s_mass_above);
+      __syncthreads();
+      const uint32_t b = s_bucket;
+      krem -= s_cnt_above;
+      above += s_mass_above;
+      prefix |= b << lv.shift;
+      if (level == 2) W = above + hmass[b];
+      __syncthreads();
+    }
+    theta = prefix;
+  } else {
+    unsigned long long sum = 0;
+    row_pass(x, V, [&](int, float xv) { sum += fixed_mass(xv, m, inv_t, scale); });
+    for (int off = 32; off >= 1; off >>= 1) sum += shfl_xor_u64(sum, off);
+    if (lane == 0) w_sum[wave] = sum;
+    __syncthreads();
+    if (tid == 0) {
+      unsigned long long t = 0;
+      for (int w = 0; w < kWarpWaves; ++w) t += w_sum[w];
+      s_total = t;
+    }
+    __syncthreads();
+    W = s_total;
+  }
+
+  if (top_p < 1.f) {
+    unsigned long long target = (unsigned long long)ceil((double)top_p * (double)W);
+    target = target < 1 ? 1 : (target > W ? W : target);
+    uint32_t prefix = 0;
+    unsigned long long above = 0;
+    for (int level = 0; level < 3; ++level) {
+      const Level lv = level_of(level);
+      for (int i = tid; i < lv.nb; i += kWarpThreads) {
+        hcnt[i] = 0;
+        hmass[i] = 0;
+      }
+      __syncthreads();
+      row_pass(x, V, [&](int, float xv) {
+        const uint32_t k = order_key(xv);
+        if (k >= theta && (k & lv.hmask) == prefix) {
+          const int b = (k >> lv.shift) & (lv.nb - 1);
+          atomicAdd(&hcnt[b], 1u);
+          atomicAdd(&hmass[b], fixed_mass(xv, m, inv_t, scale));
+        }
+      });
+      __syncthreads();
+      if (wave == 0)
+        select_bucket<true>(hcnt, hmass, lv.nb, target - above, lcnt, lmass, &s_bucket, &s_cnt_above, &s_mass_above);
+      __syncthreads();
+      const uint32_t b = s_bucket;
+      above += s_mass_above;
+      prefix |= b << lv.shift;
+      if (level == 2) W = above + hmass[b];
+      __syncthreads();
+    }
+    theta = prefix;
+  }
+
+  if (tid == 0) {
+    const float lse = (float)((double)m * (double)inv_t + log((double)W / scale));
+    out[row] = WarpRow{inv_t, theta, lse, -1};
+    row_lse[row] = lse;
+    row_min_logit[row] = theta == 0 ? -INFINITY : key_value(theta);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_warp(int M, int V, const float* logits, float temperature, int top_k, float top_p, WarpRow* out,
+                       float* row_lse, float* row_min_logit, hipStream_t stream, hipEvent_t ev_start) {
+  if (M <= 0) return hipSuccess;
+  const int greedy = temperature == 0.f;
+  const float inv_t = greedy ? 0.f : 1.f / temperature;  // float32 division, correctly rounded
+  int bits = 0;
+  while ((int64_t(1) << bits) < V) ++bits;
+  const double scale = std::ldexp(1.0, 62 - bits);
+  hipExtLaunchKernelGGL(warp_kernel, dim3(M), dim3(kWarpThreads), 0, stream, ev_start, nullptr, 0, V, logits, inv_t,
+                        greedy, top_k, top_p, scale, out, row_lse, row_min_logit);
+  return hipGetLastError();
+}
+
+}  // namespace sdv

@@ -26,7 +26,7 @@ def test_library_loads_and_exports_header_symbols():
     names = sd.exported_symbols()
     assert set(names) == {"sd_workspace_bytes", "sd_verify_attention", "sd_verify_logits", "sd_accept_resample",
                           "sd_verify_step", "sd_status_string", "sd_version", "sd_vocab_packed_bytes",
-                          "sd_pack_vocab"}
+                          "sd_pack_vocab", "sd_accept_resample_sampled", "sd_verify_step_sampled"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2
@@ -106,6 +106,34 @@ def test_logits_and_accept_reject_bad_arguments():
     short = (ctypes.c_int32 * 2)(2, 10)
     assert lib.sd_accept_resample(ctypes.byref(d), P, P, P, P, P, short, P, P, P, None, 0, None) == \
         sd.SD_ERR_INVALID_ARGUMENT
+
+
+@cpu_only
+def test_sampled_calls_reject_bad_sampling_and_arguments():
+    lib = sd.library()
+    d = dims()
+
+    def acc(sp, row_min=P, ws_bytes=1 << 30):
+        return lib.sd_accept_resample_sampled(ctypes.byref(d), None if sp is None else ctypes.byref(sp), P, P, P, P,
+                                              None, P, row_min, P, P, None, P, ws_bytes, None)
+
+    good = sd.Sampling(0.8, 50, 0.9)
+    for bad in (None, sd.Sampling(-1.0, 0, 1.0), sd.Sampling(float("nan"), 0, 1.0), sd.Sampling(float("inf"), 0, 1.0),
+                sd.Sampling(1.0, -1, 1.0), sd.Sampling(1.0, 0, 0.0), sd.Sampling(1.0, 0, 1.5),
+                sd.Sampling(1.0, 0, float("nan"))):
+        assert acc(bad) == sd.SD_ERR_INVALID_ARGUMENT
+    assert acc(good, row_min=None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert acc(good, row_min=P + 2) == sd.SD_ERR_INVALID_ARGUMENT
+    assert acc(good, ws_bytes=64) == sd.SD_ERR_WORKSPACE
+    off = (ctypes.c_int64 * 2)(0, 8 * 128 * 2 * 64)
+    ln = (ctypes.c_int32 * 2)(64, 64)
+    args = [P, P, P, off, ln, 0.1, P, P, P, P, P, P, P, P, P, P, P, P, P, 1 << 30, None, None]
+    assert lib.sd_verify_step_sampled(ctypes.byref(d), ctypes.byref(sd.Sampling(-2.0, 0, 1.0)), *args) == \
+        sd.SD_ERR_INVALID_ARGUMENT
+    args_no_min = list(args)
+    args_no_min[14] = None  # row_min_logit
+    assert lib.sd_verify_step_sampled(ctypes.byref(d), ctypes.byref(good), *args_no_min) == sd.SD_ERR_INVALID_ARGUMENT
+    assert sd.sd_workspace_bytes(d, 1000) > 0
 
 
 @cpu_only
