@@ -86,6 +86,9 @@ CASES = [
     ("many_requests", 70, 3, 300, "noisy"),
     ("v128256", 6, 8, 128256, "noisy"),
     ("single_token_vocab", 5, 2, 1, "equal"),
+    ("max_gamma", 3, 63, 300, "noisy"),          # gamma at its limit: 64 positions, one per lane
+    ("max_gamma_equal", 2, 63, 300, "equal"),
+    ("max_vocab", 2, 1, 2097152, "noisy"),       # the largest vocabulary: 4096 segments of 512
 ]
 
 
