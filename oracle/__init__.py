@@ -24,6 +24,11 @@ What it computes (StarSD, "One-for-Many Speculative Decoding"):
 * :mod:`oracle.warp` -- warped target distributions for sampled verification
   (temperature, top-k, top-p, greedy), with which the same test and
   correction stay lossless with respect to the warped target.  By definition.
+* :mod:`oracle.tree` -- tree verification: tree-masked attention (each node
+  sees the prefix, the root and its ancestors) and lossless acceptance of a
+  candidate tree (candidates as point-mass proposals of the Sec. 2 test, in
+  place of the longest-path rule of Algorithm 2, which is not lossless).
+  Attention by definition; acceptance step by step.
 * :mod:`oracle.step` -- the composition of the three for one pooled batch.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against closed forms,
@@ -35,6 +40,7 @@ from .attention import verify_attention
 from .logits import verify_logits, probabilities
 from .accept import accept_request, accept_resample, accept_resample_sampled, near_threshold
 from .warp import order_keys, warp_row, warped_from_cut
+from .tree import accept_tree, accept_tree_request, ancestor_masks, tree_attention, tree_near_threshold
 from .step import verify_step
 
 __all__ = [
@@ -48,5 +54,10 @@ __all__ = [
     "order_keys",
     "warp_row",
     "warped_from_cut",
+    "accept_tree",
+    "accept_tree_request",
+    "ancestor_masks",
+    "tree_attention",
+    "tree_near_threshold",
     "verify_step",
 ]
