@@ -113,6 +113,24 @@ SD_API int sd_verify_attention(const sd_dims_t* dims, const void* q, const void*
                         sd_stream_t stream);
 
 /*
+ * Tree verification: attention of the G = gamma + 1 positions of a candidate
+ * tree (Algorithm 2's proposal tree, scored in one pass).  Here gamma is the
+ * number of tree nodes N; position 0 is the root (the last verified token)
+ * and position i + 1 is node i.  Arguments as in sd_verify_attention, plus
+ *   parent   [B][N] int32 (device): parent[b][i] in [-1, i) is node i's parent
+ *            node (-1: the root); parents precede their children.  A value
+ *            outside that range is taken as -1.
+ * The last G entries of each request's cache are the root and the nodes in
+ * position order.  Position g attends to every key before them and to tail
+ * position a iff a is g, the root or an ancestor of g.  A chain (parent[i] =
+ * i - 1) gives sd_verify_attention's result.
+ */
+SD_API int sd_verify_attention_tree(const sd_dims_t* dims, const void* q, const void* k_pool,
+                                    const void* v_pool, const int64_t* kv_off, const int32_t* kv_len,
+                                    const int32_t* parent, float scale, void* out, void* workspace,
+                                    size_t workspace_bytes, sd_stream_t stream);
+
+/*
  * Repacked vocabulary weights.  The projection streams W once per step; in
  * the [V][hidden] layout every MFMA operand load touches 16 rows 2*hidden
  * bytes apart.  sd_pack_vocab rewrites W once (at weight-load time) into

@@ -31,6 +31,7 @@ from ._binding import (  # noqa: F401
     sd_pack_vocab,
     sd_status_string,
     sd_verify_attention,
+    sd_verify_attention_tree,
     sd_verify_logits,
     sd_verify_step,
     sd_verify_step_sampled,

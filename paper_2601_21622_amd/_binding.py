@@ -93,6 +93,8 @@ def library() -> ctypes.CDLL:
     lib.sd_accept_resample.restype = ctypes.c_int
     lib.sd_verify_step.argtypes = [DP, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
     lib.sd_verify_step.restype = ctypes.c_int
+    lib.sd_verify_attention_tree.argtypes = [DP, P, P, P, P, P, P, F, P, P, SZ, P]
+    lib.sd_verify_attention_tree.restype = ctypes.c_int
     SP = ctypes.POINTER(Sampling)
     lib.sd_accept_resample_sampled.argtypes = [DP, SP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.sd_accept_resample_sampled.restype = ctypes.c_int
@@ -189,6 +191,16 @@ def sd_verify_attention(dims: Dims, q, k_pool, v_pool, kv_off: Sequence[int], kv
                                        float(scale), _ptr(out), _ptr(workspace), _nbytes(workspace),
                                        _stream(stream))
     _check(st, "sd_verify_attention")
+
+
+def sd_verify_attention_tree(dims: Dims, q, k_pool, v_pool, kv_off: Sequence[int], kv_len: Sequence[int], parent,
+                             scale: float, out, workspace, stream=None) -> None:
+    _off, off_p = _host(kv_off, np.int64)
+    _len, len_p = _host(kv_len, np.int32)
+    st = library().sd_verify_attention_tree(ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p,
+                                            _ptr(parent), float(scale), _ptr(out), _ptr(workspace),
+                                            _nbytes(workspace), _stream(stream))
+    _check(st, "sd_verify_attention_tree")
 
 
 def sd_verify_logits(dims: Dims, hidden, w_vocab, logits, row_lse, workspace, stream=None) -> None:

@@ -72,6 +72,9 @@ size_t attention_ws(const sd_dims_t* d, int64_t chunks) {
   return align_up(attn_partial_bytes(chunks, s.Hkv, s.rows, s.D));
 }
 
+// Tree verification: the ancestor masks, at the start of the workspace.
+size_t tree_ws(const sd_dims_t* d) { return align_up(sizeof(uint64_t) * static_cast<size_t>(d->batch) * (d->gamma + 1)); }
+
 size_t logits_ws(const sd_dims_t* d) {
   const VocabPlan p = vocab_plan(d->dtype, d->batch * (d->gamma + 1), d->hidden, d->vocab, (d->flags & SD_FLAG_PACKED_VOCAB) != 0);
   return align_up(vocab_workspace_bytes(p));
@@ -94,7 +97,7 @@ int hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
 // most kMaxReqPerLaunch requests whose tables ride in the kernel arguments.
 int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* v, const int64_t* kv_off,
                   const int32_t* kv_len, float scale, void* out, void* ws, hipStream_t stream,
-                  hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
+                  hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const uint64_t* anc = nullptr) {
   const AttnShape s = attn_shape(d, scale, kv_len);
   const int64_t chunks = total_chunks(kv_len, d->batch, s.chunk_keys);
   const AttnPartials parts = attn_carve(ws, chunks, s.Hkv, s.rows, s.D);
@@ -105,6 +108,7 @@ int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* 
     bt.nreq = std::min(kMaxReqPerLaunch, d->batch - r0);
     bt.req0 = r0;
     bt.chunk_base = static_cast<int32_t>(chunk_base);
+    bt.anc = anc;
     int32_t acc = 0;
     for (int i = 0; i < bt.nreq; ++i) {
       bt.chunk_prefix[i] = acc;
@@ -187,7 +191,7 @@ extern "C" {
 size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
   if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
   const int64_t chunks = attn_max_chunks(dims->dtype, dims->n_kv_heads, dims->batch, max_kv_len);
-  return std::max(attention_ws(dims, chunks), logits_ws(dims) + accept_ws(dims) + warp_ws(dims));
+  return std::max(tree_ws(dims) + attention_ws(dims, chunks), logits_ws(dims) + accept_ws(dims) + warp_ws(dims));
 }
 
 int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
@@ -207,6 +211,28 @@ int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool
     return SD_ERR_WORKSPACE;
   return run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, out, workspace,
                        static_cast<hipStream_t>(stream));
+}
+
+int sd_verify_attention_tree(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
+                             const int64_t* kv_off, const int32_t* kv_len, const int32_t* parent, float scale,
+                             void* out, void* workspace, size_t workspace_bytes, sd_stream_t stream) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!q || !k_pool || !v_pool || !out || !workspace || !parent) return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(out, 16) ||
+      !aligned(workspace, 16) || !aligned(parent, 4))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return SD_ERR_INVALID_ARGUMENT;
+  st = check_kv(dims, kv_off, kv_len);
+  if (st != SD_OK) return st;
+  const AttnShape s = attn_shape(dims, scale, kv_len);
+  if (workspace_bytes < tree_ws(dims) + attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)))
+    return SD_ERR_WORKSPACE;
+  hipStream_t stm = static_cast<hipStream_t>(stream);
+  uint64_t* masks = static_cast<uint64_t*>(workspace);
+  if (launch_tree_masks(dims->batch, dims->gamma, parent, masks, stm) != hipSuccess) return SD_ERR_HIP;
+  return run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, out,
+                       static_cast<char*>(workspace) + tree_ws(dims), stm, nullptr, nullptr, masks);
 }
 
 int sd_verify_logits(const sd_dims_t* dims, const void* hidden, const void* w_vocab, float* logits,

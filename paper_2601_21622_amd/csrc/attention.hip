@@ -57,6 +57,17 @@ __device__ __forceinline__ int find_request(const AttnBatch& bt, int c) {
   return lo;
 }
 
+// Visibility of key `key` to a row: every prefix key up to pend, then the G
+// tail positions (root, then drafts or tree nodes) whose bit is set in anc.
+// A chain row j has anc = bits 0..j (causal); a padding row has pend = -1 and
+// anc = 0 (nothing visible).
+__device__ __forceinline__ bool key_visible(int key, int pend, uint64_t anc) {
+  const unsigned off = (unsigned)(key - pend - 1);
+  return key <= pend || (off < 64u && ((anc >> off) & 1ull));
+}
+
+__device__ __forceinline__ uint64_t chain_mask(int j) { return j >= 63 ? ~0ull : ((2ull << j) - 1ull); }
+
 // Online softmax of one 16-row block over a 32-key tile, in the log2 domain:
 // the lane owns row lr of the block and keys k0 + kb*16 + lg*4 + e.  With
 // LAZY the reference maximum m of the rows moves lazily: only when some row's
@@ -64,9 +75,9 @@ __device__ __forceinline__ int find_request(const AttnBatch& bt, int c) {
 // new maxima and rescale the sums and O (rows whose maximum did not grow get
 // alpha = 1).  Otherwise p = 2^(s*scale - m) stays below 2^kLazyLog2, well
 // inside float32 and bfloat16 range, and O and the sum share the same m, so
-// the normalised result is unchanged.  Masking (keys past the row's causal
-// limit lim) applies only when `masked` (always without LAZY, which keeps the
-// step one branch-free block); a fully masked row gives p = 0.
+// the normalised result is unchanged.  Masking (key_visible) applies only
+// when `masked` (always without LAZY, which keeps the step one branch-free
+// block); a fully masked row gives p = 0.
 // Requires scale_log2 > 0 (the row maximum is taken before scaling).
 constexpr float kLazyLog2 = 8.f;
 // Up to this many row blocks the rescale branch costs nothing; with more, the
@@ -78,8 +89,8 @@ constexpr int kLazyMaxBlocks = 2;
 __device__ __forceinline__ float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
 
 template <int DB, bool LAZY>
-__device__ __forceinline__ bf16x8 softmax_tile(const f32x4 (&sc)[2], float scale_log2, bool masked, int k0, int lim,
-                                               float& m, float& lsum, f32x4 (&o)[DB]) {
+__device__ __forceinline__ bf16x8 softmax_tile(const f32x4 (&sc)[2], float scale_log2, bool masked, int k0, int pend,
+                                               uint64_t anc, float& m, float& lsum, f32x4 (&o)[DB]) {
   const int lg = (threadIdx.x & 63) >> 4;
   float raw[8];
 #pragma unroll
@@ -91,7 +102,7 @@ __device__ __forceinline__ bf16x8 softmax_tile(const f32x4 (&sc)[2], float scale
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (k0 + kb * 16 + lg * 4 + e > lim) raw[kb * 4 + e] = -INFINITY;
+        if (!key_visible(k0 + kb * 16 + lg * 4 + e, pend, anc)) raw[kb * 4 + e] = -INFINITY;
   }
   float mx = fmaxf(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])),
                    fmaxf(fmaxf(raw[4], raw[5]), fmaxf(raw[6], raw[7])));
@@ -157,7 +168,8 @@ struct KVTile {
 template <int RB, int D>
 struct AttnRows {
   bf16x8 qf[RB][D / 32];  // Q fragments, B operand of S^T = K Q^T
-  int lim[RB];            // last visible key of the lane's row (-1: padding row)
+  int pend[RB];           // last visible prefix key of the lane's row (-1: padding row)
+  uint64_t anc[RB];       // visible tail positions of the lane's row
   float m[RB], lsum[RB];  // running maximum (log2 domain) and sum
   f32x4 o[RB][D / 16];    // running O^T blocks
 };
@@ -202,7 +214,8 @@ __device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2,
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
     pf[rb] = softmax_tile<DB, (RB <= kLazyMaxBlocks)>(sc[rb], scale_log2, masked || !live, k0,
-                                                      live ? st.lim[rb] : -1, st.m[rb], st.lsum[rb], st.o[rb]);
+                                                      live ? st.pend[rb] : -1, live ? st.anc[rb] : 0ull,
+                                                      st.m[rb], st.lsum[rb], st.o[rb]);
 
   // V^T fragments (A operand of O^T += V^T P^T): lane (lg, lr) needs
   // d = db*16 + lr and keys {lg*4 .. +3} then {16 + lg*4 .. +3}, the
@@ -278,8 +291,8 @@ __device__ __forceinline__ void write_partial(const AttnShape& s, const AttnBatc
 // (B operand of S^T = K Q^T; lane holds row row0 + rb*16 + lr, d = ds*32 +
 // lg*8 .. +8), causal limits, empty sums.  Rows past s.rows are padding.
 template <int RB, int D>
-__device__ __forceinline__ void init_rows(AttnRows<RB, D>& st, const AttnShape& s, const uint16_t* __restrict__ q,
-                                          int req, int g, int L, int row0) {
+__device__ __forceinline__ void init_rows(AttnRows<RB, D>& st, const AttnShape& s, const uint64_t* __restrict__ anc,
+                                          const uint16_t* __restrict__ q, int req, int g, int L, int row0) {
   constexpr int DS = D / 32;
   constexpr int DB = D / 16;
   const int lane = threadIdx.x & 63;
@@ -294,11 +307,13 @@ __device__ __forceinline__ void init_rows(AttnRows<RB, D>& st, const AttnShape& 
       const uint16_t* qrow = q + (((int64_t)req * s.G + j) * s.Hq + h) * D;
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = load_bf16x8(qrow + ds * 32 + lg * 8);
-      st.lim[rb] = L - s.G + j;
+      st.pend[rb] = L - s.G - 1;
+      st.anc[rb] = anc != nullptr ? anc[(int64_t)req * s.G + j] : chain_mask(j);
     } else {
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = bf16x8{};
-      st.lim[rb] = -1;
+      st.pend[rb] = -1;
+      st.anc[rb] = 0ull;
     }
     st.m[rb] = kNegBig;
     st.lsum[rb] = 0.f;
@@ -340,7 +355,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   const uint16_t* Vb = vp + off + (int64_t)g * L * D;
 
   AttnRows<RB, D> st;
-  init_rows<RB, D>(st, s, q, req, g, L, 0);
+  init_rows<RB, D>(st, s, bt.anc, q, req, g, L, 0);
 
   // Tile i of the item starts at key k_begin + 32i; the load past the last
   // tile is dead (one cache line per instruction, never folded in).  Tile i+1 loads while
@@ -400,7 +415,7 @@ void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
   const uint16_t* Vb = vp + off + (int64_t)g * L * D;
 
   AttnRows<RB, D> st;
-  init_rows<RB, D>(st, s, q, req, g, L, 0);
+  init_rows<RB, D>(st, s, bt.anc, q, req, g, L, 0);
 
   const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
   unsigned char* vt = vsm + wave * VT::kBytes;
@@ -485,8 +500,9 @@ void attn_f32_kernel(const AttnShape s, const AttnBatch bt, const float* __restr
     const float* qr = qs + row * D;
     float acc = 0.f;
     for (int d = 0; d < D; ++d) acc = fmaf(qr[d], kr[d], acc);
-    const int lim = L - s.G + row / s.group;
-    ps[row * C + kk] = key > lim ? -INFINITY : acc * s.scale_log2;
+    const int j = row / s.group;
+    const uint64_t anc = bt.anc != nullptr ? bt.anc[(int64_t)req * s.G + j] : chain_mask(j);
+    ps[row * C + kk] = key_visible(key, L - s.G - 1, anc) ? acc * s.scale_log2 : -INFINITY;
   }
   __syncthreads();
   for (int row = wave; row < s.rows; row += kAttnWaves) {
@@ -593,6 +609,24 @@ hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchu
   }
 }
 
+// One workgroup per request, one thread per position: walk up the parents
+// (each step moves to a strictly smaller position, so at most g steps).
+__global__ __launch_bounds__(kWave)
+void tree_masks_kernel(int N, const int32_t* __restrict__ parent, uint64_t* __restrict__ masks) {
+  const int b = blockIdx.x;
+  const int G = N + 1;
+  for (int g = threadIdx.x; g < G; g += kWave) {
+    uint64_t m = 1ull;
+    int pos = g;
+    while (pos > 0) {
+      m |= 1ull << pos;
+      const int pp = parent[(int64_t)b * N + pos - 1];
+      pos = (pp >= -1 && pp < pos - 1) ? pp + 1 : 0;
+    }
+    masks[(int64_t)b * G + g] = m;
+  }
+}
+
 }  // namespace
 
 int attn_chunk_keys(int dtype, int rows, int Hkv, int64_t total_keys) {
@@ -658,6 +692,12 @@ hipError_t launch_attention_combine(int dtype, const AttnShape& s, const AttnBat
   else
     hipLaunchKernelGGL(attn_combine_kernel<uint16_t>, grid, dim3(kAttnThreads), 0, stream, s, bt, parts,
                        static_cast<uint16_t*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_tree_masks(int B, int N, const int32_t* parent, uint64_t* masks, hipStream_t stream) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(tree_masks_kernel, dim3(B), dim3(kWave), 0, stream, N, parent, masks);
   return hipGetLastError();
 }
 

@@ -18,7 +18,12 @@ struct AttnBatch {
   int32_t chunk_prefix[kMaxReqPerLaunch + 1];    // local chunk index where each request starts
   int32_t kv_len[kMaxReqPerLaunch];
   int64_t kv_off[kMaxReqPerLaunch];
+  const uint64_t* anc;  // tree verification: [B][G] ancestor masks (bit a: tail position a visible), or null
 };
+
+// Tree verification: ancestor masks [B][N + 1] from parents [B][N] (node i's
+// parent in [-1, i), -1 the root; anything else is taken as the root).
+hipError_t launch_tree_masks(int B, int N, const int32_t* parent, uint64_t* masks, hipStream_t stream);
 
 struct AttnShape {
   int G;            // query positions per request

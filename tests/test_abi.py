@@ -26,7 +26,8 @@ def test_library_loads_and_exports_header_symbols():
     names = sd.exported_symbols()
     assert set(names) == {"sd_workspace_bytes", "sd_verify_attention", "sd_verify_logits", "sd_accept_resample",
                           "sd_verify_step", "sd_status_string", "sd_version", "sd_vocab_packed_bytes",
-                          "sd_pack_vocab", "sd_accept_resample_sampled", "sd_verify_step_sampled"}
+                          "sd_pack_vocab", "sd_accept_resample_sampled", "sd_verify_step_sampled",
+                          "sd_verify_attention_tree"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2
