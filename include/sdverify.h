@@ -276,6 +276,55 @@ SD_API int sd_verify_step_sampled(const sd_dims_t* dims, const sd_sampling_t* sa
                                   int32_t* out_tok, int32_t* new_kv_len, void* workspace, size_t workspace_bytes,
                                   sd_stream_t stream, void* const* kernel_events);
 
+/*
+ * Tree verification: lossless acceptance of a candidate tree (Algorithm 2's
+ * top-k proposal tree, whose longest-path rule as printed does not preserve
+ * the target distribution).  dims->gamma is the number of nodes N; rows and
+ * draws follow the positions of sd_verify_attention_tree (position 0 the
+ * root, position i + 1 node i).
+ *   logits_or_probs [B*(N+1)][V] float32, row_lse [B*(N+1)] or NULL: as in
+ *                   sd_accept_resample (row g: the target after position g)
+ *   tokens   [B][N] int32: node i's token (a token outside [0, V) never passes)
+ *   parent   [B][N] int32: as in sd_verify_attention_tree
+ *   u        [B][N+1] float32 in [0,1): u[b][i] tests node i, u[b][N] drives
+ *            the final sample
+ *   accept_len [B] int32 output: accepted nodes (the depth reached)
+ *   out_tok  [B][N+1] int32 output: the accepted nodes' tokens, the final
+ *            token, then -1
+ *   out_node [B][N+1] int32 output: the accepted nodes in order, then -1
+ *   new_kv_len [B] int32 output or NULL: kv_len[b] - N + accept_len[b] (the
+ *            caller keeps the prefix, the root and the accepted nodes, moved
+ *            into consecutive positions)
+ *   workspace sd_workspace_bytes(dims, ...) bytes suffice.
+ * Rule: candidates are point-mass proposals of the Leviathan test (Sec. 2).
+ * At the current position (starting at the root) its children are tested in
+ * node order: child c passes iff u[c] < p(token_c) / (1 - R), R the target
+ * mass of the candidates rejected before it at this position (a token already
+ * rejected there has mass 0); the first child that passes is accepted and the
+ * walk moves to it.  When none passes (or there are none), the final token is
+ * drawn by inverse CDF in ascending token id, with u[N], from that position's
+ * p with the rejected candidates removed (float64 prefix sums; falls back to
+ * p itself when rounding leaves no mass).  Every emitted token then follows
+ * the target's next-token distribution; the draft distributions do not enter.
+ */
+SD_API int sd_accept_tree(const sd_dims_t* dims, const float* logits_or_probs, const float* row_lse,
+                          const int32_t* tokens, const int32_t* parent, const float* u, const int32_t* kv_len,
+                          int32_t* accept_len, int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len,
+                          void* workspace, size_t workspace_bytes, sd_stream_t stream);
+
+/*
+ * One whole tree verification step: sd_verify_attention_tree, sd_verify_logits
+ * (row_lse is an output), then sd_accept_tree.  Arguments as in those calls
+ * and sd_verify_step; kernel_events' last pair spans the tree walk through the
+ * pick kernel.
+ */
+SD_API int sd_verify_step_tree(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
+                               const int64_t* kv_off, const int32_t* kv_len, const int32_t* parent, float scale,
+                               const void* hidden, const void* w_vocab, const int32_t* tokens, const float* u,
+                               void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
+                               int32_t* out_node, int32_t* new_kv_len, void* workspace, size_t workspace_bytes,
+                               sd_stream_t stream, void* const* kernel_events);
+
 /* Static description of a status code. */
 SD_API const char* sd_status_string(int status);
 

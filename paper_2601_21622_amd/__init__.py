@@ -26,8 +26,10 @@ from ._binding import (  # noqa: F401
     library_path,
     prepare_verify_step,
     prepare_verify_step_sampled,
+    prepare_verify_step_tree,
     sd_accept_resample,
     sd_accept_resample_sampled,
+    sd_accept_tree,
     sd_pack_vocab,
     sd_status_string,
     sd_verify_attention,
@@ -35,6 +37,7 @@ from ._binding import (  # noqa: F401
     sd_verify_logits,
     sd_verify_step,
     sd_verify_step_sampled,
+    sd_verify_step_tree,
     sd_version,
     sd_vocab_packed_bytes,
     sd_workspace_bytes,

@@ -95,6 +95,10 @@ def library() -> ctypes.CDLL:
     lib.sd_verify_step.restype = ctypes.c_int
     lib.sd_verify_attention_tree.argtypes = [DP, P, P, P, P, P, P, F, P, P, SZ, P]
     lib.sd_verify_attention_tree.restype = ctypes.c_int
+    lib.sd_accept_tree.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.sd_accept_tree.restype = ctypes.c_int
+    lib.sd_verify_step_tree.argtypes = [DP, P, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
+    lib.sd_verify_step_tree.restype = ctypes.c_int
     SP = ctypes.POINTER(Sampling)
     lib.sd_accept_resample_sampled.argtypes = [DP, SP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.sd_accept_resample_sampled.restype = ctypes.c_int
@@ -229,6 +233,15 @@ def sd_accept_resample_sampled(dims: Dims, sampling: Sampling, logits, q_draft, 
     _check(st, "sd_accept_resample_sampled")
 
 
+def sd_accept_tree(dims: Dims, logits_or_probs, row_lse, tokens, parent, u, kv_len, accept_len, out_tok, out_node,
+                   new_kv_len, workspace, stream=None) -> None:
+    _len, len_p = _host(kv_len, np.int32)
+    st = library().sd_accept_tree(ctypes.byref(dims), _ptr(logits_or_probs), _ptr(row_lse), _ptr(tokens),
+                                  _ptr(parent), _ptr(u), len_p, _ptr(accept_len), _ptr(out_tok), _ptr(out_node),
+                                  _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace), _stream(stream))
+    _check(st, "sd_accept_tree")
+
+
 def _event_handles(events):
     if events is None:
         return None
@@ -306,6 +319,34 @@ def prepare_verify_step_sampled(*a, **kw) -> PreparedCall:
     """sd_verify_step_sampled with the same arguments, converted once (see PreparedCall)."""
     args, keep = _step_sampled_args(*a, **kw)
     return PreparedCall(library().sd_verify_step_sampled, args, (keep, a, kw), "sd_verify_step_sampled")
+
+
+def _step_tree_args(dims, q, k_pool, v_pool, kv_off, kv_len, parent, scale, hidden, w_vocab, tokens, u, attn_out,
+                    logits, row_lse, accept_len, out_tok, out_node, new_kv_len, workspace, stream=None,
+                    kernel_events=None):
+    off, off_p = _host(kv_off, np.int64)
+    ln, len_p = _host(kv_len, np.int32)
+    ev = _event_handles(kernel_events)
+    args = (ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p, _ptr(parent), float(scale),
+            _ptr(hidden), _ptr(w_vocab), _ptr(tokens), _ptr(u), _ptr(attn_out), _ptr(logits), _ptr(row_lse),
+            _ptr(accept_len), _ptr(out_tok), _ptr(out_node), _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace),
+            _stream(stream), ev)
+    return args, (dims, off, ln, ev)
+
+
+def sd_verify_step_tree(dims: Dims, q, k_pool, v_pool, kv_off, kv_len, parent, scale: float, hidden, w_vocab, tokens,
+                        u, attn_out, logits, row_lse, accept_len, out_tok, out_node, new_kv_len, workspace,
+                        stream=None, kernel_events=None) -> None:
+    args, _keep = _step_tree_args(dims, q, k_pool, v_pool, kv_off, kv_len, parent, scale, hidden, w_vocab, tokens, u,
+                                  attn_out, logits, row_lse, accept_len, out_tok, out_node, new_kv_len, workspace,
+                                  stream, kernel_events)
+    _check(library().sd_verify_step_tree(*args), "sd_verify_step_tree")
+
+
+def prepare_verify_step_tree(*a, **kw) -> PreparedCall:
+    """sd_verify_step_tree with the same arguments, converted once (see PreparedCall)."""
+    args, keep = _step_tree_args(*a, **kw)
+    return PreparedCall(library().sd_verify_step_tree, args, (keep, a, kw), "sd_verify_step_tree")
 
 
 def prepare_verify_step(*a, **kw) -> PreparedCall:

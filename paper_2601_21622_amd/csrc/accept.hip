@@ -47,6 +47,16 @@ struct AcceptArgs {
   const int32_t* draft;  // [B][gamma]
   const float* u;        // [B][G]
   double* segsum;        // [B][nseg] segment totals
+  const struct TreeFinal* tree;  // tree verification: per request, where the walk ended, or nullptr
+};
+
+// Where a request's tree walk ended: the position whose row the final token
+// is drawn from, and the candidates rejected there (excluded from that draw).
+struct TreeFinal {
+  int32_t pos;
+  int32_t nrej;
+  int32_t pad[2];
+  int32_t rej_tok[kWave];
 };
 
 // How a row's p is evaluated: from probabilities, from logits and the row
@@ -128,6 +138,14 @@ __device__ __forceinline__ int p_mode(const AcceptArgs& a) {
   return a.warp != nullptr ? kWarped : (a.lse != nullptr ? kLogits : kProbs);
 }
 
+__device__ __forceinline__ float p_of_mode(const AcceptArgs& a, const RowP& rp, float x, int v) {
+  switch (p_mode(a)) {
+    case kWarped: return p_of<kWarped>(rp, x, v);
+    case kLogits: return p_of<kLogits>(rp, x, v);
+    default: return p_of<kProbs>(rp, x, v);
+  }
+}
+
 __device__ __forceinline__ void segment_load(const AcceptArgs& a, const float* xrow, const float* qrow, const RowP& rp,
                                              bool residual, int sg, float (&r)[kPerLane]) {
   switch (p_mode(a)) {
@@ -204,6 +222,18 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int G = a.gamma + 1;
+
+  if (a.tree != nullptr) {
+    // Tree verification: the walk chose the row; sum its p (the rejected
+    // candidates are taken out by the pick kernel).
+    const int pos = a.tree[req].pos;
+    const int64_t row = (int64_t)req * G + pos;
+    const RowP rp = row_p(a, row, a.lse != nullptr ? a.lse[row] : 0.f);
+    const int sg0 = s * a.segs_per_group;
+    const int sg1 = min(a.nseg, sg0 + a.segs_per_group);
+    segment_totals(a, a.x + row * a.V, nullptr, rp, false, sg0, sg1, kSumWaves, a.segsum + (int64_t)req * a.nseg);
+    return;
+  }
 
   // 1. Test operands first, then the row log-sum-exp fold.
   float xv = 0.f, qv = 0.f, uv = 0.f;
@@ -295,10 +325,35 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
     for (int k = 0; k < 8; ++k)
       if (base + k * kWave + lane < nseg) seg[base + k * kWave + lane] = v[k];
   }
-  const RowP rp = row_p(a, (int64_t)req * G + l, a.lse != nullptr ? a.lse[(int64_t)req * G + l] : 0.f);
-  bool residual = l < a.gamma;
-  const float* xrow = a.x + ((int64_t)req * G + l) * a.V;
+  // Chain: row l, residual after a rejection.  Tree: the walk's final row,
+  // plain p without the candidates rejected there.
+  const bool tree = a.tree != nullptr;
+  const int pos = tree ? a.tree[req].pos : l;
+  const int nrej = tree ? a.tree[req].nrej : 0;
+  const int rej = tree && lane < nrej ? a.tree[req].rej_tok[lane] : -1;
+  const int64_t row = (int64_t)req * G + pos;
+  const RowP rp = row_p(a, row, a.lse != nullptr ? a.lse[row] : 0.f);
+  bool residual = !tree && l < a.gamma;
+  const float* xrow = a.x + row * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
+  // The p of each rejected candidate, evaluated as the segment sums did, is
+  // taken out of its segment (in candidate order, so deterministically).
+  __shared__ int s_rej[kWave];
+  const double rej_p = (tree && rej >= 0) ? (double)p_of_mode(a, rp, xrow[rej], rej) : 0.0;
+  s_rej[lane] = rej;
+  lds_wait();
+  for (int k = 0; k < nrej; ++k) {
+    const int tk = __shfl(rej, k);
+    const double pk = __shfl(rej_p, k);
+    if (lane == 0 && tk >= 0) seg[tk / kSeg] -= pk;
+    lds_wait();
+  }
+  int nexcl = nrej;
+  auto excluded = [&](int v) {
+    bool e = false;
+    for (int k = 0; k < nexcl; ++k) e |= s_rej[k] == v;
+    return e;
+  };
 
   // Inclusive prefix of the segment totals, in place.
   auto prefix = [&]() -> double {
@@ -315,9 +370,11 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
     return carry;
   };
   double z = prefix();
-  if (!(z > 0.0) && residual) {
-    // The residual vanished (possible only through rounding): sample from p_{l+1}.
+  if (!(z > 0.0) && (residual || nexcl > 0)) {
+    // The residual vanished (possible only through rounding): sample from p_{l+1}
+    // (tree: from the final row's p, no candidate excluded).
     residual = false;
+    nexcl = 0;
     segment_totals(a, xrow, qrow, rp, false, 0, nseg, 1, seg);
     z = prefix();
   }
@@ -338,7 +395,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
 #pragma unroll
     for (int e = 0; e < kPerLane; ++e) {
       const int v = found * kSeg + e * kWave + lane;
-      const double r = (double)rv[e];
+      const double r = excluded(v) ? 0.0 : (double)rv[e];
       const double cum = wave_inclusive_scan_f64(r) + c;
       const unsigned long long hit = __ballot(v < a.V && r > 0.0 && cum > thr);
       if (hit && t < 0) t = found * kSeg + e * kWave + __ffsll(hit) - 1;
@@ -354,13 +411,18 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
       float rv[kPerLane];
       segment_load(a, xrow, qrow, rp, residual, sg, rv);
       for (int e = kPerLane - 1; e >= 0 && t < 0; --e) {
-        const unsigned long long pos = __ballot(rv[e] > 0.f);
+        const unsigned long long pos = __ballot(rv[e] > 0.f && !excluded(sg * kSeg + e * kWave + lane));
         if (pos) t = sg * kSeg + e * kWave + 63 - __clzll(pos);
       }
     }
     if (t < 0) t = 0;  // no mass at all (non-finite input)
   }
 
+  if (tree) {
+    // The walk wrote the accepted nodes' tokens and the cache length.
+    if (lane < G && lane >= l) out_tok[(int64_t)req * G + lane] = lane == l ? t : -1;
+    return;
+  }
   if (lane < G) {
     int32_t v = -1;
     if (lane < l) v = a.draft[(int64_t)req * a.gamma + lane];
@@ -368,6 +430,91 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
     out_tok[(int64_t)req * G + lane] = v;
   }
   if (lane == 0 && new_kv_len != nullptr && bt.has_kv_len) new_kv_len[req] = bt.kv_len[b] - a.gamma + l;
+}
+
+// Tree verification, one wave per request (N = gamma nodes, N + 1 <= 64
+// positions; lane i stands for node i).  Candidates are point-mass proposals
+// of the ratio test: at the current position its children (nodes whose parent
+// sits there) are tested in node order, child c passing iff
+//   u[c] < p(token_c) / (1 - mass of the candidates already rejected here),
+// a token already rejected among its siblings having mass 0; the first child
+// that passes is accepted and the walk moves to it.  The walk ends at a
+// position none of whose children passes (or that has none); the final token
+// is drawn there from p without the rejected candidates by the sums and pick
+// kernels.  All test operands are gathered at once (lane i: node i's token
+// under its parent's row); the walk itself runs on registers and ballots.
+__global__ __launch_bounds__(kWave)
+void tree_walk_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t* __restrict__ tokens,
+                      const int32_t* __restrict__ parent, TreeFinal* __restrict__ fin,
+                      int32_t* __restrict__ accept_len, int32_t* __restrict__ out_tok,
+                      int32_t* __restrict__ out_node, int32_t* __restrict__ new_kv_len) {
+  const int b = blockIdx.x;
+  const int req = bt.req0 + b;
+  const int lane = threadIdx.x;
+  const int N = a.gamma;
+  const int G = N + 1;
+
+  int tok = -1, par = -1;
+  double pc = 0.0;
+  float uc = 1.f;
+  if (lane < N) {
+    tok = tokens[(int64_t)req * N + lane];
+    const int pp = parent[(int64_t)req * N + lane];
+    par = (pp >= -1 && pp < lane) ? pp : -1;
+    uc = a.u[(int64_t)req * G + lane];
+    if (tok >= 0 && tok < a.V) {
+      const int64_t row = (int64_t)req * G + par + 1;
+      const float xv = a.x[row * a.V + tok];
+      pc = a.lse != nullptr ? exp((double)xv - (double)a.lse[row]) : (double)xv;
+    } else {
+      tok = -1;
+    }
+  }
+
+  int pos = 0, l = 0, nrej = 0, rej_tok = -1;
+  int path = -1;  // lane j: the j-th accepted node
+  while (true) {
+    unsigned long long kids = __ballot(lane < N && par + 1 == pos);
+    double rejected_mass = 0.0;
+    nrej = 0;
+    rej_tok = -1;
+    int accepted = -1;
+    while (kids) {
+      const int c = __ffsll(kids) - 1;
+      kids &= kids - 1;
+      const int t = __shfl(tok, c);
+      const double pt = __shfl(pc, c);
+      const float ut = __shfl(uc, c);
+      const bool dup = t < 0 || __ballot(lane < nrej && rej_tok == t) != 0;
+      const double rest = 1.0 - rejected_mass;
+      const double thr = (dup || !(rest > 0.0)) ? 0.0 : pt / rest;
+      if ((double)ut < thr) {
+        accepted = c;
+        break;
+      }
+      if (!dup) {
+        rejected_mass += pt;
+        if (lane == nrej) rej_tok = t;
+        ++nrej;
+      }
+    }
+    if (accepted < 0) break;
+    if (lane == l) path = accepted;
+    ++l;
+    pos = accepted + 1;
+  }
+
+  if (lane < G) {
+    out_node[(int64_t)req * G + lane] = lane < l ? path : -1;
+    if (lane < l) out_tok[(int64_t)req * G + lane] = tokens[(int64_t)req * N + path];
+  }
+  if (lane == 0) {
+    accept_len[req] = l;
+    fin[req].pos = pos;
+    fin[req].nrej = nrej;
+    if (new_kv_len != nullptr && bt.has_kv_len) new_kv_len[req] = bt.kv_len[b] - N + l;
+  }
+  fin[req].rej_tok[lane] = lane < nrej ? rej_tok : -1;
 }
 
 }  // namespace
@@ -395,6 +542,7 @@ hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const f
   a.x = x;
   a.lse = warp != nullptr ? nullptr : row_lse;
   a.warp = warp;
+  a.tree = nullptr;
   a.q = q_draft;
   a.draft = draft_tok;
   a.u = u;
@@ -403,6 +551,48 @@ hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const f
   hipExtLaunchKernelGGL(accept_sums_kernel, dim3(S, bt.nreq), dim3(kSumWaves * kWave), 0, stream, ev_start, nullptr,
                         0, a, bt, warp != nullptr ? nullptr : partials, ntiles, accept_len);
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, nullptr, ev_stop, 0, a, bt,
+                        accept_len, out_tok, new_kv_len);
+  return hipGetLastError();
+}
+
+size_t accept_tree_workspace_bytes(int B, int V) {
+  return (accept_workspace_bytes(B, V) + 255) / 256 * 256 + sizeof(TreeFinal) * static_cast<size_t>(B);
+}
+
+hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
+                              const int32_t* tokens, const int32_t* parent, const float* u, void* ws,
+                              int32_t* accept_len, int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len,
+                              hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+  if (bt.nreq <= 0) return hipSuccess;
+  AcceptArgs a;
+  a.gamma = N;
+  a.V = V;
+  a.nseg = (V + kSeg - 1) / kSeg;
+  if (a.nseg > kMaxSeg || N + 1 > kWave) return hipErrorInvalidValue;
+  const int64_t want = ((int64_t)a.nseg * bt.nreq + kTargetGroups - 1) / kTargetGroups;
+  a.segs_per_group = (int)std::min<int64_t>(a.nseg, std::max<int64_t>(kSumWaves, (want + kSumWaves - 1) / kSumWaves * kSumWaves));
+  a.x = x;
+  a.lse = row_lse;
+  a.warp = nullptr;
+  a.q = nullptr;
+  a.draft = nullptr;
+  a.u = u;
+  // Workspace: segment totals [B][nseg], then one TreeFinal per request (all
+  // requests, indexed by the global request number).
+  const size_t seg_bytes = (accept_workspace_bytes(B, V) + 255) / 256 * 256;
+  a.segsum = static_cast<double*>(ws);
+  TreeFinal* fin = reinterpret_cast<TreeFinal*>(static_cast<char*>(ws) + seg_bytes);
+  a.tree = fin;
+  hipExtLaunchKernelGGL(tree_walk_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, ev_start, nullptr, 0, a, bt, tokens,
+                        parent, fin, accept_len, out_tok, out_node, new_kv_len);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int S = (a.nseg + a.segs_per_group - 1) / a.segs_per_group;
+  hipLaunchKernelGGL(accept_sums_kernel, dim3(S, bt.nreq), dim3(kSumWaves * kWave), 0, stream, a, bt,
+                     (const float2*)nullptr, 0, accept_len);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, nullptr, ev_stop, 0, a, bt,
                         accept_len, out_tok, new_kv_len);

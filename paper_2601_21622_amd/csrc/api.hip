@@ -165,6 +165,32 @@ size_t accept_ws(const sd_dims_t* d) { return align_up(accept_workspace_bytes(d-
 // Warped target rows of sampled verification, after the acceptance sums.
 size_t warp_ws(const sd_dims_t* d) { return align_up(sizeof(WarpRow) * static_cast<size_t>(d->batch) * (d->gamma + 1)); }
 
+size_t accept_tree_ws(const sd_dims_t* d) { return align_up(accept_tree_workspace_bytes(d->batch, d->vocab)); }
+
+// Workspace of the acceptance stage, whichever variant runs.
+size_t accept_stage_ws(const sd_dims_t* d) { return std::max(accept_ws(d) + warp_ws(d), accept_tree_ws(d)); }
+
+int run_accept_tree(const sd_dims_t* d, const float* x, const float* row_lse, const int32_t* tokens,
+                    const int32_t* parent, const float* u, const int32_t* kv_len, int32_t* accept_len,
+                    int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len, void* ws, hipStream_t stream,
+                    hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
+  for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
+    AcceptBatch bt;
+    memset(&bt, 0, sizeof(bt));
+    bt.nreq = std::min(kMaxReqPerLaunch, d->batch - r0);
+    bt.req0 = r0;
+    bt.has_kv_len = kv_len != nullptr;
+    if (kv_len != nullptr)
+      for (int i = 0; i < bt.nreq; ++i) bt.kv_len[i] = kv_len[r0 + i];
+    const bool first = r0 == 0, last = r0 + kMaxReqPerLaunch >= d->batch;
+    hipError_t e = launch_accept_tree(d->gamma, d->vocab, d->batch, bt, x, row_lse, tokens, parent, u, ws, accept_len,
+                                      out_tok, out_node, new_kv_len, stream, first ? ev_start : nullptr,
+                                      last ? ev_stop : nullptr);
+    if (e != hipSuccess) return SD_ERR_HIP;
+  }
+  return SD_OK;
+}
+
 int check_sampling(const sd_sampling_t* sp) {
   if (sp == nullptr) return SD_ERR_INVALID_ARGUMENT;
   if (!std::isfinite(sp->temperature) || sp->temperature < 0.f) return SD_ERR_INVALID_ARGUMENT;
@@ -191,7 +217,7 @@ extern "C" {
 size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
   if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
   const int64_t chunks = attn_max_chunks(dims->dtype, dims->n_kv_heads, dims->batch, max_kv_len);
-  return std::max(tree_ws(dims) + attention_ws(dims, chunks), logits_ws(dims) + accept_ws(dims) + warp_ws(dims));
+  return std::max(tree_ws(dims) + attention_ws(dims, chunks), logits_ws(dims) + accept_stage_ws(dims));
 }
 
 int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
@@ -287,7 +313,7 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   if (st != SD_OK) return st;
   const AttnShape s = attn_shape(dims, scale, kv_len);
   const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
-                               logits_ws(dims) + accept_ws(dims) + warp_ws(dims));
+                               logits_ws(dims) + accept_stage_ws(dims));
   if (workspace_bytes < need) return SD_ERR_WORKSPACE;
 
   hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
@@ -361,7 +387,7 @@ int sd_verify_step_sampled(const sd_dims_t* dims, const sd_sampling_t* sampling,
   if (st != SD_OK) return st;
   const AttnShape s = attn_shape(dims, scale, kv_len);
   const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
-                               logits_ws(dims) + accept_ws(dims) + warp_ws(dims));
+                               logits_ws(dims) + accept_stage_ws(dims));
   if (workspace_bytes < need) return SD_ERR_WORKSPACE;
 
   hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
@@ -382,6 +408,69 @@ int sd_verify_step_sampled(const sd_dims_t* dims, const sd_sampling_t* sampling,
     return SD_ERR_HIP;
   return run_accept(dims, logits, nullptr, nullptr, 0, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
                     new_kv_len, acc_ws, stm, nullptr, ev[5], warp);
+}
+
+int sd_accept_tree(const sd_dims_t* dims, const float* logits_or_probs, const float* row_lse, const int32_t* tokens,
+                   const int32_t* parent, const float* u, const int32_t* kv_len, int32_t* accept_len,
+                   int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len, void* workspace,
+                   size_t workspace_bytes, sd_stream_t stream) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!logits_or_probs || !tokens || !parent || !u || !accept_len || !out_tok || !out_node || !workspace)
+    return SD_ERR_INVALID_ARGUMENT;
+  if (new_kv_len != nullptr && kv_len == nullptr) return SD_ERR_INVALID_ARGUMENT;
+  const void* p4[] = {logits_or_probs, row_lse, tokens, parent, u, accept_len, out_tok, out_node, new_kv_len};
+  for (const void* p : p4)
+    if (p != nullptr && !aligned(p, 4)) return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(workspace, 16)) return SD_ERR_INVALID_ARGUMENT;
+  if (kv_len != nullptr)
+    for (int b = 0; b < dims->batch; ++b)
+      if (kv_len[b] < dims->gamma + 1 || kv_len[b] > kMaxKvLen) return SD_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < accept_tree_ws(dims)) return SD_ERR_WORKSPACE;
+  return run_accept_tree(dims, logits_or_probs, row_lse, tokens, parent, u, kv_len, accept_len, out_tok, out_node,
+                         new_kv_len, workspace, static_cast<hipStream_t>(stream));
+}
+
+int sd_verify_step_tree(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
+                        const int64_t* kv_off, const int32_t* kv_len, const int32_t* parent, float scale,
+                        const void* hidden, const void* w_vocab, const int32_t* tokens, const float* u,
+                        void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
+                        int32_t* out_node, int32_t* new_kv_len, void* workspace, size_t workspace_bytes,
+                        sd_stream_t stream, void* const* kernel_events) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!q || !k_pool || !v_pool || !attn_out || !w_vocab || !logits || !row_lse || !workspace || !parent || !tokens ||
+      !u || !accept_len || !out_tok || !out_node)
+    return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(q, 16) || !aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(attn_out, 16) ||
+      !aligned(w_vocab, 16) || !aligned(logits, 16) || !aligned(row_lse, 4) || !aligned(workspace, 16) ||
+      !aligned(parent, 4) || !aligned(tokens, 4) || !aligned(u, 4) || !aligned(accept_len, 4) ||
+      !aligned(out_tok, 4) || !aligned(out_node, 4) || (new_kv_len != nullptr && !aligned(new_kv_len, 4)) ||
+      (hidden != nullptr && !aligned(hidden, 16)))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (hidden == nullptr && dims->hidden != dims->n_q_heads * dims->head_dim) return SD_ERR_INVALID_ARGUMENT;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return SD_ERR_INVALID_ARGUMENT;
+  st = check_kv(dims, kv_off, kv_len);
+  if (st != SD_OK) return st;
+  const AttnShape s = attn_shape(dims, scale, kv_len);
+  const size_t need = std::max(tree_ws(dims) + attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
+                               logits_ws(dims) + accept_stage_ws(dims));
+  if (workspace_bytes < need) return SD_ERR_WORKSPACE;
+
+  hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  if (kernel_events != nullptr)
+    for (int i = 0; i < 6; ++i) ev[i] = static_cast<hipEvent_t>(kernel_events[i]);
+  hipStream_t stm = static_cast<hipStream_t>(stream);
+  uint64_t* masks = static_cast<uint64_t*>(workspace);
+  if (launch_tree_masks(dims->batch, dims->gamma, parent, masks, stm) != hipSuccess) return SD_ERR_HIP;
+  st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out,
+                     static_cast<char*>(workspace) + tree_ws(dims), stm, ev[0], ev[1], masks);
+  if (st != SD_OK) return st;
+  st = run_logits(dims, hidden != nullptr ? hidden : attn_out, w_vocab, logits, row_lse, workspace, stm, ev[2],
+                  ev[3]);
+  if (st != SD_OK) return st;
+  return run_accept_tree(dims, logits, row_lse, tokens, parent, u, kv_len, accept_len, out_tok, out_node,
+                         new_kv_len, static_cast<char*>(workspace) + logits_ws(dims), stm, ev[4], ev[5]);
 }
 
 size_t sd_vocab_packed_bytes(const sd_dims_t* dims) {

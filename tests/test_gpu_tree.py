@@ -79,3 +79,105 @@ def test_chain_tree_equals_chain_attention(name):
     sd.sd_verify_attention_tree(db.dims, db.q, db.k, db.v, x.kv_off, x.kv_len, tensor(parent), db.scale, db.attn,
                                 db.ws)
     assert np.array_equal(chain, to_np(db.attn))
+
+
+# ---- acceptance -----------------------------------------------------------------
+
+from oracle import accept_tree, tree_near_threshold  # noqa: E402
+
+
+def _tree_inputs(rng, B, N, V):
+    G = N + 1
+    parent = random_parents(rng, B, N)
+    logits = (rng.standard_normal((B * G, V)) * 2.0).astype(np.float32)
+    l64 = logits.astype(np.float64)
+    mx = l64.max(axis=1, keepdims=True)
+    lse = (mx[:, 0] + np.log(np.exp(l64 - mx).sum(axis=1))).astype(np.float32)
+    tokens = np.empty((B, N), dtype=np.int32)
+    for b in range(B):
+        for i in range(N):
+            row = logits[b * G + parent[b, i] + 1]
+            r = rng.random()
+            if r < 0.5:
+                tokens[b, i] = int(np.argsort(-row)[rng.integers(0, min(3, V))])   # among the top 3
+            elif r < 0.97:
+                tokens[b, i] = int(rng.integers(0, V))
+            else:
+                tokens[b, i] = V + 3 if rng.random() < 0.5 else -1            # never passes
+    u = ((rng.integers(0, 1 << 32, size=(B, G), dtype=np.uint64) >> np.uint64(8)).astype(np.float64)
+         * 2.0 ** -24).astype(np.float32)
+    kv_len = rng.integers(G, 5000, size=B).astype(np.int32)
+    return logits, lse, tokens, parent, u, kv_len
+
+
+def _run_tree_accept(logits, lse, tokens, parent, u, kv_len, probs_mode):
+    B, N = tokens.shape
+    G = N + 1
+    V = logits.shape[1]
+    cfg = get_config("tiny").replace(batch=B, gamma=N, vocab=V, n_q_heads=1, n_kv_heads=1)
+    dims = sd.Dims.of(cfg)
+    if probs_mode:
+        x = np.exp(logits.astype(np.float64) - lse.astype(np.float64)[:, None]).astype(np.float32)
+        dx, dl = tensor(x), None
+    else:
+        x, dx, dl = logits, tensor(logits), tensor(lse)
+    acc = torch.empty((B,), dtype=torch.int32, device="cuda")
+    tok = torch.empty((B, G), dtype=torch.int32, device="cuda")
+    node = torch.empty((B, G), dtype=torch.int32, device="cuda")
+    new = torch.empty((B,), dtype=torch.int32, device="cuda")
+    ws = torch.empty((sd.sd_workspace_bytes(dims, int(kv_len.max())),), dtype=torch.uint8, device="cuda")
+    sd.sd_accept_tree(dims, dx, dl, tensor(tokens), tensor(parent), tensor(u), kv_len, acc, tok, node, new, ws)
+    ref = accept_tree(x, None if probs_mode else lse, tokens, parent, u, kv_len=kv_len)
+    return [to_np(t) for t in (acc, tok, node, new)], ref
+
+
+def _assert_tree_parity(got, ref):
+    acc, tok, node, new = got
+    near = np.array([tree_near_threshold(t) for t in ref["traces"]])
+    keep = ~near
+    assert np.array_equal(acc[keep], ref["accept_len"][keep]), (acc, ref["accept_len"])
+    assert np.array_equal(tok[keep], ref["out_tok"][keep])
+    assert np.array_equal(node[keep], ref["out_node"][keep])
+    assert np.array_equal(new[keep], ref["new_kv_len"][keep])
+    return int(near.sum())
+
+
+ACCEPT_CASES = [
+    ("n6_v1000", 40, 6, 1000),
+    ("n15_v32000", 16, 15, 32000),
+    ("n63_v3000", 4, 63, 3000),
+    ("many_requests", 70, 4, 300),
+    ("n10_v128256", 6, 10, 128256),
+    ("single_token_vocab", 5, 3, 1),
+]
+
+
+@pytest.mark.parametrize("name,B,N,V", ACCEPT_CASES)
+@pytest.mark.parametrize("probs_mode", [False, True])
+def test_tree_accept_matches_oracle(name, B, N, V, probs_mode):
+    announce(f"tree accept case={name} B={B} N={N} V={V} probs_mode={probs_mode}")
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    got, ref = _run_tree_accept(*_tree_inputs(rng, B, N, V), probs_mode)
+    near = _assert_tree_parity(got, ref)
+    announce(f"tree accept case={name}: near-threshold {near}, mean depth {got[0].mean():.2f}")
+
+
+def test_tree_step_matches_oracle():
+    cfg = get_config("llama3_8b").replace(batch=3, gamma=9, n_q_heads=8, n_kv_heads=2, hidden=1024, vocab=4099,
+                                          lengths=("explicit", (10, 700, 1500)))
+    announce(f"tree step case=gqa_small B={cfg.batch} nodes={cfg.gamma} V={cfg.vocab}")
+    x = make_inputs(cfg)
+    rng = np.random.default_rng(11)
+    parent = random_parents(rng, cfg.batch, cfg.gamma)
+    tokens = rng.integers(0, cfg.vocab, size=(cfg.batch, cfg.gamma)).astype(np.int32)
+    db = DeviceBatch(x)
+    node = torch.empty_like(db.out_tok)
+    sd.sd_verify_step_tree(db.dims, db.q, db.k, db.v, x.kv_off, x.kv_len, tensor(parent), db.scale, db.hidden, db.w,
+                           tensor(tokens), db.u, db.attn, db.logits, db.lse, db.accept_len, db.out_tok, node,
+                           db.new_kv_len, db.ws)
+    torch.cuda.synchronize()
+    ref_attn = tree_attention(x.f32("q"), x.f32("k_pool"), x.f32("v_pool"), x.kv_off, x.kv_len, cfg.n_kv_heads, parent)
+    assert_close_rows(to_np(db.attn), ref_attn, RTOL[cfg.dtype], "tree step attention")
+    ref = accept_tree(to_np(db.logits), to_np(db.lse), tokens, parent, x.u, kv_len=x.kv_len)
+    near = _assert_tree_parity([to_np(db.accept_len), to_np(db.out_tok), to_np(node), to_np(db.new_kv_len)], ref)
+    announce(f"tree step: near-threshold {near}")
