@@ -104,6 +104,9 @@ def main() -> int:
     ap.add_argument("--sampling", default=None, metavar="T,K,P",
                     help="time sd_verify_step_sampled with temperature T, top-k K (0: off), top-p P (1: off) "
                          "instead of the plain step (T = 0: greedy)")
+    ap.add_argument("--tree-nodes", type=int, default=0, metavar="N",
+                    help="time sd_verify_step_tree on a binary candidate tree of N nodes (two children per node, "
+                         "breadth first) instead of the chain; the workload's draft length becomes N")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -123,6 +126,11 @@ def main() -> int:
         return 2
     torch.cuda.set_device(0)
     cfg = get_config(args.workload)
+    if args.tree_nodes:
+        if args.sampling is not None:
+            print("--tree-nodes and --sampling are separate modes", file=sys.stderr)
+            return 2
+        cfg = cfg.replace(gamma=args.tree_nodes)
     B, G, M, V, K = cfg.batch, cfg.positions, cfg.rows, cfg.vocab, cfg.hidden
     log(f"generating workload {cfg.name}")
     x = make_inputs(cfg)
@@ -154,18 +162,27 @@ def main() -> int:
         t["lse"] = torch.empty((M,), dtype=torch.float32, device="cuda")
         t["acc"] = torch.full((B,), -7, dtype=torch.int32, device="cuda")
         t["tok"] = torch.empty((B, G), dtype=torch.int32, device="cuda")
+        t["node"] = torch.empty((B, G), dtype=torch.int32, device="cuda")
         t["new"] = torch.empty((B,), dtype=torch.int32, device="cuda")
         t["rmin"] = torch.empty((M,), dtype=torch.float32, device="cuda")
         t["ws"] = torch.empty((ws_bytes,), dtype=torch.uint8, device="cuda")
         copies.append(t)
     log(f"{ncopies} input copies of {big_bytes / 1e6:.0f} MB each")
 
+    # Binary candidate tree: nodes 0 and 1 hang from the root, node i >= 2 from node (i - 2) // 2.
+    parent = torch.tensor([[-1 if i < 2 else (i - 2) // 2 for i in range(cfg.gamma)]] * B, dtype=torch.int32,
+                          device="cuda")
     sampling = None
     if args.sampling is not None:
         s_t, s_k, s_p = args.sampling.split(",")
         sampling = sd.Sampling(float(s_t), int(s_k), float(s_p))
 
     def prepared(t, events=None):
+        if args.tree_nodes:
+            return sd.prepare_verify_step_tree(dims, t["q"], t["k_pool"], t["v_pool"], x.kv_off, x.kv_len, parent,
+                                               scale, t["hidden"], t["w"], t["draft"], t["u"], t["attn"],
+                                               t["logits"], t["lse"], t["acc"], t["tok"], t["node"], t["new"],
+                                               t["ws"], kernel_events=events)
         if sampling is not None:
             return sd.prepare_verify_step_sampled(dims, sampling, t["q"], t["k_pool"], t["v_pool"], x.kv_off,
                                                   x.kv_len, scale, t["hidden"], t["w"], t["q_draft"], t["draft"],
@@ -272,6 +289,7 @@ def main() -> int:
             "input_copies": ncopies, "vocab_layout": "packed" if packed else "row-major",
             **({"sampling": {"temperature": sampling.temperature, "top_k": sampling.top_k, "top_p": sampling.top_p}}
                if sampling is not None else {}),
+            **({"tree": {"nodes": args.tree_nodes, "shape": "binary"}} if args.tree_nodes else {}),
         },
         "roofline": roof,
         "scored_tokens_per_s": B * G / (ms_step * 1e-3),
@@ -286,7 +304,7 @@ def main() -> int:
         "vocab_attainable_frac": vocab_tflops / min(BF16_MFMA_PEAK_TFLOPS, vocab_flops / vocab_bytes * HBM_PEAK_GBPS / 1e3),
         "wall_ms_per_step": wall * 1e3 / args.steps,
     }
-    if not args.no_cpu_baseline and sampling is None:  # the CPU leg times the plain step
+    if not args.no_cpu_baseline and sampling is None and not args.tree_nodes:  # the CPU leg times the plain step
         log("timing the CPU oracle on the same batch")
         result["cpu_baseline"] = cpu_baseline(x, args.cpu_seconds)
     print(json.dumps(result), flush=True)

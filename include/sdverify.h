@@ -325,6 +325,19 @@ SD_API int sd_verify_step_tree(const sd_dims_t* dims, const void* q, const void*
                                int32_t* out_node, int32_t* new_kv_len, void* workspace, size_t workspace_bytes,
                                sd_stream_t stream, void* const* kernel_events);
 
+/*
+ * After a tree verification step: in every request's cache, move the K and V
+ * rows of the accepted nodes (out_node[b][0..accept_len[b]) from
+ * sd_accept_tree) into consecutive positions right after the root, in place,
+ * so that the first new_kv_len[b] = kv_len[b] - N + accept_len[b] entries are
+ * the verified sequence.  k_pool, v_pool, kv_off, kv_len as in
+ * sd_verify_attention_tree; out_node [B][N+1], accept_len [B] (device).
+ * Accept lengths or node numbers out of range end that request's move early.
+ */
+SD_API int sd_tree_commit_kv(const sd_dims_t* dims, void* k_pool, void* v_pool, const int64_t* kv_off,
+                             const int32_t* kv_len, const int32_t* out_node, const int32_t* accept_len,
+                             sd_stream_t stream);
+
 /* Static description of a status code. */
 SD_API const char* sd_status_string(int status);
 

@@ -40,7 +40,8 @@ from .attention import verify_attention
 from .logits import verify_logits, probabilities
 from .accept import accept_request, accept_resample, accept_resample_sampled, near_threshold
 from .warp import order_keys, warp_row, warped_from_cut
-from .tree import accept_tree, accept_tree_request, ancestor_masks, tree_attention, tree_near_threshold
+from .tree import (accept_tree, accept_tree_request, ancestor_masks, tree_attention, tree_commit_kv,
+                   tree_near_threshold)
 from .step import verify_step
 
 __all__ = [
@@ -58,6 +59,7 @@ __all__ = [
     "accept_tree_request",
     "ancestor_masks",
     "tree_attention",
+    "tree_commit_kv",
     "tree_near_threshold",
     "verify_step",
 ]

@@ -199,3 +199,27 @@ def tree_near_threshold(trace, band: float = 1e-6) -> bool:
             return True
     z = trace["z"]
     return (trace["threshold"] - trace["c_before"]) < band * z or (trace["c_at"] - trace["threshold"]) < band * z
+
+
+def tree_commit_kv(k_pool, v_pool, kv_off, kv_len, n_kv_heads, head_dim, out_node, accept_len, N):
+    """Copies of the pools after moving each request's accepted nodes next to
+    the root: for every KV head, tail position j + 1 receives the row of tail
+    position out_node[b][j] + 1, for j < accept_len[b], in increasing j (the
+    tail is the last N + 1 rows of the request's cache).  Rows are moved as
+    raw values; nothing else changes."""
+    k = np.array(k_pool, copy=True)
+    v = np.array(v_pool, copy=True)
+    G = N + 1
+    D = head_dim
+    for b in range(len(kv_len)):
+        L = int(kv_len[b])
+        off = int(kv_off[b])
+        tail0 = L - G
+        for g in range(n_kv_heads):
+            base = off + g * L * D
+            for j in range(int(accept_len[b])):
+                src = base + (tail0 + int(out_node[b][j]) + 1) * D
+                dst = base + (tail0 + j + 1) * D
+                k[dst:dst + D] = k[src:src + D]
+                v[dst:dst + D] = v[src:src + D]
+    return k, v

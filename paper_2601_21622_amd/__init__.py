@@ -32,6 +32,7 @@ from ._binding import (  # noqa: F401
     sd_accept_tree,
     sd_pack_vocab,
     sd_status_string,
+    sd_tree_commit_kv,
     sd_verify_attention,
     sd_verify_attention_tree,
     sd_verify_logits,

@@ -99,6 +99,8 @@ def library() -> ctypes.CDLL:
     lib.sd_accept_tree.restype = ctypes.c_int
     lib.sd_verify_step_tree.argtypes = [DP, P, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
     lib.sd_verify_step_tree.restype = ctypes.c_int
+    lib.sd_tree_commit_kv.argtypes = [DP, P, P, P, P, P, P, P]
+    lib.sd_tree_commit_kv.restype = ctypes.c_int
     SP = ctypes.POINTER(Sampling)
     lib.sd_accept_resample_sampled.argtypes = [DP, SP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.sd_accept_resample_sampled.restype = ctypes.c_int
@@ -240,6 +242,14 @@ def sd_accept_tree(dims: Dims, logits_or_probs, row_lse, tokens, parent, u, kv_l
                                   _ptr(parent), _ptr(u), len_p, _ptr(accept_len), _ptr(out_tok), _ptr(out_node),
                                   _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace), _stream(stream))
     _check(st, "sd_accept_tree")
+
+
+def sd_tree_commit_kv(dims: Dims, k_pool, v_pool, kv_off, kv_len, out_node, accept_len, stream=None) -> None:
+    _off, off_p = _host(kv_off, np.int64)
+    _len, len_p = _host(kv_len, np.int32)
+    st = library().sd_tree_commit_kv(ctypes.byref(dims), _ptr(k_pool), _ptr(v_pool), off_p, len_p, _ptr(out_node),
+                                     _ptr(accept_len), _stream(stream))
+    _check(st, "sd_tree_commit_kv")
 
 
 def _event_handles(events):

@@ -473,6 +473,32 @@ int sd_verify_step_tree(const sd_dims_t* dims, const void* q, const void* k_pool
                          new_kv_len, static_cast<char*>(workspace) + logits_ws(dims), stm, ev[4], ev[5]);
 }
 
+int sd_tree_commit_kv(const sd_dims_t* dims, void* k_pool, void* v_pool, const int64_t* kv_off,
+                      const int32_t* kv_len, const int32_t* out_node, const int32_t* accept_len, sd_stream_t stream) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!k_pool || !v_pool || !out_node || !accept_len) return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(k_pool, 16) || !aligned(v_pool, 16) || !aligned(out_node, 4) || !aligned(accept_len, 4))
+    return SD_ERR_INVALID_ARGUMENT;
+  st = check_kv(dims, kv_off, kv_len);
+  if (st != SD_OK) return st;
+  const int G = dims->gamma + 1;
+  for (int r0 = 0; r0 < dims->batch; r0 += kMaxReqPerLaunch) {
+    CommitBatch cb;
+    memset(&cb, 0, sizeof(cb));
+    cb.nreq = std::min(kMaxReqPerLaunch, dims->batch - r0);
+    cb.req0 = r0;
+    for (int i = 0; i < cb.nreq; ++i) {
+      cb.kv_len[i] = kv_len[r0 + i];
+      cb.kv_off[i] = kv_off[r0 + i];
+    }
+    if (launch_tree_commit(cb, dims->n_kv_heads, G, dims->head_dim, static_cast<int>(elem_size(dims->dtype)),
+                           out_node, accept_len, k_pool, v_pool, static_cast<hipStream_t>(stream)) != hipSuccess)
+      return SD_ERR_HIP;
+  }
+  return SD_OK;
+}
+
 size_t sd_vocab_packed_bytes(const sd_dims_t* dims) {
   if (check_dims(dims) != SD_OK || dims->dtype != SD_DTYPE_BF16) return 0;
   return vocab_packed_bytes(dims->hidden, dims->vocab);

@@ -609,6 +609,41 @@ hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchu
   }
 }
 
+// Tree commit: move the K and V rows of request b's accepted nodes (tail
+// positions out_node[j] + 1, increasing in j) to positions j + 1 after the
+// root, in place.  Every thread moves one 16-byte piece of one (KV head, row)
+// for all j in increasing order; since out_node[j] + 1 >= j + 1 and the
+// sources increase with j, no source is overwritten before it is read.
+// Accept lengths and node numbers outside their ranges end the move (every
+// access stays inside the request's cache).  Grid (requests, Hkv).
+__global__ __launch_bounds__(kAttnThreads)
+void tree_commit_kernel(CommitBatch cb, int G, int D, int esz, const int32_t* __restrict__ out_node,
+                        const int32_t* __restrict__ accept_len, unsigned char* __restrict__ kp,
+                        unsigned char* __restrict__ vp) {
+  const int b = blockIdx.x;
+  const int req = cb.req0 + b;
+  const int g = blockIdx.y;
+  const int L = cb.kv_len[b];
+  const int l = min(max(accept_len[req], 0), G - 1);
+  const int row_bytes = D * esz;
+  const int pieces = row_bytes / 16;
+  const int64_t head0 = (cb.kv_off[b] + (int64_t)g * L * D) * esz;  // byte offset of the head's row 0
+  const int tail0 = L - G;
+  for (int t = threadIdx.x; t < 2 * pieces; t += blockDim.x) {
+    unsigned char* base = (t < pieces ? kp : vp) + head0 + (t % pieces) * 16;
+    for (int j = 0; j < l; ++j) {
+      const int n = out_node[(int64_t)req * G + j];
+      if (n < j || n >= G - 1) break;
+      const int src = tail0 + n + 1;
+      const int dst = tail0 + j + 1;
+      if (src != dst) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(base + (int64_t)src * row_bytes);
+        *reinterpret_cast<u32x4*>(base + (int64_t)dst * row_bytes) = v;
+      }
+    }
+  }
+}
+
 // One workgroup per request, one thread per position: walk up the parents
 // (each step moves to a strictly smaller position, so at most g steps).
 __global__ __launch_bounds__(kWave)
@@ -698,6 +733,14 @@ hipError_t launch_attention_combine(int dtype, const AttnShape& s, const AttnBat
 hipError_t launch_tree_masks(int B, int N, const int32_t* parent, uint64_t* masks, hipStream_t stream) {
   if (B <= 0) return hipSuccess;
   hipLaunchKernelGGL(tree_masks_kernel, dim3(B), dim3(kWave), 0, stream, N, parent, masks);
+  return hipGetLastError();
+}
+
+hipError_t launch_tree_commit(const CommitBatch& cb, int Hkv, int G, int D, int esz, const int32_t* out_node,
+                              const int32_t* accept_len, void* k_pool, void* v_pool, hipStream_t stream) {
+  if (cb.nreq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(tree_commit_kernel, dim3(cb.nreq, Hkv), dim3(kAttnThreads), 0, stream, cb, G, D, esz, out_node,
+                     accept_len, static_cast<unsigned char*>(k_pool), static_cast<unsigned char*>(v_pool));
   return hipGetLastError();
 }
 

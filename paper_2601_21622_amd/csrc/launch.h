@@ -24,6 +24,15 @@ struct AttnBatch {
 // Tree verification: ancestor masks [B][N + 1] from parents [B][N] (node i's
 // parent in [-1, i), -1 the root; anything else is taken as the root).
 hipError_t launch_tree_masks(int B, int N, const int32_t* parent, uint64_t* masks, hipStream_t stream);
+// Tree commit: in each request's cache move the accepted nodes' K/V rows next
+// to the root.
+struct CommitBatch {
+  int32_t nreq, req0;
+  int32_t kv_len[kMaxReqPerLaunch];
+  int64_t kv_off[kMaxReqPerLaunch];
+};
+hipError_t launch_tree_commit(const CommitBatch& cb, int Hkv, int G, int D, int esz, const int32_t* out_node,
+                              const int32_t* accept_len, void* k_pool, void* v_pool, hipStream_t stream);
 
 struct AttnShape {
   int G;            // query positions per request

@@ -27,7 +27,7 @@ def test_library_loads_and_exports_header_symbols():
     assert set(names) == {"sd_workspace_bytes", "sd_verify_attention", "sd_verify_logits", "sd_accept_resample",
                           "sd_verify_step", "sd_status_string", "sd_version", "sd_vocab_packed_bytes",
                           "sd_pack_vocab", "sd_accept_resample_sampled", "sd_verify_step_sampled",
-                          "sd_verify_attention_tree", "sd_accept_tree", "sd_verify_step_tree"}
+                          "sd_verify_attention_tree", "sd_accept_tree", "sd_verify_step_tree", "sd_tree_commit_kv"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2

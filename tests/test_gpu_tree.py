@@ -181,3 +181,23 @@ def test_tree_step_matches_oracle():
     ref = accept_tree(to_np(db.logits), to_np(db.lse), tokens, parent, x.u, kv_len=x.kv_len)
     near = _assert_tree_parity([to_np(db.accept_len), to_np(db.out_tok), to_np(node), to_np(db.new_kv_len)], ref)
     announce(f"tree step: near-threshold {near}")
+
+
+def test_tree_commit_moves_accepted_rows():
+    from oracle import tree_commit_kv
+    cfg = get_config("llama3_8b").replace(batch=5, gamma=12, n_q_heads=8, n_kv_heads=2, hidden=1024, vocab=500,
+                                          lengths=("explicit", (13, 40, 300, 77, 2000)))
+    x = make_inputs(cfg)
+    rng = np.random.default_rng(21)
+    B, N = cfg.batch, cfg.gamma
+    logits, lse, tokens, parent, u, _ = _tree_inputs(rng, B, N, cfg.vocab)
+    ref = accept_tree(logits, lse, tokens, parent, u)
+    db = DeviceBatch(x)
+    sd.sd_tree_commit_kv(db.dims, db.k, db.v, x.kv_off, x.kv_len, tensor(ref["out_node"]), tensor(ref["accept_len"]))
+    torch.cuda.synchronize()
+    want_k, want_v = tree_commit_kv(x.k_pool, x.v_pool, x.kv_off, x.kv_len, cfg.n_kv_heads, cfg.head_dim,
+                                    ref["out_node"], ref["accept_len"], N)
+    got_k = db.k.view(torch.int16).cpu().numpy().view(np.uint16)
+    got_v = db.v.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got_k, want_k) and np.array_equal(got_v, want_v)
+    announce(f"tree commit: accept lengths {ref['accept_len'].tolist()}")

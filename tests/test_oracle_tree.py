@@ -275,3 +275,21 @@ def test_pin_rejects_planted_mistake(name):
     want = _target_joint(target)
     err = max(abs(joint.get(s, 0.0) - want[s]) for s in want)
     assert err > 1e-6, f"pin did not catch {name}"
+
+
+def test_commit_keeps_a_chain_in_place_and_compacts_a_path():
+    from oracle.tree import tree_commit_kv
+    D, Hkv, N = 4, 2, 5
+    L = 9
+    k = np.arange(Hkv * L * D, dtype=np.float32)
+    v = -k
+    same_k, same_v = tree_commit_kv(k, v, [0], [L], Hkv, D, [[0, 1, 2, -1, -1, -1]], [3], N)
+    assert np.array_equal(same_k, k) and np.array_equal(same_v, v)     # a chain prefix is already in place
+    got_k, _ = tree_commit_kv(k, v, [0], [L], Hkv, D, [[1, 3, -1, -1, -1, -1]], [2], N)
+    tail0 = L - (N + 1)
+    for g in range(Hkv):
+        rows = got_k[g * L * D:(g + 1) * L * D].reshape(L, D)
+        orig = k[g * L * D:(g + 1) * L * D].reshape(L, D)
+        assert np.array_equal(rows[tail0 + 1], orig[tail0 + 2])        # node 1
+        assert np.array_equal(rows[tail0 + 2], orig[tail0 + 4])        # node 3
+        assert np.array_equal(rows[:tail0 + 1], orig[:tail0 + 1])      # prefix and root untouched
