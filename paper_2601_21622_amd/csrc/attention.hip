@@ -88,9 +88,11 @@ constexpr int kLazyMaxBlocks = 2;
 
 __device__ __forceinline__ float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int DB, bool LAZY>
+// TREE = false promises chain rows, whose test is one comparison with the
+// row's last visible key lim (-1: nothing visible); pend and anc are then unused.
+template <int DB, bool LAZY, bool TREE>
 __device__ __forceinline__ bf16x8 softmax_tile(const f32x4 (&sc)[2], float scale_log2, bool masked, int k0, int pend,
-                                               uint64_t anc, float& m, float& lsum, f32x4 (&o)[DB]) {
+                                               uint64_t anc, int lim, float& m, float& lsum, f32x4 (&o)[DB]) {
   const int lg = (threadIdx.x & 63) >> 4;
   float raw[8];
 #pragma unroll
@@ -102,7 +104,8 @@ __device__ __forceinline__ bf16x8 softmax_tile(const f32x4 (&sc)[2], float scale
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (!key_visible(k0 + kb * 16 + lg * 4 + e, pend, anc)) raw[kb * 4 + e] = -INFINITY;
+        if (TREE ? !key_visible(k0 + kb * 16 + lg * 4 + e, pend, anc) : k0 + kb * 16 + lg * 4 + e > lim)
+          raw[kb * 4 + e] = -INFINITY;
   }
   float mx = fmaxf(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])),
                    fmaxf(fmaxf(raw[4], raw[5]), fmaxf(raw[6], raw[7])));
@@ -170,6 +173,7 @@ struct AttnRows {
   bf16x8 qf[RB][D / 32];  // Q fragments, B operand of S^T = K Q^T
   int pend[RB];           // last visible prefix key of the lane's row (-1: padding row)
   uint64_t anc[RB];       // visible tail positions of the lane's row
+  int lim[RB];            // chain rows: last visible key (-1: padding row)
   float m[RB], lsum[RB];  // running maximum (log2 domain) and sum
   f32x4 o[RB][D / 16];    // running O^T blocks
 };
@@ -179,7 +183,7 @@ struct AttnRows {
 // `masked` says whether some key of the tile may lie past a row's causal
 // limit (only then are the limits applied); a tile with live == false
 // contributes nothing (all of its keys are masked).
-template <int RB, int D>
+template <int RB, int D, bool TREE>
 __device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2, int k0, bool masked,
                                           const unsigned char* __restrict__ ksrc,
                                           const unsigned char* __restrict__ vsrc, bool live = true) {
@@ -213,9 +217,9 @@ __device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2,
   bf16x8 pf[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
-    pf[rb] = softmax_tile<DB, (RB <= kLazyMaxBlocks)>(sc[rb], scale_log2, masked || !live, k0,
-                                                      live ? st.pend[rb] : -1, live ? st.anc[rb] : 0ull,
-                                                      st.m[rb], st.lsum[rb], st.o[rb]);
+    pf[rb] = softmax_tile<DB, (RB <= kLazyMaxBlocks), TREE>(sc[rb], scale_log2, masked || !live, k0,
+                                                            live ? st.pend[rb] : -1, live ? st.anc[rb] : 0ull,
+                                                            live ? st.lim[rb] : -1, st.m[rb], st.lsum[rb], st.o[rb]);
 
   // V^T fragments (A operand of O^T += V^T P^T): lane (lg, lr) needs
   // d = db*16 + lr and keys {lg*4 .. +3} then {16 + lg*4 .. +3}, the
@@ -238,7 +242,7 @@ __device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2,
 // then fold the current tile.  The stage pointers are restrict-qualified, so
 // the compiler knows the new DMAs cannot write what this step reads and
 // leaves the ordering to the explicit wait.
-template <int RB, int D>
+template <int RB, int D, bool TREE>
 __device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2, const uint16_t* Kb,
                                           const uint16_t* Vb, int L, int k0_next, bool next_dead, int k0,
                                           bool masked, unsigned char* __restrict__ kdst,
@@ -250,7 +254,7 @@ __device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2,
   KT::load(Kb, k0_next, L, kdst, lane, next_dead);
   VT::load(Vb, k0_next, L, vdst, lane, next_dead);
   wait_vmcnt<KT::kDmas + VT::kDmas>();
-  attn_fold<RB, D>(st, scale_log2, k0, masked, ksrc, vsrc);
+  attn_fold<RB, D, TREE>(st, scale_log2, k0, masked, ksrc, vsrc);
 }
 
 // Item of wave `wave` in workgroup blockIdx.x: (chunk, KV head), KV head
@@ -309,11 +313,13 @@ __device__ __forceinline__ void init_rows(AttnRows<RB, D>& st, const AttnShape& 
       for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = load_bf16x8(qrow + ds * 32 + lg * 8);
       st.pend[rb] = L - s.G - 1;
       st.anc[rb] = anc != nullptr ? anc[(int64_t)req * s.G + j] : chain_mask(j);
+      st.lim[rb] = L - s.G + j;
     } else {
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) st.qf[rb][ds] = bf16x8{};
       st.pend[rb] = -1;
       st.anc[rb] = 0ull;
+      st.lim[rb] = -1;
     }
     st.m[rb] = kNegBig;
     st.lsum[rb] = 0.f;
@@ -322,7 +328,7 @@ __device__ __forceinline__ void init_rows(AttnRows<RB, D>& st, const AttnShape& 
   }
 }
 
-template <int RB, int D>
+template <int RB, int D, bool TREE>
 __global__ __launch_bounds__(kAttnThreads, 1)
 void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
                       const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
@@ -369,7 +375,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   KT::load(Kb, key0(0), L, k0s, lane);
   VT::load(Vb, key0(0), L, v0s, lane);
   for (int i = 0; i < ntiles; ++i) {
-    attn_step<RB, D>(st, s.scale_log2, Kb, Vb, L, key0(i + 1), i + 1 >= ntiles, key0(i),
+    attn_step<RB, D, TREE>(st, s.scale_log2, Kb, Vb, L, key0(i + 1), i + 1 >= ntiles, key0(i),
                      key0(i) + kTile - 1 > L - s.G, k1s, v1s, k0s, v0s);
     unsigned char* t = k0s;
     k0s = k1s;
@@ -387,7 +393,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
 // registers, so the compiler's own vmcnt accounting covers the pipeline, and
 // two tiles of each wave are in flight while it folds.  With one 16-row block
 // (multi-head attention) two workgroups share a CU.
-template <int RB, int D>
+template <int RB, int D, bool TREE>
 __global__ __launch_bounds__(kAttnThreads, (RB == 1 ? 2 : 1))
 void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
                           const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
@@ -444,7 +450,7 @@ void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
       *reinterpret_cast<u32x4*>(kt + KT::at(r, d)) = kr[set][it];
       *reinterpret_cast<u32x4*>(vt + VT::at(r, d)) = vr[set][it];
     }
-    attn_fold<RB, D>(st, s.scale_log2, k0, k0 + kTile - 1 > L - s.G, kt, vt, live);
+    attn_fold<RB, D, TREE>(st, s.scale_log2, k0, k0 + kTile - 1 > L - s.G, kt, vt, live);
   };
 
   // Tile i+1 loads while tile i is folded in; the body always folds two
@@ -574,37 +580,37 @@ void attn_combine_kernel(const AttnShape s, const AttnBatch bt, AttnPartials par
   for (int e = 0; e < 4; ++e) store_out(dst + e, num[e] / den);
 }
 
-template <int RB, int D>
+template <int RB, int D, bool TREE>
 hipError_t launch_bf16(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                        const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   const int items = nchunks * s.Hkv;
-  hipExtLaunchKernelGGL((attn_bf16_kernel<RB, D>), dim3((items + kAttnWaves - 1) / kAttnWaves), dim3(kAttnThreads), 0,
+  hipExtLaunchKernelGGL((attn_bf16_kernel<RB, D, TREE>), dim3((items + kAttnWaves - 1) / kAttnWaves), dim3(kAttnThreads), 0,
                         stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                         static_cast<const uint16_t*>(v), parts);
   return hipGetLastError();
 }
 
-template <int RB, int D>
+template <int RB, int D, bool TREE>
 hipError_t launch_reg(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                       const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  hipExtLaunchKernelGGL((attn_bf16_reg_kernel<RB, D>), dim3((nchunks * s.Hkv + kAttnWaves - 1) / kAttnWaves),
+  hipExtLaunchKernelGGL((attn_bf16_reg_kernel<RB, D, TREE>), dim3((nchunks * s.Hkv + kAttnWaves - 1) / kAttnWaves),
                         dim3(kAttnThreads), 0, stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q),
                         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), parts);
   return hipGetLastError();
 }
 
-template <int D>
+template <int D, bool TREE>
 hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                        const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   switch (rb) {
-    case 1: return launch_reg<1, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 2: return launch_bf16<2, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 3: return launch_bf16<3, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 4: return launch_bf16<4, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 5: return launch_bf16<5, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 6: return launch_bf16<6, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 7: return launch_bf16<7, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 8: return launch_bf16<8, D>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 1: return launch_reg<1, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 2: return launch_bf16<2, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 3: return launch_bf16<3, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 4: return launch_bf16<4, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 5: return launch_bf16<5, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 6: return launch_bf16<6, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 7: return launch_bf16<7, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 8: return launch_bf16<8, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
@@ -712,8 +718,13 @@ hipError_t launch_attention(int dtype, const AttnShape& s, const AttnBatch& bt, 
     return hipGetLastError();
   }
   const int rb = (s.rows + 15) / 16;
-  if (s.D == 128) return dispatch_rb<128>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-  if (s.D == 64) return dispatch_rb<64>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+  const bool tree = bt.anc != nullptr;
+  if (s.D == 128)
+    return tree ? dispatch_rb<128, true>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1)
+                : dispatch_rb<128, false>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+  if (s.D == 64)
+    return tree ? dispatch_rb<64, true>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1)
+                : dispatch_rb<64, false>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
   return hipErrorInvalidValue;
 }
 
