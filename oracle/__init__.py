@@ -30,6 +30,11 @@ What it computes (StarSD, "One-for-Many Speculative Decoding"):
   place of the longest-path rule of Algorithm 2, which is not lossless).
   Attention by definition; acceptance step by step.
 * :mod:`oracle.step` -- the composition of the three for one pooled batch.
+* :mod:`oracle.model` -- the performance model of Sec. 3 and Sec. 4.2: the
+  acceptance rate beta (sum of min(p, q)), the expected accept length from
+  the distribution of the accept length, and the per-iteration time, idle
+  time, N_full and N_max from a discrete-event run of the draft server of
+  Algorithm 1.  By definition.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against closed forms,
 special cases, library routines of other packages and brute-force enumeration;
@@ -43,8 +48,18 @@ from .warp import order_keys, warp_row, warped_from_cut
 from .tree import (accept_tree, accept_tree_request, ancestor_masks, tree_attention, tree_commit_kv,
                    tree_near_threshold)
 from .step import verify_step
+from .model import (acceptance_rate, acceptance_rate_batch, accept_length_pmf, expected_accept_length, n_full, n_max,
+                    per_target_throughput, simulate_star)
 
 __all__ = [
+    "acceptance_rate",
+    "acceptance_rate_batch",
+    "accept_length_pmf",
+    "expected_accept_length",
+    "n_full",
+    "n_max",
+    "per_target_throughput",
+    "simulate_star",
     "verify_attention",
     "verify_logits",
     "probabilities",
