@@ -89,6 +89,44 @@ def cpu_baseline(x, budget_s: float):
     }
 
 
+def starsd_leg(sd, dims, cfg, copies, ms_step, args) -> dict:
+    """Acceptance rates of the step's own target and draft distributions
+    (sd_acceptance_rate, timed on its own), then the performance model with
+    t_v = the measured step time."""
+    import numpy as np
+    import torch
+    from paper_2601_21622_amd import starsd
+
+    parts = [float(v) for v in args.starsd.split(",")]
+    t_s, t_c = parts[0], parts[1]
+    rate = parts[2] if len(parts) > 2 else None
+    B, gamma, V = cfg.batch, cfg.gamma, cfg.vocab
+    betas = [torch.empty((B, gamma), dtype=torch.float64, device="cuda") for _ in copies]
+    for t, b in zip(copies, betas):
+        sd.sd_acceptance_rate(dims, t["logits"], t["lse"], t["q_draft"], b, t["ws"])
+    torch.cuda.synchronize()
+    n = max(20, min(args.steps, 200))
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record()
+    for i in range(n):
+        t = copies[i % len(copies)]
+        sd.sd_acceptance_rate(dims, t["logits"], t["lse"], t["q_draft"], betas[i % len(copies)], t["ws"])
+    s1.record()
+    torch.cuda.synchronize()
+    ms = s0.elapsed_time(s1) / n
+    beta = betas[0].cpu().numpy()
+    if not all(np.array_equal(beta, b.cpu().numpy()) for b in betas):
+        raise RuntimeError("input copies disagree on the acceptance rates")
+    nbytes = B * gamma * V * 8 + B * (gamma + 1) * 4    # p (logits) and q read once, lse
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    rep = starsd.star_report(beta.ravel().tolist(), gamma, t_s, t_c, ms_step, standalone_rate=rate)
+    log(f"acceptance rate: {ms * 1e3:.1f} us per call ({gbps:.0f} GB/s), mean beta {rep.beta:.4f}")
+    return {"rate_kernel": {"ms_per_call": ms, "bytes_per_call": nbytes, "hbm_gbps": gbps,
+                            "hbm_frac": gbps / HBM_PEAK_GBPS},
+            "beta_per_position": beta.mean(axis=0).tolist(),
+            "time_unit": "ms", "standalone_rate": rate, "model": rep.as_dict()}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -107,6 +145,10 @@ def main() -> int:
     ap.add_argument("--tree-nodes", type=int, default=0, metavar="N",
                     help="time sd_verify_step_tree on a binary candidate tree of N nodes (two children per node, "
                          "breadth first) instead of the chain; the workload's draft length becomes N")
+    ap.add_argument("--starsd", default=None, metavar="T_S,T_C[,RATE]",
+                    help="also time sd_acceptance_rate on the step's distributions and evaluate the StarSD model "
+                         "with the measured t_v: draft time per layer t_s and transfer time t_c in ms, and "
+                         "optionally a standalone target rate in tokens/ms (gives N_max)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -130,6 +172,9 @@ def main() -> int:
         if args.sampling is not None:
             print("--tree-nodes and --sampling are separate modes", file=sys.stderr)
             return 2
+    if args.starsd is not None and (args.tree_nodes or args.sampling is not None):
+        print("--starsd applies to the plain verification step", file=sys.stderr)
+        return 2
         cfg = cfg.replace(gamma=args.tree_nodes)
     B, G, M, V, K = cfg.batch, cfg.positions, cfg.rows, cfg.vocab, cfg.hidden
     log(f"generating workload {cfg.name}")
@@ -304,6 +349,8 @@ def main() -> int:
         "vocab_attainable_frac": vocab_tflops / min(BF16_MFMA_PEAK_TFLOPS, vocab_flops / vocab_bytes * HBM_PEAK_GBPS / 1e3),
         "wall_ms_per_step": wall * 1e3 / args.steps,
     }
+    if args.starsd is not None:
+        result["starsd"] = starsd_leg(sd, dims, cfg, copies, ms_step, args)
     if not args.no_cpu_baseline and sampling is None and not args.tree_nodes:  # the CPU leg times the plain step
         log("timing the CPU oracle on the same batch")
         result["cpu_baseline"] = cpu_baseline(x, args.cpu_seconds)

@@ -338,6 +338,28 @@ SD_API int sd_tree_commit_kv(const sd_dims_t* dims, void* k_pool, void* v_pool, 
                              const int32_t* kv_len, const int32_t* out_node, const int32_t* accept_len,
                              sd_stream_t stream);
 
+/*
+ * Acceptance rate of every draft position (Sec. 3, eq. beta_cond): the sum
+ * over the vocabulary of min(p(v), q(v)), i.e. one minus the total-variation
+ * distance of the target and draft distributions, which is the probability
+ * that the ratio test accepts a draft drawn from q.  Its mean over positions
+ * is the beta of the expected accept length beta (1 - beta^d) / (1 - beta)
+ * (eq. El_closed) that the performance model of Sec. 3 builds on.
+ *   logits_or_probs [B*G][V] float32 (device): logits if row_lse != NULL, else
+ *                   probabilities; row b*G + i is the target distribution p
+ *                   that tests draft position i (i < gamma)
+ *   row_lse         [B*G] float32 (device) or NULL: p(v) = exp(logit - lse),
+ *                   the difference kept exact, as in sd_accept_resample
+ *   q_draft         [B][gamma][V] float32 (device): the draft distributions
+ *   beta            [B][gamma] float64 (device) output
+ *   workspace       at least sd_workspace_bytes(dims, ...) bytes, 16-byte aligned
+ * min(p, q) is summed in float64 in an order fixed by the shapes, so repeated
+ * calls give identical results.  Two kernel launches on `stream`.
+ */
+SD_API int sd_acceptance_rate(const sd_dims_t* dims, const float* logits_or_probs, const float* row_lse,
+                              const float* q_draft, double* beta, void* workspace, size_t workspace_bytes,
+                              sd_stream_t stream);
+
 /* Static description of a status code. */
 SD_API const char* sd_status_string(int status);
 

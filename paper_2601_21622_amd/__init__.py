@@ -27,6 +27,7 @@ from ._binding import (  # noqa: F401
     prepare_verify_step,
     prepare_verify_step_sampled,
     prepare_verify_step_tree,
+    sd_acceptance_rate,
     sd_accept_resample,
     sd_accept_resample_sampled,
     sd_accept_tree,

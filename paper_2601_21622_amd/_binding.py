@@ -101,6 +101,8 @@ def library() -> ctypes.CDLL:
     lib.sd_verify_step_tree.restype = ctypes.c_int
     lib.sd_tree_commit_kv.argtypes = [DP, P, P, P, P, P, P, P]
     lib.sd_tree_commit_kv.restype = ctypes.c_int
+    lib.sd_acceptance_rate.argtypes = [DP, P, P, P, P, P, SZ, P]
+    lib.sd_acceptance_rate.restype = ctypes.c_int
     SP = ctypes.POINTER(Sampling)
     lib.sd_accept_resample_sampled.argtypes = [DP, SP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.sd_accept_resample_sampled.restype = ctypes.c_int
@@ -250,6 +252,12 @@ def sd_tree_commit_kv(dims: Dims, k_pool, v_pool, kv_off, kv_len, out_node, acce
     st = library().sd_tree_commit_kv(ctypes.byref(dims), _ptr(k_pool), _ptr(v_pool), off_p, len_p, _ptr(out_node),
                                      _ptr(accept_len), _stream(stream))
     _check(st, "sd_tree_commit_kv")
+
+
+def sd_acceptance_rate(dims: Dims, logits_or_probs, row_lse, q_draft, beta, workspace, stream=None) -> None:
+    st = library().sd_acceptance_rate(ctypes.byref(dims), _ptr(logits_or_probs), _ptr(row_lse), _ptr(q_draft),
+                                      _ptr(beta), _ptr(workspace), _nbytes(workspace), _stream(stream))
+    _check(st, "sd_acceptance_rate")
 
 
 def _event_handles(events):

@@ -29,15 +29,6 @@ namespace sdv {
 namespace {
 
 
-// exp(a - b), with a - b carried exactly as s + err.
-__device__ __forceinline__ float exp_diff(float a, float b) {
-  const float s = a - b;
-  const float bb = s - a;
-  const float err = (a - (s - bb)) + (-b - bb);
-  const float e = expf(s);
-  return fmaf(e, err, e);
-}
-
 struct AcceptArgs {
   int gamma, V, nseg, segs_per_group;
   const float* x;        // [M][V] logits (lse != nullptr or warp != nullptr) or probabilities

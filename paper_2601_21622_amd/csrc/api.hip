@@ -199,6 +199,8 @@ int check_sampling(const sd_sampling_t* sp) {
   return SD_OK;
 }
 
+size_t rate_ws(const sd_dims_t* d) { return align_up(rate_workspace_bytes(d->batch, d->gamma, d->vocab)); }
+
 int check_accept_args(const float* x, const float* row_lse, const float* q_draft, const int32_t* draft_tok,
                       const float* u, const int32_t* kv_len, const int32_t* accept_len, const int32_t* out_tok,
                       const int32_t* new_kv_len) {
@@ -217,7 +219,8 @@ extern "C" {
 size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
   if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
   const int64_t chunks = attn_max_chunks(dims->dtype, dims->n_kv_heads, dims->batch, max_kv_len);
-  return std::max(tree_ws(dims) + attention_ws(dims, chunks), logits_ws(dims) + accept_stage_ws(dims));
+  return std::max({tree_ws(dims) + attention_ws(dims, chunks), logits_ws(dims) + accept_stage_ws(dims),
+                   rate_ws(dims)});
 }
 
 int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
@@ -497,6 +500,20 @@ int sd_tree_commit_kv(const sd_dims_t* dims, void* k_pool, void* v_pool, const i
       return SD_ERR_HIP;
   }
   return SD_OK;
+}
+
+int sd_acceptance_rate(const sd_dims_t* dims, const float* logits_or_probs, const float* row_lse,
+                       const float* q_draft, double* beta, void* workspace, size_t workspace_bytes,
+                       sd_stream_t stream) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!logits_or_probs || !q_draft || !beta || !workspace) return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(logits_or_probs, 4) || (row_lse != nullptr && !aligned(row_lse, 4)) || !aligned(q_draft, 4) ||
+      !aligned(beta, 8) || !aligned(workspace, 16))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < rate_ws(dims)) return SD_ERR_WORKSPACE;
+  return hip_status(launch_rate(dims->gamma, dims->vocab, dims->batch, logits_or_probs, row_lse, q_draft, workspace,
+                                beta, static_cast<hipStream_t>(stream)));
 }
 
 size_t sd_vocab_packed_bytes(const sd_dims_t* dims) {

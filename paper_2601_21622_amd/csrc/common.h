@@ -119,6 +119,16 @@ __device__ __forceinline__ void lds_wait() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
+// exp(a - b), with a - b carried exactly as s + err (TwoSum), so that the
+// result is within a few float32 ulp of the exact exp(a - b).
+__device__ __forceinline__ float exp_diff(float a, float b) {
+  const float s = a - b;
+  const float bb = s - a;
+  const float err = (a - (s - bb)) + (-b - bb);
+  const float e = expf(s);
+  return fmaf(e, err, e);
+}
+
 // 32-bit key whose unsigned order is the order of the float32 values (-0
 // below +0): negative values bit-inverted, the others with the sign bit set.
 __device__ __forceinline__ uint32_t order_key(float f) {

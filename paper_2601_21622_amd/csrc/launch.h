@@ -137,4 +137,13 @@ hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& batch, con
                               int32_t* accept_len, int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len,
                               hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
+// Acceptance rate of every draft position: beta[b * gamma + i] = sum_v
+// min(p(v), q_draft[b][i][v]), p from row b * (gamma + 1) + i of x (logits
+// with row_lse, probabilities without), float64.  ws holds
+// rate_workspace_bytes(B, gamma, V).  ev_start/ev_stop (may be null) bracket
+// both launches.
+size_t rate_workspace_bytes(int B, int gamma, int V);
+hipError_t launch_rate(int gamma, int V, int B, const float* x, const float* row_lse, const float* q_draft, void* ws,
+                       double* beta, hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+
 }  // namespace sdv

@@ -27,7 +27,8 @@ def test_library_loads_and_exports_header_symbols():
     assert set(names) == {"sd_workspace_bytes", "sd_verify_attention", "sd_verify_logits", "sd_accept_resample",
                           "sd_verify_step", "sd_status_string", "sd_version", "sd_vocab_packed_bytes",
                           "sd_pack_vocab", "sd_accept_resample_sampled", "sd_verify_step_sampled",
-                          "sd_verify_attention_tree", "sd_accept_tree", "sd_verify_step_tree", "sd_tree_commit_kv"}
+                          "sd_verify_attention_tree", "sd_accept_tree", "sd_verify_step_tree", "sd_tree_commit_kv",
+                          "sd_acceptance_rate"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2
@@ -107,6 +108,23 @@ def test_logits_and_accept_reject_bad_arguments():
     short = (ctypes.c_int32 * 2)(2, 10)
     assert lib.sd_accept_resample(ctypes.byref(d), P, P, P, P, P, short, P, P, P, None, 0, None) == \
         sd.SD_ERR_INVALID_ARGUMENT
+
+
+@cpu_only
+def test_acceptance_rate_rejects_bad_arguments():
+    lib = sd.library()
+    d = dims()
+    call = lib.sd_acceptance_rate
+    assert call(ctypes.byref(d), None, P, P, P, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert call(ctypes.byref(d), P, P, None, P, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert call(ctypes.byref(d), P, P, P, None, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert call(ctypes.byref(d), P, P, P, P + 4, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT   # beta: 8-byte
+    assert call(ctypes.byref(d), P + 2, P, P, P, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert call(ctypes.byref(d), P, P, P, P, P + 8, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT   # ws: 16-byte
+    assert call(ctypes.byref(d), P, P, P, P, P, 8, None) == sd.SD_ERR_WORKSPACE
+    assert call(ctypes.byref(dims(gamma=0)), P, P, P, P, P, 1 << 30, None) == sd.SD_ERR_INVALID_ARGUMENT
+    # The step-sized workspace covers the rate's.
+    assert sd.sd_workspace_bytes(d, 1000) >= 8
 
 
 @cpu_only
