@@ -89,6 +89,38 @@ def cpu_baseline(x, budget_s: float):
     }
 
 
+def paged_caches(sd, cfg, x, k_pool, v_pool, P):
+    """The workload's caches moved into pools of P-key pages.  Page ids come
+    from the library's allocator (sd_kv_pool_*), every request (tag) growing
+    one page at a time in turn, as sessions that advance together do."""
+    import numpy as np
+    import torch
+
+    Hkv, D, B = cfg.n_kv_heads, cfg.head_dim, cfg.batch
+    need = [(int(L) + P - 1) // P for L in x.kv_len]
+    num_pages = sum(need)
+    pool = sd.KVPool(num_pages, P)
+    for j in range(max(need)):
+        for b in range(B):
+            if j < need[b]:
+                pool.reserve(b, min(int(x.kv_len[b]), (j + 1) * P))
+    table = pool.block_table(list(range(B)), max(need))
+    pool.close()
+    kp = torch.zeros((num_pages, Hkv, P, D), dtype=k_pool.dtype, device="cuda")
+    vp = torch.zeros_like(kp)
+    for b in range(B):
+        L, off = int(x.kv_len[b]), int(x.kv_off[b])
+        segk = k_pool[off:off + Hkv * L * D].view(Hkv, L, D)
+        segv = v_pool[off:off + Hkv * L * D].view(Hkv, L, D)
+        for j in range(need[b]):
+            k0, k1 = j * P, min(L, (j + 1) * P)
+            kp[int(table[b, j]), :, :k1 - k0] = segk[:, k0:k1]
+            vp[int(table[b, j]), :, :k1 - k0] = segv[:, k0:k1]
+    torch.cuda.synchronize()
+    log(f"paged caches: {num_pages} pages of {P} keys")
+    return kp, vp, torch.from_numpy(np.ascontiguousarray(table)).cuda(), num_pages
+
+
 def starsd_leg(sd, dims, cfg, copies, ms_step, args) -> dict:
     """Acceptance rates of the step's own target and draft distributions
     (sd_acceptance_rate, timed on its own), then the performance model with
@@ -145,6 +177,9 @@ def main() -> int:
     ap.add_argument("--tree-nodes", type=int, default=0, metavar="N",
                     help="time sd_verify_step_tree on a binary candidate tree of N nodes (two children per node, "
                          "breadth first) instead of the chain; the workload's draft length becomes N")
+    ap.add_argument("--paged", type=int, default=0, metavar="P",
+                    help="keep the KV caches in a paged pool of P-key pages (sd_verify_step_paged); pages come "
+                         "from the library's allocator with the requests growing in turn, so they interleave")
     ap.add_argument("--starsd", default=None, metavar="T_S,T_C[,RATE]",
                     help="also time sd_acceptance_rate on the step's distributions and evaluate the StarSD model "
                          "with the measured t_v: draft time per layer t_s and transfer time t_c in ms, and "
@@ -172,6 +207,9 @@ def main() -> int:
         if args.sampling is not None:
             print("--tree-nodes and --sampling are separate modes", file=sys.stderr)
             return 2
+    if args.paged and (args.tree_nodes or args.sampling is not None):
+        print("--paged applies to the plain verification step", file=sys.stderr)
+        return 2
     if args.starsd is not None and (args.tree_nodes or args.sampling is not None):
         print("--starsd applies to the plain verification step", file=sys.stderr)
         return 2
@@ -200,6 +238,11 @@ def main() -> int:
         sd.sd_pack_vocab(dims, base["w"], wp)
         torch.cuda.synchronize()
         base["w"] = wp
+    pages = None
+    if args.paged:
+        base["k_pool"], base["v_pool"], table, num_pages = paged_caches(sd, cfg, x, base["k_pool"], base["v_pool"],
+                                                                        args.paged)
+        pages = sd.KVPages.of(table, args.paged, num_pages)
     for i in range(ncopies):
         t = {n: (a if i == 0 else a.clone()) for n, a in base.items()}
         t["attn"] = torch.empty((B, G, cfg.n_q_heads, cfg.head_dim), dtype=adt, device="cuda")
@@ -233,6 +276,11 @@ def main() -> int:
                                                   x.kv_len, scale, t["hidden"], t["w"], t["q_draft"], t["draft"],
                                                   t["u"], t["attn"], t["logits"], t["lse"], t["rmin"], t["acc"],
                                                   t["tok"], t["new"], t["ws"], kernel_events=events)
+        if pages is not None:
+            return sd.prepare_verify_step_paged(dims, t["q"], t["k_pool"], t["v_pool"], pages, x.kv_len, scale,
+                                                t["hidden"], t["w"], t["q_draft"], t["draft"], t["u"], t["attn"],
+                                                t["logits"], t["lse"], t["acc"], t["tok"], t["new"], t["ws"],
+                                                kernel_events=events)
         return sd.prepare_verify_step(dims, t["q"], t["k_pool"], t["v_pool"], x.kv_off, x.kv_len, scale, t["hidden"],
                                       t["w"], t["q_draft"], t["draft"], t["u"], t["attn"], t["logits"], t["lse"],
                                       t["acc"], t["tok"], t["new"], t["ws"], kernel_events=events)
@@ -335,6 +383,7 @@ def main() -> int:
             **({"sampling": {"temperature": sampling.temperature, "top_k": sampling.top_k, "top_p": sampling.top_p}}
                if sampling is not None else {}),
             **({"tree": {"nodes": args.tree_nodes, "shape": "binary"}} if args.tree_nodes else {}),
+            **({"kv_cache": {"layout": "paged", "page_size": args.paged}} if args.paged else {}),
         },
         "roofline": roof,
         "scored_tokens_per_s": B * G / (ms_step * 1e-3),
@@ -351,7 +400,8 @@ def main() -> int:
     }
     if args.starsd is not None:
         result["starsd"] = starsd_leg(sd, dims, cfg, copies, ms_step, args)
-    if not args.no_cpu_baseline and sampling is None and not args.tree_nodes:  # the CPU leg times the plain step
+    if not args.no_cpu_baseline and sampling is None and not args.tree_nodes and not args.paged:
+        # the CPU leg times the plain step
         log("timing the CPU oracle on the same batch")
         result["cpu_baseline"] = cpu_baseline(x, args.cpu_seconds)
     print(json.dumps(result), flush=True)

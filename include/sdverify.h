@@ -65,7 +65,8 @@ enum {
   SD_ERR_INVALID_ARGUMENT = -1, /* null/misaligned pointer, bad size, inconsistent shape */
   SD_ERR_UNSUPPORTED = -2,      /* valid but outside what the kernels implement */
   SD_ERR_WORKSPACE = -3,        /* workspace smaller than sd_workspace_bytes requires */
-  SD_ERR_HIP = -4               /* a HIP launch or runtime call failed */
+  SD_ERR_HIP = -4,              /* a HIP launch or runtime call failed */
+  SD_ERR_CAPACITY = -5          /* a KV page pool has too few free pages */
 };
 
 /* Flags of sd_dims_t.flags. */
@@ -359,6 +360,74 @@ SD_API int sd_tree_commit_kv(const sd_dims_t* dims, void* k_pool, void* v_pool, 
 SD_API int sd_acceptance_rate(const sd_dims_t* dims, const float* logits_or_probs, const float* row_lse,
                               const float* q_draft, double* beta, void* workspace, size_t workspace_bytes,
                               sd_stream_t stream);
+
+/*
+ * Paged KV caches: per-session (per-tag) state in one shared pool
+ * (Algorithm 1: each target's KV cache is isolated and indexed by its tag;
+ * the session's cache is created with the session, grows by the gamma + 1
+ * positions of every step, is cut back to the accepted prefix after it, and
+ * is released at the end).  K and V each live in a pool of num_pages pages of
+ * page_size keys, laid out [num_pages][n_kv_heads][page_size][head_dim]
+ * (bf16).  Request b's key k is row k % page_size of page
+ * block_table[b][k / page_size].  page_size is a power of two in [64, 4096],
+ * so a 32-key attention tile never crosses a page.
+ */
+typedef struct {
+  const int32_t* block_table; /* device [B][max_pages] int32 page ids; an id outside
+                                 [0, num_pages) is clamped into it (never read out of bounds) */
+  int32_t max_pages;          /* entries per request in block_table; kv_len[b] <= max_pages * page_size */
+  int32_t page_size;          /* keys per page: a power of two in [64, 4096] */
+  int32_t num_pages;          /* pages in each of the K and V pools */
+} sd_kv_pages_t;
+
+/*
+ * sd_verify_attention over a paged cache: identical results to the segment
+ * layout holding the same rows (same kernels; only the row addresses differ,
+ * and the split of each request's keys into chunks is rounded to whole
+ * pages).  k_pages, v_pages: the pools (16-byte aligned).  kv_len (host) as
+ * for sd_verify_attention; the last G keys of request b are this step's
+ * positions.  bf16 only (SD_ERR_UNSUPPORTED for fp32).
+ */
+SD_API int sd_verify_attention_paged(const sd_dims_t* dims, const void* q, const void* k_pages, const void* v_pages,
+                                     const sd_kv_pages_t* pages, const int32_t* kv_len, float scale, void* out,
+                                     void* workspace, size_t workspace_bytes, sd_stream_t stream);
+
+/* sd_verify_step with the attention reading a paged cache; other arguments as there. */
+SD_API int sd_verify_step_paged(const sd_dims_t* dims, const void* q, const void* k_pages, const void* v_pages,
+                                const sd_kv_pages_t* pages, const int32_t* kv_len, float scale,
+                                const void* hidden, const void* w_vocab, const float* q_draft,
+                                const int32_t* draft_tok, const float* u, void* attn_out, float* logits,
+                                float* row_lse, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
+                                void* workspace, size_t workspace_bytes, sd_stream_t stream,
+                                void* const* kernel_events);
+
+/*
+ * Host-side page allocator of a paged pool (host memory only; no device
+ * work; not thread-safe: one caller at a time per pool).  Sessions are
+ * non-negative int32 tags.  Pages are handed out from a free list, lowest id
+ * first when the pool is fresh, and a freed page is the next one handed out.
+ *   sd_kv_pool_create      NULL if num_pages < 1 or page_size is not a power of two in [64, 4096]
+ *   sd_kv_pool_reserve     grow `tag`'s pages to hold `length` keys (a new tag starts empty);
+ *                          SD_ERR_CAPACITY, with nothing changed, if the free pages do not suffice
+ *   sd_kv_pool_truncate    keep the pages holding keys [0, length), free the rest
+ *                          (the roll-back to new_kv_len after a step)
+ *   sd_kv_pool_release     free all of `tag`'s pages and forget it
+ *   sd_kv_pool_free_pages  free pages in the pool
+ *   sd_kv_pool_tag_pages   pages `tag` holds (0 for an unknown tag)
+ *   sd_kv_pool_block_table (host) table [n][max_pages]: row i lists tags[i]'s pages in key
+ *                          order, then -1; SD_ERR_INVALID_ARGUMENT if a tag holds more than max_pages
+ * Negative tags or lengths give SD_ERR_INVALID_ARGUMENT.
+ */
+typedef struct sd_kv_pool sd_kv_pool_t;
+SD_API sd_kv_pool_t* sd_kv_pool_create(int32_t num_pages, int32_t page_size);
+SD_API void sd_kv_pool_destroy(sd_kv_pool_t* pool);
+SD_API int sd_kv_pool_reserve(sd_kv_pool_t* pool, int32_t tag, int32_t length);
+SD_API int sd_kv_pool_truncate(sd_kv_pool_t* pool, int32_t tag, int32_t length);
+SD_API int sd_kv_pool_release(sd_kv_pool_t* pool, int32_t tag);
+SD_API int32_t sd_kv_pool_free_pages(const sd_kv_pool_t* pool);
+SD_API int32_t sd_kv_pool_tag_pages(const sd_kv_pool_t* pool, int32_t tag);
+SD_API int sd_kv_pool_block_table(const sd_kv_pool_t* pool, const int32_t* tags, int32_t n, int32_t max_pages,
+                                  int32_t* table);
 
 /* Static description of a status code. */
 SD_API const char* sd_status_string(int status);

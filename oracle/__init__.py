@@ -30,6 +30,9 @@ What it computes (StarSD, "One-for-Many Speculative Decoding"):
   place of the longest-path rule of Algorithm 2, which is not lossless).
   Attention by definition; acceptance step by step.
 * :mod:`oracle.step` -- the composition of the three for one pooled batch.
+* :mod:`oracle.paged` -- attention of requests whose KV rows live in pages
+  of a shared pool (per-tag state, Algorithm 1): the rows gathered key by key
+  through the block table, then the chain attention above.  By definition.
 * :mod:`oracle.model` -- the performance model of Sec. 3 and Sec. 4.2: the
   acceptance rate beta (sum of min(p, q)), the expected accept length from
   the distribution of the accept length, and the per-iteration time, idle
@@ -48,10 +51,13 @@ from .warp import order_keys, warp_row, warped_from_cut
 from .tree import (accept_tree, accept_tree_request, ancestor_masks, tree_attention, tree_commit_kv,
                    tree_near_threshold)
 from .step import verify_step
+from .paged import gather_request, paged_attention
 from .model import (acceptance_rate, acceptance_rate_batch, accept_length_pmf, expected_accept_length, n_full, n_max,
                     per_target_throughput, simulate_star)
 
 __all__ = [
+    "gather_request",
+    "paged_attention",
     "acceptance_rate",
     "acceptance_rate_batch",
     "accept_length_pmf",

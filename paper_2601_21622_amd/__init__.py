@@ -11,6 +11,7 @@ loudly when the library has not been built.
 from ._binding import (  # noqa: F401
     SD_DTYPE_BF16,
     SD_DTYPE_F32,
+    SD_ERR_CAPACITY,
     SD_ERR_HIP,
     SD_ERR_INVALID_ARGUMENT,
     SD_ERR_UNSUPPORTED,
@@ -18,6 +19,8 @@ from ._binding import (  # noqa: F401
     SD_FLAG_PACKED_VOCAB,
     SD_OK,
     Dims,
+    KVPages,
+    KVPool,
     PreparedCall,
     Sampling,
     SdError,
@@ -25,6 +28,7 @@ from ._binding import (  # noqa: F401
     library,
     library_path,
     prepare_verify_step,
+    prepare_verify_step_paged,
     prepare_verify_step_sampled,
     prepare_verify_step_tree,
     sd_acceptance_rate,
@@ -35,9 +39,11 @@ from ._binding import (  # noqa: F401
     sd_status_string,
     sd_tree_commit_kv,
     sd_verify_attention,
+    sd_verify_attention_paged,
     sd_verify_attention_tree,
     sd_verify_logits,
     sd_verify_step,
+    sd_verify_step_paged,
     sd_verify_step_sampled,
     sd_verify_step_tree,
     sd_version,

@@ -22,6 +22,7 @@ SD_ERR_INVALID_ARGUMENT = -1
 SD_ERR_UNSUPPORTED = -2
 SD_ERR_WORKSPACE = -3
 SD_ERR_HIP = -4
+SD_ERR_CAPACITY = -5
 
 
 class SdError(RuntimeError):
@@ -64,6 +65,24 @@ class Sampling(ctypes.Structure):
     ]
 
 
+class KVPages(ctypes.Structure):
+    """sd_kv_pages_t: a paged cache's block table (device int32 [B][max_pages]),
+    keys per page and pages per pool.  Build it with KVPages.of(table, ...),
+    which keeps the table tensor referenced."""
+    _fields_ = [
+        ("block_table", ctypes.c_void_p),
+        ("max_pages", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("num_pages", ctypes.c_int32),
+    ]
+
+    @classmethod
+    def of(cls, block_table, page_size: int, num_pages: int) -> "KVPages":
+        pg = cls(_ptr(block_table), int(block_table.shape[-1]), int(page_size), int(num_pages))
+        pg._table = block_table
+        return pg
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -103,6 +122,26 @@ def library() -> ctypes.CDLL:
     lib.sd_tree_commit_kv.restype = ctypes.c_int
     lib.sd_acceptance_rate.argtypes = [DP, P, P, P, P, P, SZ, P]
     lib.sd_acceptance_rate.restype = ctypes.c_int
+    KP = ctypes.POINTER(KVPages)
+    lib.sd_verify_attention_paged.argtypes = [DP, P, P, P, KP, P, F, P, P, SZ, P]
+    lib.sd_verify_attention_paged.restype = ctypes.c_int
+    lib.sd_verify_step_paged.argtypes = [DP, P, P, P, KP, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
+    lib.sd_verify_step_paged.restype = ctypes.c_int
+    lib.sd_kv_pool_create.argtypes = [I32, I32]
+    lib.sd_kv_pool_create.restype = P
+    lib.sd_kv_pool_destroy.argtypes = [P]
+    lib.sd_kv_pool_destroy.restype = None
+    for name in ("sd_kv_pool_reserve", "sd_kv_pool_truncate"):
+        getattr(lib, name).argtypes = [P, I32, I32]
+        getattr(lib, name).restype = ctypes.c_int
+    lib.sd_kv_pool_release.argtypes = [P, I32]
+    lib.sd_kv_pool_release.restype = ctypes.c_int
+    lib.sd_kv_pool_free_pages.argtypes = [P]
+    lib.sd_kv_pool_free_pages.restype = I32
+    lib.sd_kv_pool_tag_pages.argtypes = [P, I32]
+    lib.sd_kv_pool_tag_pages.restype = I32
+    lib.sd_kv_pool_block_table.argtypes = [P, P, I32, I32, P]
+    lib.sd_kv_pool_block_table.restype = ctypes.c_int
     SP = ctypes.POINTER(Sampling)
     lib.sd_accept_resample_sampled.argtypes = [DP, SP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.sd_accept_resample_sampled.restype = ctypes.c_int
@@ -365,6 +404,84 @@ def prepare_verify_step_tree(*a, **kw) -> PreparedCall:
     """sd_verify_step_tree with the same arguments, converted once (see PreparedCall)."""
     args, keep = _step_tree_args(*a, **kw)
     return PreparedCall(library().sd_verify_step_tree, args, (keep, a, kw), "sd_verify_step_tree")
+
+
+def sd_verify_attention_paged(dims: Dims, q, k_pages, v_pages, pages: KVPages, kv_len, scale: float, out, workspace,
+                              stream=None) -> None:
+    _len, len_p = _host(kv_len, np.int32)
+    st = library().sd_verify_attention_paged(ctypes.byref(dims), _ptr(q), _ptr(k_pages), _ptr(v_pages),
+                                             ctypes.byref(pages), len_p, float(scale), _ptr(out), _ptr(workspace),
+                                             _nbytes(workspace), _stream(stream))
+    _check(st, "sd_verify_attention_paged")
+
+
+def _step_paged_args(dims, q, k_pages, v_pages, pages, kv_len, scale, hidden, w_vocab, q_draft, draft_tok, u,
+                     attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace, stream=None,
+                     kernel_events=None):
+    ln, len_p = _host(kv_len, np.int32)
+    ev = _event_handles(kernel_events)
+    args = (ctypes.byref(dims), _ptr(q), _ptr(k_pages), _ptr(v_pages), ctypes.byref(pages), len_p, float(scale),
+            _ptr(hidden), _ptr(w_vocab), _ptr(q_draft), _ptr(draft_tok), _ptr(u), _ptr(attn_out), _ptr(logits),
+            _ptr(row_lse), _ptr(accept_len), _ptr(out_tok), _ptr(new_kv_len), _ptr(workspace), _nbytes(workspace),
+            _stream(stream), ev)
+    return args, (dims, pages, ln, ev)
+
+
+def sd_verify_step_paged(dims: Dims, q, k_pages, v_pages, pages: KVPages, kv_len, scale: float, hidden, w_vocab,
+                         q_draft, draft_tok, u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace,
+                         stream=None, kernel_events=None) -> None:
+    args, _keep = _step_paged_args(dims, q, k_pages, v_pages, pages, kv_len, scale, hidden, w_vocab, q_draft,
+                                   draft_tok, u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len,
+                                   workspace, stream, kernel_events)
+    _check(library().sd_verify_step_paged(*args), "sd_verify_step_paged")
+
+
+def prepare_verify_step_paged(*a, **kw) -> PreparedCall:
+    """sd_verify_step_paged with the same arguments, converted once (see PreparedCall)."""
+    args, keep = _step_paged_args(*a, **kw)
+    return PreparedCall(library().sd_verify_step_paged, args, (keep, a, kw), "sd_verify_step_paged")
+
+
+class KVPool:
+    """The library's host-side page allocator (sd_kv_pool_*): per-tag page
+    lists over num_pages pages of page_size keys."""
+
+    def __init__(self, num_pages: int, page_size: int):
+        self._lib = library()
+        self._h = self._lib.sd_kv_pool_create(int(num_pages), int(page_size))
+        if not self._h:
+            raise SdError(SD_ERR_INVALID_ARGUMENT, "sd_kv_pool_create")
+        self.num_pages, self.page_size = int(num_pages), int(page_size)
+
+    def close(self) -> None:
+        if self._h:
+            self._lib.sd_kv_pool_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.close()
+
+    def reserve(self, tag: int, length: int) -> None:
+        _check(self._lib.sd_kv_pool_reserve(self._h, int(tag), int(length)), "sd_kv_pool_reserve")
+
+    def truncate(self, tag: int, length: int) -> None:
+        _check(self._lib.sd_kv_pool_truncate(self._h, int(tag), int(length)), "sd_kv_pool_truncate")
+
+    def release(self, tag: int) -> None:
+        _check(self._lib.sd_kv_pool_release(self._h, int(tag)), "sd_kv_pool_release")
+
+    def free_pages(self) -> int:
+        return int(self._lib.sd_kv_pool_free_pages(self._h))
+
+    def tag_pages(self, tag: int) -> int:
+        return int(self._lib.sd_kv_pool_tag_pages(self._h, int(tag)))
+
+    def block_table(self, tags, max_pages: int) -> np.ndarray:
+        t, t_p = _host(tags, np.int32)
+        out = np.empty((len(t), int(max_pages)), dtype=np.int32)
+        _check(self._lib.sd_kv_pool_block_table(self._h, t_p, len(t), int(max_pages),
+                                                out.ctypes.data_as(ctypes.c_void_p)), "sd_kv_pool_block_table")
+        return out
 
 
 def prepare_verify_step(*a, **kw) -> PreparedCall:

@@ -45,7 +45,9 @@ int check_dims(const sd_dims_t* d) {
   return SD_OK;
 }
 
-AttnShape attn_shape(const sd_dims_t* d, float scale, const int32_t* kv_len = nullptr) {
+// page_size > 0 (paged caches): chunks are whole pages, so each work item's
+// page ids fit one register (a chunk is at most 4096 keys, a page at least 64).
+AttnShape attn_shape(const sd_dims_t* d, float scale, const int32_t* kv_len = nullptr, int page_size = 0) {
   AttnShape s;
   s.G = d->gamma + 1;
   s.Hq = d->n_q_heads;
@@ -57,6 +59,7 @@ AttnShape attn_shape(const sd_dims_t* d, float scale, const int32_t* kv_len = nu
   if (kv_len != nullptr)
     for (int b = 0; b < d->batch; ++b) total += kv_len[b];
   s.chunk_keys = attn_chunk_keys(d->dtype, s.rows, s.Hkv, total);
+  if (page_size > 0) s.chunk_keys = (s.chunk_keys + page_size - 1) / page_size * page_size;
   s.scale_log2 = scale * 1.4426950408889634f;
   return s;
 }
@@ -80,6 +83,29 @@ size_t logits_ws(const sd_dims_t* d) {
   return align_up(vocab_workspace_bytes(p));
 }
 
+int log2_exact(int v) {
+  int k = 0;
+  while ((1 << k) < v) ++k;
+  return (1 << k) == v ? k : -1;
+}
+
+// A paged cache (bf16 only): table present and aligned, page size a power of
+// two in [64, 4096], every request's keys within its table row.
+int check_pages(const sd_dims_t* d, const sd_kv_pages_t* pg, const int32_t* kv_len) {
+  if (pg == nullptr || kv_len == nullptr || pg->block_table == nullptr || !aligned(pg->block_table, 4))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (d->dtype != SD_DTYPE_BF16) return SD_ERR_UNSUPPORTED;
+  const int shift = log2_exact(pg->page_size);
+  if (pg->page_size < 64 || pg->page_size > 4096 || shift < 0) return SD_ERR_INVALID_ARGUMENT;
+  if (pg->num_pages < 1 || pg->max_pages < 1) return SD_ERR_INVALID_ARGUMENT;
+  const int G = d->gamma + 1;
+  for (int b = 0; b < d->batch; ++b) {
+    if (kv_len[b] < G || kv_len[b] > kMaxKvLen) return SD_ERR_INVALID_ARGUMENT;
+    if (int64_t(kv_len[b]) > int64_t(pg->max_pages) * pg->page_size) return SD_ERR_INVALID_ARGUMENT;
+  }
+  return SD_OK;
+}
+
 int check_kv(const sd_dims_t* d, const int64_t* kv_off, const int32_t* kv_len) {
   if (kv_off == nullptr || kv_len == nullptr) return SD_ERR_INVALID_ARGUMENT;
   const int G = d->gamma + 1;
@@ -97,8 +123,9 @@ int hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
 // most kMaxReqPerLaunch requests whose tables ride in the kernel arguments.
 int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* v, const int64_t* kv_off,
                   const int32_t* kv_len, float scale, void* out, void* ws, hipStream_t stream,
-                  hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const uint64_t* anc = nullptr) {
-  const AttnShape s = attn_shape(d, scale, kv_len);
+                  hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const uint64_t* anc = nullptr,
+                  const sd_kv_pages_t* pages = nullptr) {
+  const AttnShape s = attn_shape(d, scale, kv_len, pages != nullptr ? pages->page_size : 0);
   const int64_t chunks = total_chunks(kv_len, d->batch, s.chunk_keys);
   const AttnPartials parts = attn_carve(ws, chunks, s.Hkv, s.rows, s.D);
   int64_t chunk_base = 0;
@@ -109,11 +136,17 @@ int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* 
     bt.req0 = r0;
     bt.chunk_base = static_cast<int32_t>(chunk_base);
     bt.anc = anc;
+    if (pages != nullptr) {
+      bt.pages = pages->block_table;
+      bt.page_shift = log2_exact(pages->page_size);
+      bt.max_pages = pages->max_pages;
+      bt.num_pages = pages->num_pages;
+    }
     int32_t acc = 0;
     for (int i = 0; i < bt.nreq; ++i) {
       bt.chunk_prefix[i] = acc;
       bt.kv_len[i] = kv_len[r0 + i];
-      bt.kv_off[i] = kv_off[r0 + i];
+      bt.kv_off[i] = kv_off != nullptr ? kv_off[r0 + i] : 0;
       acc += (kv_len[r0 + i] + s.chunk_keys - 1) / s.chunk_keys;
     }
     bt.chunk_prefix[bt.nreq] = acc;
@@ -212,6 +245,13 @@ int check_accept_args(const float* x, const float* row_lse, const float* q_draft
   return SD_OK;
 }
 
+int verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool, const int64_t* kv_off,
+                const sd_kv_pages_t* pages, const int32_t* kv_len, float scale, const void* hidden,
+                const void* w_vocab, const float* q_draft, const int32_t* draft_tok, const float* u,
+                void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
+                int32_t* new_kv_len, void* workspace, size_t workspace_bytes, sd_stream_t stream,
+                void* const* kernel_events);
+
 }  // namespace
 
 extern "C" {
@@ -300,6 +340,53 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
                    void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
                    int32_t* new_kv_len, void* workspace, size_t workspace_bytes, sd_stream_t stream,
                    void* const* kernel_events) {
+  return verify_step(dims, q, k_pool, v_pool, kv_off, nullptr, kv_len, scale, hidden, w_vocab, q_draft, draft_tok, u,
+                     attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace, workspace_bytes, stream,
+                     kernel_events);
+}
+
+int sd_verify_step_paged(const sd_dims_t* dims, const void* q, const void* k_pages, const void* v_pages,
+                         const sd_kv_pages_t* pages, const int32_t* kv_len, float scale, const void* hidden,
+                         const void* w_vocab, const float* q_draft, const int32_t* draft_tok, const float* u,
+                         void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
+                         int32_t* new_kv_len, void* workspace, size_t workspace_bytes, sd_stream_t stream,
+                         void* const* kernel_events) {
+  if (pages == nullptr) return SD_ERR_INVALID_ARGUMENT;
+  return verify_step(dims, q, k_pages, v_pages, nullptr, pages, kv_len, scale, hidden, w_vocab, q_draft, draft_tok,
+                     u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace, workspace_bytes,
+                     stream, kernel_events);
+}
+
+int sd_verify_attention_paged(const sd_dims_t* dims, const void* q, const void* k_pages, const void* v_pages,
+                              const sd_kv_pages_t* pages, const int32_t* kv_len, float scale, void* out,
+                              void* workspace, size_t workspace_bytes, sd_stream_t stream) {
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  if (!q || !k_pages || !v_pages || !out || !workspace) return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(q, 16) || !aligned(k_pages, 16) || !aligned(v_pages, 16) || !aligned(out, 16) ||
+      !aligned(workspace, 16))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return SD_ERR_INVALID_ARGUMENT;
+  st = check_pages(dims, pages, kv_len);
+  if (st != SD_OK) return st;
+  const AttnShape s = attn_shape(dims, scale, kv_len, pages->page_size);
+  if (workspace_bytes < attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)))
+    return SD_ERR_WORKSPACE;
+  return run_attention(dims, q, k_pages, v_pages, nullptr, kv_len, scale, out, workspace,
+                       static_cast<hipStream_t>(stream), nullptr, nullptr, nullptr, pages);
+}
+
+}  // extern "C"
+
+namespace {
+
+// One whole step; the cache is segments (kv_off) or pages (pages).
+int verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool, const int64_t* kv_off,
+                const sd_kv_pages_t* pages, const int32_t* kv_len, float scale, const void* hidden,
+                const void* w_vocab, const float* q_draft, const int32_t* draft_tok, const float* u,
+                void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
+                int32_t* new_kv_len, void* workspace, size_t workspace_bytes, sd_stream_t stream,
+                void* const* kernel_events) {
   int st = check_dims(dims);
   if (st != SD_OK) return st;
   if (!q || !k_pool || !v_pool || !attn_out || !w_vocab || !logits || !row_lse || !workspace)
@@ -312,9 +399,9 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   if (!(scale > 0.f) || !std::isfinite(scale)) return SD_ERR_INVALID_ARGUMENT;
   st = check_accept_args(logits, row_lse, q_draft, draft_tok, u, kv_len, accept_len, out_tok, new_kv_len);
   if (st != SD_OK) return st;
-  st = check_kv(dims, kv_off, kv_len);
+  st = pages != nullptr ? check_pages(dims, pages, kv_len) : check_kv(dims, kv_off, kv_len);
   if (st != SD_OK) return st;
-  const AttnShape s = attn_shape(dims, scale, kv_len);
+  const AttnShape s = attn_shape(dims, scale, kv_len, pages != nullptr ? pages->page_size : 0);
   const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
                                logits_ws(dims) + accept_stage_ws(dims));
   if (workspace_bytes < need) return SD_ERR_WORKSPACE;
@@ -326,7 +413,8 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   // Stream order serialises the stages, so they share one workspace: the
   // attention partials are dead once the combine has run, the vocabulary
   // statistics once the log-sum-exp combine has run.
-  st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out, workspace, stm, ev[0], ev[1]);
+  st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out, workspace, stm, ev[0], ev[1],
+                     nullptr, pages);
   if (st != SD_OK) return st;
   // The vocabulary statistics live at the start of the workspace and the
   // acceptance sums after them, since the fold reads the former while the
@@ -340,6 +428,10 @@ int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, con
   return run_accept(dims, logits, row_lse, partials, vp.ntiles, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
                     new_kv_len, acc_ws, stm, ev[4], ev[5]);
 }
+
+}  // namespace
+
+extern "C" {
 
 int sd_accept_resample_sampled(const sd_dims_t* dims, const sd_sampling_t* sampling, const float* logits,
                                const float* q_draft, const int32_t* draft_tok, const float* u, const int32_t* kv_len,
@@ -541,6 +633,7 @@ const char* sd_status_string(int status) {
     case SD_ERR_UNSUPPORTED: return "SD_ERR_UNSUPPORTED: shape outside what the kernels implement";
     case SD_ERR_WORKSPACE: return "SD_ERR_WORKSPACE: workspace smaller than sd_workspace_bytes requires";
     case SD_ERR_HIP: return "SD_ERR_HIP: a HIP launch or runtime call failed";
+    case SD_ERR_CAPACITY: return "SD_ERR_CAPACITY: the KV page pool has too few free pages";
     default: return "unknown status";
   }
 }

@@ -152,20 +152,66 @@ struct KVTile {
     return r * D * 2 + (((d >> 3) + rot(r)) % kPieces) * 16 + (d & 7) * 2;
   }
   // DMA instruction i of a tile: lane l brings row r = i*kRowsPerDma +
-  // l/kPieces, the global piece that belongs in LDS slot l%kPieces.  A dead
+  // l/kPieces, the global piece that belongs in LDS slot l%kPieces.  t0 is
+  // key k0's row; rows past the request's last key L - 1 repeat it.  A dead
   // tile (past the item's last, issued only to keep the pipeline shape) has
   // every lane read the same 16 bytes: one cache line per instruction.
-  __device__ static void load(const uint16_t* rows, int k0, int L, unsigned char* tile, int lane, bool dead = false) {
+  __device__ static void load(const uint16_t* t0, int k0, int L, unsigned char* tile, int lane, bool dead = false) {
 #pragma unroll
     for (int i = 0; i < kDmas; ++i) {
       const int r = i * kRowsPerDma + lane / kPieces;
       const int piece = (lane % kPieces - rot(r) + kPieces) % kPieces;
       const int key = min(k0 + r, L - 1);
-      const int64_t src = dead ? (int64_t)min(k0, L - 1) * D : (int64_t)key * D + piece * 8;
-      dma_16B_to_lds_opaque(rows + src, tile + i * 1024);
+      const int src = dead ? 0 : (key - k0) * D + piece * 8;
+      dma_16B_to_lds_opaque(t0 + src, tile + i * 1024);
     }
   }
 };
+
+// Where the K and V rows of one (request, KV head) live.  Contiguous: the
+// request's segment [Hkv][L][D] at kv_off.  Paged: pages [num_pages][Hkv][P][D]
+// (P = 2^shift keys) named by the request's block table; each wave loads the
+// page ids of its chunk once (lane j: the chunk's page j) and reads them back
+// per tile with readlane.  A 32-key tile never crosses a page (P is a multiple
+// of 32), so tile(k0) + (key - k0) * D addresses every key of the tile.
+template <int D, bool PAGED>
+struct KVSrc {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t page_elems = 0;  // paged: Hkv * P * D
+  int64_t head_off = 0;    // paged: g * P * D
+  int shift = 0, page0 = 0, ids = 0;
+  __device__ int64_t tile(int k0) const {
+    if (!PAGED) return (int64_t)k0 * D;
+    const int page = __builtin_amdgcn_readlane(ids, (k0 >> shift) - page0);
+    return (int64_t)page * page_elems + head_off + (int64_t)(k0 & ((1 << shift) - 1)) * D;
+  }
+};
+
+// The rows of (request b of the launch, KV head g) for the item whose chunk
+// starts at key k_begin (a multiple of the page size when paged).
+template <int D, bool PAGED>
+__device__ __forceinline__ KVSrc<D, PAGED> kv_src(const AttnShape& s, const AttnBatch& bt, const uint16_t* kp,
+                                                  const uint16_t* vp, int b, int g, int L, int k_begin) {
+  KVSrc<D, PAGED> src;
+  if (!PAGED) {
+    const int64_t base = bt.kv_off[b] + (int64_t)g * L * D;
+    src.k = kp + base;
+    src.v = vp + base;
+    return src;
+  }
+  src.k = kp;
+  src.v = vp;
+  src.shift = bt.page_shift;
+  src.page0 = k_begin >> bt.page_shift;
+  src.page_elems = ((int64_t)s.Hkv << bt.page_shift) * D;
+  src.head_off = ((int64_t)g << bt.page_shift) * D;
+  const int npages = (L + (1 << bt.page_shift) - 1) >> bt.page_shift;
+  const int j = min(src.page0 + (int)(threadIdx.x & 63), npages - 1);
+  const int id = bt.pages[(int64_t)(bt.req0 + b) * bt.max_pages + j];
+  src.ids = min(max(id, 0), bt.num_pages - 1);
+  return src;
+}
 
 // Per-wave running state of the online softmax over its query rows.
 template <int RB, int D>
@@ -238,21 +284,21 @@ __device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2,
 }
 
 // One step of a wave's software pipeline: start the DMAs of the next tile
-// (keys from k0_next) into (kdst, vdst), wait until only those are in flight,
+// (keys from k0_next, rows at kn / vn) into (kdst, vdst), wait until only those are in flight,
 // then fold the current tile.  The stage pointers are restrict-qualified, so
 // the compiler knows the new DMAs cannot write what this step reads and
 // leaves the ordering to the explicit wait.
 template <int RB, int D, bool TREE>
-__device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2, const uint16_t* Kb,
-                                          const uint16_t* Vb, int L, int k0_next, bool next_dead, int k0,
+__device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2, const uint16_t* kn,
+                                          const uint16_t* vn, int L, int k0_next, bool next_dead, int k0,
                                           bool masked, unsigned char* __restrict__ kdst,
                                           unsigned char* __restrict__ vdst, const unsigned char* __restrict__ ksrc,
                                           const unsigned char* __restrict__ vsrc) {
   using KT = KVTile<D, false>;
   using VT = KVTile<D, true>;
   const int lane = threadIdx.x & 63;
-  KT::load(Kb, k0_next, L, kdst, lane, next_dead);
-  VT::load(Vb, k0_next, L, vdst, lane, next_dead);
+  KT::load(kn, k0_next, L, kdst, lane, next_dead);
+  VT::load(vn, k0_next, L, vdst, lane, next_dead);
   wait_vmcnt<KT::kDmas + VT::kDmas>();
   attn_fold<RB, D, TREE>(st, scale_log2, k0, masked, ksrc, vsrc);
 }
@@ -328,7 +374,7 @@ __device__ __forceinline__ void init_rows(AttnRows<RB, D>& st, const AttnShape& 
   }
 }
 
-template <int RB, int D, bool TREE>
+template <int RB, int D, bool TREE, bool PAGED>
 __global__ __launch_bounds__(kAttnThreads, 1)
 void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
                       const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
@@ -353,12 +399,10 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
 
   const int b = find_request(bt, c_local);
   const int L = bt.kv_len[b];
-  const int64_t off = bt.kv_off[b];
   const int req = bt.req0 + b;
   const int k_begin = (c_local - bt.chunk_prefix[b]) * s.chunk_keys;
   const int k_end = min(L, k_begin + s.chunk_keys);
-  const uint16_t* Kb = kp + off + (int64_t)g * L * D;
-  const uint16_t* Vb = vp + off + (int64_t)g * L * D;
+  const KVSrc<D, PAGED> src = kv_src<D, PAGED>(s, bt, kp, vp, b, g, L, k_begin);
 
   AttnRows<RB, D> st;
   init_rows<RB, D>(st, s, bt.anc, q, req, g, L, 0);
@@ -372,11 +416,13 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   unsigned char* v0s = vs0 + wave * VT::kBytes;
   unsigned char* v1s = vs1 + wave * VT::kBytes;
   auto key0 = [&](int i) { return k_begin + min(i, ntiles - 1) * kTile; };
-  KT::load(Kb, key0(0), L, k0s, lane);
-  VT::load(Vb, key0(0), L, v0s, lane);
+  const int64_t t0 = src.tile(key0(0));
+  KT::load(src.k + t0, key0(0), L, k0s, lane);
+  VT::load(src.v + t0, key0(0), L, v0s, lane);
   for (int i = 0; i < ntiles; ++i) {
-    attn_step<RB, D, TREE>(st, s.scale_log2, Kb, Vb, L, key0(i + 1), i + 1 >= ntiles, key0(i),
-                     key0(i) + kTile - 1 > L - s.G, k1s, v1s, k0s, v0s);
+    const int64_t tn = src.tile(key0(i + 1));
+    attn_step<RB, D, TREE>(st, s.scale_log2, src.k + tn, src.v + tn, L, key0(i + 1), i + 1 >= ntiles, key0(i),
+                           key0(i) + kTile - 1 > L - s.G, k1s, v1s, k0s, v0s);
     unsigned char* t = k0s;
     k0s = k1s;
     k1s = t;
@@ -393,7 +439,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
 // registers, so the compiler's own vmcnt accounting covers the pipeline, and
 // two tiles of each wave are in flight while it folds.  With one 16-row block
 // (multi-head attention) two workgroups share a CU.
-template <int RB, int D, bool TREE>
+template <int RB, int D, bool TREE, bool PAGED>
 __global__ __launch_bounds__(kAttnThreads, (RB == 1 ? 2 : 1))
 void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
                           const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
@@ -413,12 +459,10 @@ void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
 
   const int b = find_request(bt, c_local);
   const int L = bt.kv_len[b];
-  const int64_t off = bt.kv_off[b];
   const int req = bt.req0 + b;
   const int k_begin = (c_local - bt.chunk_prefix[b]) * s.chunk_keys;
   const int k_end = min(L, k_begin + s.chunk_keys);
-  const uint16_t* Kb = kp + off + (int64_t)g * L * D;
-  const uint16_t* Vb = vp + off + (int64_t)g * L * D;
+  const KVSrc<D, PAGED> src = kv_src<D, PAGED>(s, bt, kp, vp, b, g, L, k_begin);
 
   AttnRows<RB, D> st;
   init_rows<RB, D>(st, s, bt.anc, q, req, g, L, 0);
@@ -435,11 +479,12 @@ void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
   auto issue = [&](int set, int i) {
     const int k0 = key0(i);
     const bool dead = i >= ntiles;
+    const int64_t t = src.tile(k0);
 #pragma unroll
     for (int it = 0; it < NV; ++it) {
-      const int64_t row = dead ? (int64_t)k0 * D : (int64_t)min(k0 + it * KPI + lane / LPR, L - 1) * D + (lane % LPR) * 8;
-      kr[set][it] = load_u32x4_stream(Kb + row);
-      vr[set][it] = load_u32x4_stream(Vb + row);
+      const int row = dead ? 0 : (min(k0 + it * KPI + lane / LPR, L - 1) - k0) * D + (lane % LPR) * 8;
+      kr[set][it] = load_u32x4_stream(src.k + t + row);
+      vr[set][it] = load_u32x4_stream(src.v + t + row);
     }
   };
   // Fold tile (set, k0) into the running state; live == false masks it.
@@ -580,37 +625,37 @@ void attn_combine_kernel(const AttnShape s, const AttnBatch bt, AttnPartials par
   for (int e = 0; e < 4; ++e) store_out(dst + e, num[e] / den);
 }
 
-template <int RB, int D, bool TREE>
+template <int RB, int D, bool TREE, bool PAGED>
 hipError_t launch_bf16(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                        const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   const int items = nchunks * s.Hkv;
-  hipExtLaunchKernelGGL((attn_bf16_kernel<RB, D, TREE>), dim3((items + kAttnWaves - 1) / kAttnWaves), dim3(kAttnThreads), 0,
+  hipExtLaunchKernelGGL((attn_bf16_kernel<RB, D, TREE, PAGED>), dim3((items + kAttnWaves - 1) / kAttnWaves), dim3(kAttnThreads), 0,
                         stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                         static_cast<const uint16_t*>(v), parts);
   return hipGetLastError();
 }
 
-template <int RB, int D, bool TREE>
+template <int RB, int D, bool TREE, bool PAGED>
 hipError_t launch_reg(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                       const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  hipExtLaunchKernelGGL((attn_bf16_reg_kernel<RB, D, TREE>), dim3((nchunks * s.Hkv + kAttnWaves - 1) / kAttnWaves),
+  hipExtLaunchKernelGGL((attn_bf16_reg_kernel<RB, D, TREE, PAGED>), dim3((nchunks * s.Hkv + kAttnWaves - 1) / kAttnWaves),
                         dim3(kAttnThreads), 0, stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q),
                         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), parts);
   return hipGetLastError();
 }
 
-template <int D, bool TREE>
+template <int D, bool TREE, bool PAGED>
 hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                        const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   switch (rb) {
-    case 1: return launch_reg<1, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 2: return launch_bf16<2, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 3: return launch_bf16<3, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 4: return launch_bf16<4, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 5: return launch_bf16<5, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 6: return launch_bf16<6, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 7: return launch_bf16<7, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 8: return launch_bf16<8, D, TREE>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 1: return launch_reg<1, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 2: return launch_bf16<2, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 3: return launch_bf16<3, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 4: return launch_bf16<4, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 5: return launch_bf16<5, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 6: return launch_bf16<6, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 7: return launch_bf16<7, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    case 8: return launch_bf16<8, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     default: return hipErrorInvalidValue;
   }
 }
@@ -711,6 +756,7 @@ hipError_t launch_attention(int dtype, const AttnShape& s, const AttnBatch& bt, 
                             hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   if (nchunks <= 0) return hipSuccess;
   if (dtype == 0) {
+    if (bt.pages != nullptr) return hipErrorInvalidValue;  // paged caches are bf16 only
     const size_t shm = sizeof(float) * static_cast<size_t>(s.rows) * (s.D + s.chunk_keys);
     hipExtLaunchKernelGGL(attn_f32_kernel, dim3(nchunks, s.Hkv), dim3(kAttnThreads), shm, stream, e0, e1, 0, s, bt,
                           static_cast<const float*>(q), static_cast<const float*>(k),
@@ -718,13 +764,20 @@ hipError_t launch_attention(int dtype, const AttnShape& s, const AttnBatch& bt, 
     return hipGetLastError();
   }
   const int rb = (s.rows + 15) / 16;
+  // Mask kinds: chain or tree; cache layouts: segments or pages (chain only).
   const bool tree = bt.anc != nullptr;
-  if (s.D == 128)
-    return tree ? dispatch_rb<128, true>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1)
-                : dispatch_rb<128, false>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-  if (s.D == 64)
-    return tree ? dispatch_rb<64, true>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1)
-                : dispatch_rb<64, false>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+  const bool paged = bt.pages != nullptr;
+  if (tree && paged) return hipErrorInvalidValue;
+  if (s.D == 128) {
+    if (paged) return dispatch_rb<128, false, true>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    return tree ? dispatch_rb<128, true, false>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1)
+                : dispatch_rb<128, false, false>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+  }
+  if (s.D == 64) {
+    if (paged) return dispatch_rb<64, false, true>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+    return tree ? dispatch_rb<64, true, false>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1)
+                : dispatch_rb<64, false, false>(rb, s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+  }
   return hipErrorInvalidValue;
 }
 

@@ -19,6 +19,10 @@ struct AttnBatch {
   int32_t kv_len[kMaxReqPerLaunch];
   int64_t kv_off[kMaxReqPerLaunch];
   const uint64_t* anc;  // tree verification: [B][G] ancestor masks (bit a: tail position a visible), or null
+  // Paged cache (kv_off unused): K and V pools [num_pages][Hkv][2^page_shift][D],
+  // block table [B][max_pages] of page ids (clamped into [0, num_pages)), or null.
+  const int32_t* pages;
+  int32_t page_shift, max_pages, num_pages;
 };
 
 // Tree verification: ancestor masks [B][N + 1] from parents [B][N] (node i's

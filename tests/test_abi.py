@@ -28,7 +28,10 @@ def test_library_loads_and_exports_header_symbols():
                           "sd_verify_step", "sd_status_string", "sd_version", "sd_vocab_packed_bytes",
                           "sd_pack_vocab", "sd_accept_resample_sampled", "sd_verify_step_sampled",
                           "sd_verify_attention_tree", "sd_accept_tree", "sd_verify_step_tree", "sd_tree_commit_kv",
-                          "sd_acceptance_rate"}
+                          "sd_acceptance_rate", "sd_verify_attention_paged", "sd_verify_step_paged",
+                          "sd_kv_pool_create", "sd_kv_pool_destroy", "sd_kv_pool_reserve", "sd_kv_pool_truncate",
+                          "sd_kv_pool_release", "sd_kv_pool_free_pages", "sd_kv_pool_tag_pages",
+                          "sd_kv_pool_block_table"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2
@@ -108,6 +111,31 @@ def test_logits_and_accept_reject_bad_arguments():
     short = (ctypes.c_int32 * 2)(2, 10)
     assert lib.sd_accept_resample(ctypes.byref(d), P, P, P, P, P, short, P, P, P, None, 0, None) == \
         sd.SD_ERR_INVALID_ARGUMENT
+
+
+@cpu_only
+def test_paged_calls_reject_bad_arguments():
+    lib = sd.library()
+    d = dims()
+    ln = (ctypes.c_int32 * 2)(200, 64)
+
+    def attn(pages, dd=d, lens=ln, ws=1 << 30):
+        return lib.sd_verify_attention_paged(ctypes.byref(dd), P, P, P, pages, lens, 0.088, P, P, ws, None)
+
+    good = sd.KVPages(P, 4, 64, 16)
+    assert attn(None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert attn(ctypes.byref(sd.KVPages(None, 4, 64, 16))) == sd.SD_ERR_INVALID_ARGUMENT
+    for bad in (sd.KVPages(P, 4, 32, 16), sd.KVPages(P, 4, 96, 16), sd.KVPages(P, 4, 8192, 16),
+                sd.KVPages(P, 0, 64, 16), sd.KVPages(P, 4, 64, 0), sd.KVPages(P + 2, 4, 64, 16),
+                sd.KVPages(P, 3, 64, 16)):                      # 3 pages of 64 < kv_len 200
+        assert attn(ctypes.byref(bad)) == sd.SD_ERR_INVALID_ARGUMENT
+    assert attn(ctypes.byref(good), dd=dims(dtype=0)) == sd.SD_ERR_UNSUPPORTED
+    assert attn(ctypes.byref(good), lens=(ctypes.c_int32 * 2)(3, 64)) == sd.SD_ERR_INVALID_ARGUMENT   # < G
+    assert attn(ctypes.byref(good), ws=8) == sd.SD_ERR_WORKSPACE
+    step = lib.sd_verify_step_paged
+    assert step(ctypes.byref(d), P, P, P, None, ln, 0.088, P, P, P, P, P, P, P, P, P, P, None, P, 1 << 30, None,
+                None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert sd.sd_status_string(sd.SD_ERR_CAPACITY).startswith("SD_ERR_CAPACITY")
 
 
 @cpu_only
