@@ -33,6 +33,9 @@ What it computes (StarSD, "One-for-Many Speculative Decoding"):
 * :mod:`oracle.paged` -- attention of requests whose KV rows live in pages
   of a shared pool (per-tag state, Algorithm 1): the rows gathered key by key
   through the block table, then the chain attention above.  By definition.
+* :mod:`oracle.expand` -- the draft side's layer expansion (Algorithm 2,
+  ExpandLayer): top-k children per frontier node with their draft
+  probabilities.  By definition.
 * :mod:`oracle.model` -- the performance model of Sec. 3 and Sec. 4.2: the
   acceptance rate beta (sum of min(p, q)), the expected accept length from
   the distribution of the accept length, and the per-iteration time, idle
@@ -52,10 +55,14 @@ from .tree import (accept_tree, accept_tree_request, ancestor_masks, tree_attent
                    tree_near_threshold)
 from .step import verify_step
 from .paged import gather_request, paged_attention
+from .expand import expand_layer, full_tree_layout, top_k_tokens
 from .model import (acceptance_rate, acceptance_rate_batch, accept_length_pmf, expected_accept_length, n_full, n_max,
                     per_target_throughput, simulate_star)
 
 __all__ = [
+    "expand_layer",
+    "full_tree_layout",
+    "top_k_tokens",
     "gather_request",
     "paged_attention",
     "acceptance_rate",
