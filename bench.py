@@ -121,6 +121,51 @@ def paged_caches(sd, cfg, x, k_pool, v_pool, P):
     return kp, vp, torch.from_numpy(np.ascontiguousarray(table)).cuda(), num_pages
 
 
+def expand_leg(sd, cfg, args) -> dict:
+    """Draft-side tree expansion for the workload's B requests: a full K-ary
+    tree of depth D grown layer by layer from synthetic draft logits."""
+    import numpy as np
+    import torch
+
+    k, depth = (int(v) for v in args.expand.split(","))
+    B, V = cfg.batch, cfg.vocab
+    layers, first, F = [], 0, 1
+    f0 = -1
+    for _ in range(depth):
+        layers.append((f0, first, F))
+        f0, first, F = first, first + F * k, F * k
+    N = first
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    logits = [torch.randn((B, L[2], V), device="cuda", generator=gen) * 2.0 for L in layers]
+    tok = torch.empty((B, N), dtype=torch.int32, device="cuda")
+    par = torch.empty_like(tok)
+    q = torch.empty((B, N), dtype=torch.float32, device="cuda")
+    specs = [sd.Expand(B, F_, V, k, f0_, first_, N) for (f0_, first_, F_) in layers]
+
+    def grow():
+        for e, x in zip(specs, logits):
+            sd.sd_expand_layer(e, x, tok, par, q)
+
+    for _ in range(3):
+        grow()
+    torch.cuda.synchronize()
+    n = max(10, min(args.steps, 100))
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record()
+    for _ in range(n):
+        grow()
+    s1.record()
+    torch.cuda.synchronize()
+    ms = s0.elapsed_time(s1) / n
+    nbytes = sum(B * L[2] * V * 4 for L in layers)
+    par_h = par.cpu().numpy()
+    if not all(np.all(par_h[:, j] < j) for j in range(N)):
+        raise RuntimeError("expanded tree has a parent after its child")
+    log(f"expansion: {N} nodes per request, {ms * 1e3:.1f} us per tree ({nbytes / (ms * 1e-3) / 1e9:.0f} GB/s)")
+    return {"top_k": k, "depth": depth, "nodes": N, "requests": B, "ms_per_tree": ms, "bytes_per_tree": nbytes,
+            "hbm_gbps": nbytes / (ms * 1e-3) / 1e9, "launches_per_tree": depth}
+
+
 def starsd_leg(sd, dims, cfg, copies, ms_step, args) -> dict:
     """Acceptance rates of the step's own target and draft distributions
     (sd_acceptance_rate, timed on its own), then the performance model with
@@ -180,6 +225,9 @@ def main() -> int:
     ap.add_argument("--paged", type=int, default=0, metavar="P",
                     help="keep the KV caches in a paged pool of P-key pages (sd_verify_step_paged); pages come "
                          "from the library's allocator with the requests growing in turn, so they interleave")
+    ap.add_argument("--expand", default=None, metavar="K,D",
+                    help="also time the draft-side expansion of a full K-ary tree of depth D for the workload's "
+                         "requests and vocabulary (sd_expand_layer, D launches per tree; synthetic draft logits)")
     ap.add_argument("--starsd", default=None, metavar="T_S,T_C[,RATE]",
                     help="also time sd_acceptance_rate on the step's distributions and evaluate the StarSD model "
                          "with the measured t_v: draft time per layer t_s and transfer time t_c in ms, and "
@@ -400,6 +448,8 @@ def main() -> int:
     }
     if args.starsd is not None:
         result["starsd"] = starsd_leg(sd, dims, cfg, copies, ms_step, args)
+    if args.expand is not None:
+        result["expand"] = expand_leg(sd, cfg, args)
     if not args.no_cpu_baseline and sampling is None and not args.tree_nodes and not args.paged:
         # the CPU leg times the plain step
         log("timing the CPU oracle on the same batch")

@@ -429,6 +429,41 @@ SD_API int32_t sd_kv_pool_tag_pages(const sd_kv_pool_t* pool, int32_t tag);
 SD_API int sd_kv_pool_block_table(const sd_kv_pool_t* pool, const int32_t* tags, int32_t n, int32_t max_pages,
                                   int32_t* table);
 
+/*
+ * Draft-side tree expansion, batched over pooled requests (Algorithm 2,
+ * ExpandLayer: the draft model grows its proposal tree one layer at a time,
+ * every frontier node taking the top-k tokens of the draft's next-token
+ * distribution there as children, and keeps their draft probabilities for
+ * the correction step).  The draft model's forward pass is the caller's; this
+ * call turns its logits at the frontier into the next layer of the tree
+ * arrays that sd_verify_step_tree consumes.
+ *   draft_logits  [B][F][V] float32 (device): row (b, f) holds the draft's logits
+ *                 at frontier node frontier0 + f of request b (finite or -inf,
+ *                 at least one finite per row)
+ *   tokens, parent [B][N] int32 (device), q_child [B][N] float32 (device):
+ *                 entries first_child + f*k + j, j < k, are written: the j-th
+ *                 ranked token of row (b, f), its parent frontier0 + f (-1 when
+ *                 frontier0 = -1, i.e. the frontier is the root), and its draft
+ *                 probability exp(logit - logsumexp(row)); nothing else is written
+ * Rank: larger float32 logit first (-0 below +0), equal logits by increasing
+ * token id.  Requires 1 <= k <= min(V, 16), first_child + F*k <= N and, for
+ * frontier0 >= 0, frontier0 + F <= first_child (parents precede children).
+ * For a full k-ary tree numbered layer by layer: layer 1 (frontier0 = -1,
+ * first_child = 0, F = 1), layer t + 1 (frontier0 = first_child of layer t,
+ * F = k^t, first_child = that plus k^t).
+ */
+typedef struct {
+  int32_t batch;        /* B requests */
+  int32_t frontier;     /* F frontier nodes per request */
+  int32_t vocab;        /* V */
+  int32_t top_k;        /* k children per frontier node */
+  int32_t frontier0;    /* tree index of frontier node 0, -1 for the root */
+  int32_t first_child;  /* tree index of the first new node */
+  int32_t nodes;        /* N: entries per request in tokens, parent and q_child */
+} sd_expand_t;
+SD_API int sd_expand_layer(const sd_expand_t* e, const float* draft_logits, int32_t* tokens, int32_t* parent,
+                           float* q_child, sd_stream_t stream);
+
 /* Static description of a status code. */
 SD_API const char* sd_status_string(int status);
 

@@ -19,6 +19,7 @@ from ._binding import (  # noqa: F401
     SD_FLAG_PACKED_VOCAB,
     SD_OK,
     Dims,
+    Expand,
     KVPages,
     KVPool,
     PreparedCall,
@@ -32,6 +33,7 @@ from ._binding import (  # noqa: F401
     prepare_verify_step_sampled,
     prepare_verify_step_tree,
     sd_acceptance_rate,
+    sd_expand_layer,
     sd_accept_resample,
     sd_accept_resample_sampled,
     sd_accept_tree,

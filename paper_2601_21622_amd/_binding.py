@@ -83,6 +83,12 @@ class KVPages(ctypes.Structure):
         return pg
 
 
+class Expand(ctypes.Structure):
+    """sd_expand_t: one layer of draft-side tree expansion."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("batch", "frontier", "vocab", "top_k", "frontier0", "first_child",
+                                              "nodes")]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -127,6 +133,8 @@ def library() -> ctypes.CDLL:
     lib.sd_verify_attention_paged.restype = ctypes.c_int
     lib.sd_verify_step_paged.argtypes = [DP, P, P, P, KP, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
     lib.sd_verify_step_paged.restype = ctypes.c_int
+    lib.sd_expand_layer.argtypes = [ctypes.POINTER(Expand), P, P, P, P, P]
+    lib.sd_expand_layer.restype = ctypes.c_int
     lib.sd_kv_pool_create.argtypes = [I32, I32]
     lib.sd_kv_pool_create.restype = P
     lib.sd_kv_pool_destroy.argtypes = [P]
@@ -297,6 +305,12 @@ def sd_acceptance_rate(dims: Dims, logits_or_probs, row_lse, q_draft, beta, work
     st = library().sd_acceptance_rate(ctypes.byref(dims), _ptr(logits_or_probs), _ptr(row_lse), _ptr(q_draft),
                                       _ptr(beta), _ptr(workspace), _nbytes(workspace), _stream(stream))
     _check(st, "sd_acceptance_rate")
+
+
+def sd_expand_layer(e: Expand, draft_logits, tokens, parent, q_child, stream=None) -> None:
+    st = library().sd_expand_layer(ctypes.byref(e), _ptr(draft_logits), _ptr(tokens), _ptr(parent), _ptr(q_child),
+                                   _stream(stream))
+    _check(st, "sd_expand_layer")
 
 
 def _event_handles(events):

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsdverify.so")
-SOURCES = ["api.hip", "attention.hip", "vocab.hip", "accept.hip", "warp.hip", "rate.hip", "pool.hip"]
+SOURCES = ["api.hip", "attention.hip", "vocab.hip", "accept.hip", "warp.hip", "rate.hip", "pool.hip", "expand.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

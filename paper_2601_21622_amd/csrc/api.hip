@@ -608,6 +608,23 @@ int sd_acceptance_rate(const sd_dims_t* dims, const float* logits_or_probs, cons
                                 beta, static_cast<hipStream_t>(stream)));
 }
 
+int sd_expand_layer(const sd_expand_t* e, const float* draft_logits, int32_t* tokens, int32_t* parent,
+                    float* q_child, sd_stream_t stream) {
+  if (e == nullptr || !draft_logits || !tokens || !parent || !q_child) return SD_ERR_INVALID_ARGUMENT;
+  if (!aligned(draft_logits, 4) || !aligned(tokens, 4) || !aligned(parent, 4) || !aligned(q_child, 4))
+    return SD_ERR_INVALID_ARGUMENT;
+  if (e->batch < 1 || e->frontier < 1 || e->vocab < 1 || e->top_k < 1 || e->nodes < 1 || e->first_child < 0 ||
+      e->frontier0 < -1)
+    return SD_ERR_INVALID_ARGUMENT;
+  if (e->top_k > e->vocab) return SD_ERR_INVALID_ARGUMENT;
+  if (e->top_k > kExpandMaxK || e->vocab > kMaxVocab) return SD_ERR_UNSUPPORTED;
+  if (int64_t(e->first_child) + int64_t(e->frontier) * e->top_k > e->nodes) return SD_ERR_INVALID_ARGUMENT;
+  if (e->frontier0 >= 0 && int64_t(e->frontier0) + e->frontier > e->first_child) return SD_ERR_INVALID_ARGUMENT;
+  if (int64_t(e->batch) * e->frontier > 0x7fffffff) return SD_ERR_UNSUPPORTED;
+  const ExpandArgs a{e->batch, e->frontier, e->vocab, e->top_k, e->frontier0, e->first_child, e->nodes};
+  return hip_status(launch_expand(a, draft_logits, tokens, parent, q_child, static_cast<hipStream_t>(stream)));
+}
+
 size_t sd_vocab_packed_bytes(const sd_dims_t* dims) {
   if (check_dims(dims) != SD_OK || dims->dtype != SD_DTYPE_BF16) return 0;
   return vocab_packed_bytes(dims->hidden, dims->vocab);

@@ -150,4 +150,14 @@ size_t rate_workspace_bytes(int B, int gamma, int V);
 hipError_t launch_rate(int gamma, int V, int B, const float* x, const float* row_lse, const float* q_draft, void* ws,
                        double* beta, hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
+// Draft-side layer expansion: children first_child + f*k + j (j < k, rank
+// order) of frontier node frontier0 + f (-1: the root) of each of B requests,
+// from the draft logits [B][F][V]; tokens, parent, q_child are [B][N].
+constexpr int kExpandMaxK = 16;
+struct ExpandArgs {
+  int32_t B, F, V, k, frontier0, first_child, N;
+};
+hipError_t launch_expand(const ExpandArgs& e, const float* logits, int32_t* tokens, int32_t* parent, float* q_child,
+                         hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+
 }  // namespace sdv

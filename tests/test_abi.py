@@ -31,7 +31,7 @@ def test_library_loads_and_exports_header_symbols():
                           "sd_acceptance_rate", "sd_verify_attention_paged", "sd_verify_step_paged",
                           "sd_kv_pool_create", "sd_kv_pool_destroy", "sd_kv_pool_reserve", "sd_kv_pool_truncate",
                           "sd_kv_pool_release", "sd_kv_pool_free_pages", "sd_kv_pool_tag_pages",
-                          "sd_kv_pool_block_table"}
+                          "sd_kv_pool_block_table", "sd_expand_layer"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2
@@ -136,6 +136,27 @@ def test_paged_calls_reject_bad_arguments():
     assert step(ctypes.byref(d), P, P, P, None, ln, 0.088, P, P, P, P, P, P, P, P, P, P, None, P, 1 << 30, None,
                 None) == sd.SD_ERR_INVALID_ARGUMENT
     assert sd.sd_status_string(sd.SD_ERR_CAPACITY).startswith("SD_ERR_CAPACITY")
+
+
+@cpu_only
+def test_expand_rejects_bad_arguments():
+    lib = sd.library()
+
+    def call(**kw):
+        base = dict(batch=2, frontier=3, vocab=100, top_k=4, frontier0=1, first_child=4, nodes=16)
+        base.update(kw)
+        return lib.sd_expand_layer(ctypes.byref(sd.Expand(**base)), P, P, P, P, None)
+
+    assert lib.sd_expand_layer(None, P, P, P, P, None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert lib.sd_expand_layer(ctypes.byref(sd.Expand(2, 3, 100, 4, 1, 4, 16)), P + 2, P, P, P, None) == \
+        sd.SD_ERR_INVALID_ARGUMENT
+    assert call(top_k=0) == sd.SD_ERR_INVALID_ARGUMENT
+    assert call(top_k=17) == sd.SD_ERR_UNSUPPORTED
+    assert call(vocab=3) == sd.SD_ERR_INVALID_ARGUMENT              # k > V
+    assert call(nodes=15) == sd.SD_ERR_INVALID_ARGUMENT             # 4 + 3*4 > 15
+    assert call(frontier0=2) == sd.SD_ERR_INVALID_ARGUMENT          # frontier 2..4 overlaps the children at 4
+    assert call(frontier0=-2) == sd.SD_ERR_INVALID_ARGUMENT
+    assert call(batch=0) == sd.SD_ERR_INVALID_ARGUMENT
 
 
 @cpu_only

@@ -1,0 +1,111 @@
+"""GPU parity of the draft-side layer expansion (sd_expand_layer) against
+the oracle (oracle.expand).
+
+Tokens and parents are integers decided by float32 comparisons that both
+sides make on the same float32 logits, so they must agree exactly; the
+draft probabilities within 2e-6 relative (float32 exp of a difference kept
+exact, normaliser summed in float64).  Rows are seeded normal logits with
+planted ties (repeated values, signed zeros) and some -inf entries;
+vocabularies from 1 to 128256, k from 1 to 16, one to 70 requests, and a
+full k-ary tree grown layer by layer whose arrays then drive
+sd_accept_tree."""
+
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2601_21622_amd as sd
+from oracle import expand_layer, full_tree_layout
+
+from gpu_util import announce, tensor, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _logits(rng, B, F, V):
+    x = (rng.standard_normal((B, F, V)) * 2.0).astype(np.float32)
+    if V >= 8:
+        for b in range(B):
+            for f in range(F):
+                idx = rng.choice(V, size=min(V // 4, 6), replace=False)
+                x[b, f, idx] = x[b, f, idx[0]]           # ties
+                x[b, f, rng.integers(0, V)] = -0.0
+                x[b, f, rng.integers(0, V)] = 0.0
+                x[b, f, rng.integers(0, V)] = -np.inf
+    return x
+
+
+def _run_layer(x, k, frontier0, first_child, N, tok=None, par=None, q=None):
+    B, F, V = x.shape
+    if tok is None:
+        tok = torch.full((B, N), -1, dtype=torch.int32, device="cuda")
+        par = torch.full((B, N), -1, dtype=torch.int32, device="cuda")
+        q = torch.zeros((B, N), dtype=torch.float32, device="cuda")
+    sd.sd_expand_layer(sd.Expand(B, F, V, k, frontier0, first_child, N), tensor(x), tok, par, q)
+    return tok, par, q
+
+
+CASES = [
+    ("v1_k1", 3, 1, 1, 1),
+    ("v7_k7", 2, 3, 7, 7),
+    ("v1000_k4", 8, 5, 1000, 4),
+    ("v32000_k10", 4, 8, 32000, 10),
+    ("v128256_k16", 2, 4, 128256, 16),
+    ("pooled_70", 70, 2, 3001, 8),
+]
+
+
+@pytest.mark.parametrize("name,B,F,V,k", CASES)
+def test_expand_matches_oracle(name, B, F, V, k):
+    announce(f"expand case={name} B={B} F={F} V={V} k={k}")
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    x = _logits(rng, B, F, V)
+    frontier0, first = 2, 2 + F
+    N = first + F * k + 3
+    tok, par, q = _run_layer(x, k, frontier0, first, N)
+    torch.cuda.synchronize()
+    rt, rp, rq = expand_layer(x, k, frontier0, first, N)
+    assert np.array_equal(to_np(tok), rt)
+    assert np.array_equal(to_np(par), rp)
+    gq = to_np(q).astype(np.float64)
+    sl = slice(first, first + F * k)
+    assert np.all(np.abs(gq[:, sl] - rq[:, sl]) <= 2e-6 * rq[:, sl] + 1e-30)
+    assert np.all(gq[:, :first] == 0) and np.all(gq[:, first + F * k:] == 0)    # nothing else written
+
+
+def test_full_tree_then_tree_acceptance():
+    # k = 2, depth 5: 62 nodes; the draft "model" is a seeded logit table per node.
+    B, V, k, depth = 4, 500, 2, 5
+    rng = np.random.default_rng(31)
+    layers, N = full_tree_layout(k, depth)
+    tok = par = q = None
+    rt = rp = rq = None
+    for frontier0, first, F in layers:
+        x = _logits(rng, B, F, V)
+        tok, par, q = _run_layer(x, k, frontier0, first, N, tok, par, q)
+        rt, rp, rq = expand_layer(x, k, frontier0, first, N, rt, rp, rq)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(tok), rt) and np.array_equal(to_np(par), rp)
+    assert np.all(rp[:, :k] == -1) and all(np.all(rp[:, n] < n) for n in range(N))
+    # The tree arrays drive tree acceptance directly (target logits: seeded).
+    from oracle import accept_tree, tree_near_threshold
+    G = N + 1
+    logits = (rng.standard_normal((B * G, V)) * 2.0).astype(np.float32)
+    l64 = logits.astype(np.float64)
+    lse = (l64.max(1) + np.log(np.exp(l64 - l64.max(1, keepdims=True)).sum(1))).astype(np.float32)
+    u = rng.random((B, G)).astype(np.float32)
+    from workloads import get_config
+    dims = sd.Dims.of(get_config("tiny").replace(batch=B, gamma=N, vocab=V, n_q_heads=1, n_kv_heads=1))
+    acc = torch.empty((B,), dtype=torch.int32, device="cuda")
+    otok = torch.empty((B, G), dtype=torch.int32, device="cuda")
+    onode = torch.empty((B, G), dtype=torch.int32, device="cuda")
+    ws = torch.empty((sd.sd_workspace_bytes(dims, G),), dtype=torch.uint8, device="cuda")
+    sd.sd_accept_tree(dims, tensor(logits), tensor(lse), tok, par, tensor(u), None, acc, otok, onode, None, ws)
+    torch.cuda.synchronize()
+    ref = accept_tree(logits, lse, rt, rp, u)
+    keep = ~np.array([tree_near_threshold(t) for t in ref["traces"]])
+    assert np.array_equal(to_np(acc)[keep], ref["accept_len"][keep])
+    assert np.array_equal(to_np(otok)[keep], ref["out_tok"][keep])
+    announce(f"expanded tree: {N} nodes, accept lengths {to_np(acc).tolist()}")
