@@ -55,10 +55,7 @@ AttnShape attn_shape(const sd_dims_t* d, float scale, const int32_t* kv_len = nu
   s.D = d->head_dim;
   s.group = d->n_q_heads / d->n_kv_heads;
   s.rows = s.G * s.group;
-  int64_t total = 0;
-  if (kv_len != nullptr)
-    for (int b = 0; b < d->batch; ++b) total += kv_len[b];
-  s.chunk_keys = attn_chunk_keys(d->dtype, s.rows, s.Hkv, total);
+  s.chunk_keys = attn_chunk_keys(d->dtype, s.rows, s.Hkv, kv_len, d->batch);
   if (page_size > 0) s.chunk_keys = (s.chunk_keys + page_size - 1) / page_size * page_size;
   s.scale_log2 = scale * 1.4426950408889634f;
   return s;

@@ -46,6 +46,12 @@ constexpr int kMaxChunkKeys = 4096;
 // (1024 slots, whose row groups come with long, uneven contexts).
 constexpr int64_t kAttnTargetItemsOne = 2048;
 constexpr int64_t kAttnTargetItemsMany = 4096;
+// Small batches of the one-block kernel: when the default split leaves CUs
+// without a workgroup, the shortest chunk (>= kRoundMinKeys) whose
+// workgroups fit one round of one per CU is taken instead (shorter chunks
+// that spill into a second workgroup on some CUs were measured slower).
+constexpr int kRoundMinKeys = 160;
+constexpr int64_t kRoundWorkgroups = 256;
 
 
 __device__ __forceinline__ int find_request(const AttnBatch& bt, int c) {
@@ -715,21 +721,32 @@ void tree_masks_kernel(int N, const int32_t* __restrict__ parent, uint64_t* __re
 
 }  // namespace
 
-int attn_chunk_keys(int dtype, int rows, int Hkv, int64_t total_keys) {
+int attn_chunk_keys(int dtype, int rows, int Hkv, const int32_t* kv_len, int B) {
   if (dtype == 0) return kF32ChunkKeys;
+  int64_t total_keys = 0;
+  if (kv_len != nullptr)
+    for (int b = 0; b < B; ++b) total_keys += kv_len[b];
   // A whole number of 32-key tiles; never so short that an item's start-up
   // (query rows, first tile) outweighs its streaming.
   const int64_t target = rows <= 16 ? kAttnTargetItemsOne : kAttnTargetItemsMany;
   const int64_t per = (total_keys * Hkv + target - 1) / target;
   const int64_t c = (per + kTile - 1) / kTile * kTile;
-  return (int)std::min<int64_t>(kMaxChunkKeys, std::max<int64_t>(kMinChunkKeys, c));
+  const int def = (int)std::min<int64_t>(kMaxChunkKeys, std::max<int64_t>(kMinChunkKeys, c));
+  if (rows <= 16 && kv_len != nullptr) {
+    for (int r = kRoundMinKeys; r < def; r += kTile) {
+      int64_t items = 0;
+      for (int b = 0; b < B; ++b) items += (kv_len[b] + r - 1) / r;
+      if ((items * Hkv + kAttnWaves - 1) / kAttnWaves <= kRoundWorkgroups) return r;
+    }
+  }
+  return def;
 }
 
 int64_t attn_max_chunks(int dtype, int Hkv, int B, int64_t max_kv_len) {
   if (dtype == 0) return (int64_t)B * ((max_kv_len + kF32ChunkKeys - 1) / kF32ChunkKeys);
   // chunks = sum_b ceil(L_b / C) <= sum(L)/C + B, with C >= sum(L)*Hkv/target
   // unless C is capped at kMaxChunkKeys, and never more than with C at its floor.
-  const int64_t by_floor = (int64_t)B * ((max_kv_len + kMinChunkKeys - 1) / kMinChunkKeys);
+  const int64_t by_floor = (int64_t)B * ((max_kv_len + kRoundMinKeys - 1) / kRoundMinKeys);
   const int64_t target = std::max(kAttnTargetItemsOne, kAttnTargetItemsMany);
   const int64_t by_target = std::max<int64_t>((target + Hkv - 1) / Hkv,
                                               (int64_t)B * ((max_kv_len + kMaxChunkKeys - 1) / kMaxChunkKeys)) + B;

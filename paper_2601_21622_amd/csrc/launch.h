@@ -57,7 +57,7 @@ struct AttnPartials {
 
 // Keys per work item (chunk), from the total number of keys over the batch;
 // attn_max_chunks bounds the chunk count for any lengths up to max_kv_len.
-int attn_chunk_keys(int dtype, int rows, int Hkv, int64_t total_keys);
+int attn_chunk_keys(int dtype, int rows, int Hkv, const int32_t* kv_len, int B);
 int64_t attn_max_chunks(int dtype, int Hkv, int B, int64_t max_kv_len);
 size_t attn_partial_bytes(int64_t total_chunks, int Hkv, int rows, int D);
 AttnPartials attn_carve(void* ws, int64_t total_chunks, int Hkv, int rows, int D);
