@@ -20,7 +20,9 @@
 // p(v) = exp(logit - lse) keeps the difference exact (TwoSum) so its error is
 // a few float32 ulp, far below the 1e-6 decision band.
 #include <hip/hip_ext.h>
+#include <string.h>
 
+#include "combine.h"
 #include "common.h"
 #include "launch.h"
 
@@ -207,6 +209,7 @@ __global__ __launch_bounds__(kSumWaves * kWave)
 void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* __restrict__ partials, int ntiles,
                         int32_t* __restrict__ accept_len) {
   __shared__ float s_lse[kWave];
+  __shared__ WarpRow s_warp[kWave];
   __shared__ int s_l;
   const int s = blockIdx.x;
   const int req = bt.req0 + blockIdx.y;
@@ -249,6 +252,9 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
   } else if (a.lse != nullptr && threadIdx.x < G) {
     s_lse[threadIdx.x] = a.lse[(int64_t)req * G + threadIdx.x];
   }
+  // Warped target: every row's cut, ahead of the accept length that picks one.
+  if (a.warp != nullptr && threadIdx.x >= kWave && threadIdx.x < kWave + G)
+    s_warp[threadIdx.x - kWave] = a.warp[(int64_t)req * G + threadIdx.x - kWave];
   __syncthreads();
 
   // 2. Ratio tests in float64; l = number of leading accepts.
@@ -260,7 +266,7 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
         double px;
         if (a.warp != nullptr) {
           // Warped target: the row's cut and normaliser (greedy: one-hot).
-          const WarpRow w = a.warp[(int64_t)req * G + lane];
+          const WarpRow w = s_warp[lane];
           const int tok = a.draft[(int64_t)req * a.gamma + lane];
           px = tok == w.argmax ? 1.0
                                : (order_key(xv) >= w.theta ? exp((double)xv * (double)w.inv_t - (double)w.lse) : 0.0);
@@ -281,7 +287,11 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
   }
   __syncthreads();
   const int l = s_l;
-  const RowP rp = row_p(a, (int64_t)req * G + l, a.lse != nullptr ? s_lse[l] : 0.f);
+  RowP rp{a.lse != nullptr ? s_lse[l] : 0.f, 1.f, 0u, -1};
+  if (a.warp != nullptr) {
+    const WarpRow w = s_warp[l];
+    rp = RowP{w.lse, w.inv_t, w.theta, w.argmax};
+  }
   const bool residual = l < a.gamma;
   const float* xrow = a.x + ((int64_t)req * G + l) * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
@@ -293,11 +303,19 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
 }
 
 // One wave per request: prefix of the segment totals, the segment holding
-// u * Z, and the scan of that segment in token order.
-__global__ __launch_bounds__(kWave)
+// u * Z, and the scan of that segment in token order.  Blocks past the
+// requests carry an attention merge (cj.nblocks blocks), which then runs in
+// the idle CUs of this latency-bound launch; a request's block uses its
+// first wave only.
+__global__ __launch_bounds__(kCombineThreads)
 void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t* __restrict__ accept_len,
-                        int32_t* __restrict__ out_tok, int32_t* __restrict__ new_kv_len) {
+                        int32_t* __restrict__ out_tok, int32_t* __restrict__ new_kv_len, const CombineJob cj) {
   __shared__ double seg[kMaxSeg];
+  if ((int)blockIdx.x >= bt.nreq) {
+    combine_job_block(cj, blockIdx.x - bt.nreq, threadIdx.x);
+    return;
+  }
+  if (threadIdx.x >= kWave) return;
   const int b = blockIdx.x;
   const int req = bt.req0 + b;
   const int lane = threadIdx.x;
@@ -305,9 +323,20 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   const int nseg = a.nseg;
   const double* tot = a.segsum + (int64_t)req * nseg;
 
-  // Segment totals into LDS, 8 loads per lane in flight; l and u alongside.
+  // Segment totals into LDS, 8 loads per lane in flight; l and u alongside,
+  // and everything else that does not depend on them: the drafts to emit and
+  // each row's normaliser (lane j: row j), so that only the segment loads
+  // wait for the draw's position.
   const int l = accept_len[req];
   const float uu = a.u[(int64_t)req * G + a.gamma];
+  const bool tree = a.tree != nullptr;
+  const int my_draft = (!tree && lane < a.gamma) ? a.draft[(int64_t)req * a.gamma + lane] : -1;
+  float my_lse = 0.f;
+  WarpRow my_warp{1.f, 0u, 0.f, -1};
+  if (lane < G) {
+    if (a.warp != nullptr) my_warp = a.warp[(int64_t)req * G + lane];
+    else if (a.lse != nullptr) my_lse = a.lse[(int64_t)req * G + lane];
+  }
   for (int base = 0; base < nseg; base += 8 * kWave) {
     double v[8];
 #pragma unroll
@@ -318,12 +347,17 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   }
   // Chain: row l, residual after a rejection.  Tree: the walk's final row,
   // plain p without the candidates rejected there.
-  const bool tree = a.tree != nullptr;
   const int pos = tree ? a.tree[req].pos : l;
   const int nrej = tree ? a.tree[req].nrej : 0;
   const int rej = tree && lane < nrej ? a.tree[req].rej_tok[lane] : -1;
   const int64_t row = (int64_t)req * G + pos;
-  const RowP rp = row_p(a, row, a.lse != nullptr ? a.lse[row] : 0.f);
+  RowP rp{__shfl(my_lse, pos), 1.f, 0u, -1};
+  if (a.warp != nullptr) {
+    rp.lse = __shfl(my_warp.lse, pos);
+    rp.inv_t = __shfl(my_warp.inv_t, pos);
+    rp.theta = (uint32_t)__shfl((int)my_warp.theta, pos);
+    rp.argmax = __shfl(my_warp.argmax, pos);
+  }
   bool residual = !tree && l < a.gamma;
   const float* xrow = a.x + row * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
@@ -416,7 +450,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   }
   if (lane < G) {
     int32_t v = -1;
-    if (lane < l) v = a.draft[(int64_t)req * a.gamma + lane];
+    if (lane < l) v = my_draft;
     else if (lane == l) v = t;
     out_tok[(int64_t)req * G + lane] = v;
   }
@@ -518,7 +552,8 @@ size_t accept_workspace_bytes(int B, int V) {
 hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
                          const float2* partials, int ntiles, const float* q_draft, const int32_t* draft_tok,
                          const float* u, void* ws, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
-                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop, const WarpRow* warp) {
+                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop, const WarpRow* warp,
+                         const CombineJob* combine) {
   (void)B;
   if (bt.nreq <= 0) return hipSuccess;
   AcceptArgs a;
@@ -543,8 +578,11 @@ hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const f
                         0, a, bt, warp != nullptr ? nullptr : partials, ntiles, accept_len);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, nullptr, ev_stop, 0, a, bt,
-                        accept_len, out_tok, new_kv_len);
+  CombineJob cj;
+  memset(&cj, 0, sizeof(cj));
+  if (combine != nullptr) cj = *combine;
+  hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq + cj.nblocks), dim3(kCombineThreads), 0, stream, nullptr,
+                        ev_stop, 0, a, bt, accept_len, out_tok, new_kv_len, cj);
   return hipGetLastError();
 }
 
@@ -585,8 +623,10 @@ hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& bt, const 
                      (const float2*)nullptr, 0, accept_len);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, nullptr, ev_stop, 0, a, bt,
-                        accept_len, out_tok, new_kv_len);
+  CombineJob cj;
+  memset(&cj, 0, sizeof(cj));
+  hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq), dim3(kCombineThreads), 0, stream, nullptr, ev_stop, 0, a,
+                        bt, accept_len, out_tok, new_kv_len, cj);
   return hipGetLastError();
 }
 

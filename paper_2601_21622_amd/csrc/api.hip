@@ -7,7 +7,10 @@
 #include <algorithm>
 #include <cmath>
 
+#include <vector>
+
 #include "sdverify.h"
+#include "combine.h"
 #include "launch.h"
 
 namespace {
@@ -118,10 +121,12 @@ int hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
 
 // Enqueue attention (partials + combine) for all requests, in launches of at
 // most kMaxReqPerLaunch requests whose tables ride in the kernel arguments.
+// With `deferred`, the merges are not launched: one CombineJob per launch is
+// appended there instead, for a later launch to carry.
 int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* v, const int64_t* kv_off,
                   const int32_t* kv_len, float scale, void* out, void* ws, hipStream_t stream,
                   hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const uint64_t* anc = nullptr,
-                  const sd_kv_pages_t* pages = nullptr) {
+                  const sd_kv_pages_t* pages = nullptr, std::vector<CombineJob>* deferred = nullptr) {
   const AttnShape s = attn_shape(d, scale, kv_len, pages != nullptr ? pages->page_size : 0);
   const int64_t chunks = total_chunks(kv_len, d->batch, s.chunk_keys);
   const AttnPartials parts = attn_carve(ws, chunks, s.Hkv, s.rows, s.D);
@@ -150,8 +155,20 @@ int run_attention(const sd_dims_t* d, const void* q, const void* k, const void* 
     const bool first = r0 == 0, last = r0 + kMaxReqPerLaunch >= d->batch;
     hipError_t e = launch_attention(d->dtype, s, bt, acc, q, k, v, parts, stream, first ? ev_start : nullptr,
                                     last ? ev_stop : nullptr);
-    if (e == hipSuccess) e = launch_attention_combine(d->dtype, s, bt, parts, out, stream);
     if (e != hipSuccess) return SD_ERR_HIP;
+    if (deferred != nullptr) {
+      CombineJob cj;
+      memset(&cj, 0, sizeof(cj));
+      cj.s = s;
+      cj.bt = bt;
+      cj.parts = parts;
+      cj.out = out;
+      cj.bf16 = d->dtype == SD_DTYPE_BF16;
+      cj.nblocks = bt.nreq * s.Hkv * combine_zblocks(s);
+      deferred->push_back(cj);
+    } else if (launch_attention_combine(d->dtype, s, bt, parts, out, stream) != hipSuccess) {
+      return SD_ERR_HIP;
+    }
     chunk_base += acc;
   }
   return SD_OK;
@@ -172,7 +189,8 @@ int run_logits(const sd_dims_t* d, const void* hidden, const void* w, float* log
 int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const float2* partials, int ntiles,
                const float* q_draft, const int32_t* draft_tok, const float* u, const int32_t* kv_len,
                int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len, void* ws, hipStream_t stream,
-               hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const WarpRow* warp = nullptr) {
+               hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const WarpRow* warp = nullptr,
+               const std::vector<CombineJob>* merges = nullptr) {
   for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
     AcceptBatch bt;
     memset(&bt, 0, sizeof(bt));
@@ -182,9 +200,11 @@ int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const f
     if (kv_len != nullptr)
       for (int i = 0; i < bt.nreq; ++i) bt.kv_len[i] = kv_len[r0 + i];
     const bool first = r0 == 0, last = r0 + kMaxReqPerLaunch >= d->batch;
+    // Both stages split the batch into the same launches of kMaxReqPerLaunch requests.
+    const CombineJob* cj = merges != nullptr ? &(*merges)[r0 / kMaxReqPerLaunch] : nullptr;
     hipError_t e = launch_accept(d->gamma, d->vocab, d->batch, bt, x, row_lse, partials, ntiles, q_draft, draft_tok,
                                  u, ws, accept_len, out_tok, new_kv_len, stream, first ? ev_start : nullptr,
-                                 last ? ev_stop : nullptr, warp);
+                                 last ? ev_stop : nullptr, warp, cj);
     if (e != hipSuccess) return SD_ERR_HIP;
   }
   return SD_OK;
@@ -256,8 +276,8 @@ extern "C" {
 size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
   if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
   const int64_t chunks = attn_max_chunks(dims->dtype, dims->n_kv_heads, dims->batch, max_kv_len);
-  return std::max({tree_ws(dims) + attention_ws(dims, chunks), logits_ws(dims) + accept_stage_ws(dims),
-                   rate_ws(dims)});
+  return std::max({tree_ws(dims) + attention_ws(dims, chunks),
+                   attention_ws(dims, chunks) + logits_ws(dims) + accept_stage_ws(dims), rate_ws(dims)});
 }
 
 int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
@@ -399,31 +419,37 @@ int verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const 
   st = pages != nullptr ? check_pages(dims, pages, kv_len) : check_kv(dims, kv_off, kv_len);
   if (st != SD_OK) return st;
   const AttnShape s = attn_shape(dims, scale, kv_len, pages != nullptr ? pages->page_size : 0);
-  const size_t need = std::max(attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
-                               logits_ws(dims) + accept_stage_ws(dims));
+  const size_t attn_bytes = attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys));
+  // With the caller's hidden rows the projection does not read the attention
+  // output, so the attention merge rides in the acceptance's last launch and
+  // its partials keep their own region: [partials][projection][acceptance].
+  // Otherwise the stages reuse one region in stream order.
+  const bool defer = hidden != nullptr;
+  const size_t base = defer ? attn_bytes : 0;
+  const size_t need = defer ? attn_bytes + logits_ws(dims) + accept_stage_ws(dims)
+                            : std::max(attn_bytes, logits_ws(dims) + accept_stage_ws(dims));
   if (workspace_bytes < need) return SD_ERR_WORKSPACE;
 
   hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   if (kernel_events != nullptr)
     for (int i = 0; i < 6; ++i) ev[i] = static_cast<hipEvent_t>(kernel_events[i]);
   hipStream_t stm = static_cast<hipStream_t>(stream);
-  // Stream order serialises the stages, so they share one workspace: the
-  // attention partials are dead once the combine has run, the vocabulary
-  // statistics once the log-sum-exp combine has run.
+  std::vector<CombineJob> merges;
   st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out, workspace, stm, ev[0], ev[1],
-                     nullptr, pages);
+                     nullptr, pages, defer ? &merges : nullptr);
   if (st != SD_OK) return st;
-  // The vocabulary statistics live at the start of the workspace and the
-  // acceptance sums after them, since the fold reads the former while the
-  // segment kernel writes the latter.
+  // The vocabulary statistics come first in their region and the acceptance
+  // sums after them, since the fold reads the former while the segment kernel
+  // writes the latter.
+  void* vws = static_cast<char*>(workspace) + base;
   const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab, (dims->flags & SD_FLAG_PACKED_VOCAB) != 0);
-  float2* partials = static_cast<float2*>(workspace);
-  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, workspace, stm, ev[2],
+  float2* partials = static_cast<float2*>(vws);
+  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, vws, stm, ev[2],
                    ev[3]) != hipSuccess)
     return SD_ERR_HIP;
-  void* acc_ws = static_cast<char*>(workspace) + logits_ws(dims);
+  void* acc_ws = static_cast<char*>(vws) + logits_ws(dims);
   return run_accept(dims, logits, row_lse, partials, vp.ntiles, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
-                    new_kv_len, acc_ws, stm, ev[4], ev[5]);
+                    new_kv_len, acc_ws, stm, ev[4], ev[5], nullptr, defer ? &merges : nullptr);
 }
 
 }  // namespace

@@ -28,6 +28,7 @@
 // pieces so that the fragment reads are free of bank conflicts.
 #include <hip/hip_ext.h>
 
+#include "combine.h"
 #include "common.h"
 #include "launch.h"
 
@@ -587,48 +588,11 @@ void attn_f32_kernel(const AttnShape s, const AttnBatch bt, const float* __restr
   }
 }
 
+// Standalone merge: grid (requests, KV heads, combine blocks per pair).
 template <typename OutT>
-__device__ __forceinline__ void store_out(OutT* p, float v);
-template <>
-__device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
-template <>
-__device__ __forceinline__ void store_out<uint16_t>(uint16_t* p, float v) {
-  *p = __builtin_bit_cast(uint16_t, (__bf16)v);
-}
-
-// Merge the chunk partials of one (request, KV head) in chunk order.  One
-// thread per (row, 4 consecutive d); chunk loads are unrolled so they are in
-// flight together.
-template <typename OutT>
-__global__ __launch_bounds__(kAttnThreads)
+__global__ __launch_bounds__(kCombineThreads)
 void attn_combine_kernel(const AttnShape s, const AttnBatch bt, AttnPartials parts, OutT* __restrict__ out) {
-  const int b = blockIdx.x;
-  const int g = blockIdx.y;
-  const int req = bt.req0 + b;
-  const int c0 = bt.chunk_base + bt.chunk_prefix[b];
-  const int c1 = bt.chunk_base + bt.chunk_prefix[b + 1];
-  const int D4 = s.D / 4;
-  const int i = blockIdx.z * kAttnThreads + threadIdx.x;
-  if (i >= s.rows * D4) return;
-  const int row = i / D4, d = (i - row * D4) * 4;
-  float mx = kNegBig;
-#pragma unroll 8
-  for (int c = c0; c < c1; ++c) mx = fmaxf(mx, parts.m[((int64_t)c * s.Hkv + g) * s.rows + row]);
-  float den = 0.f;
-  f32x4 num = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int c = c0; c < c1; ++c) {
-    const int64_t slot = (int64_t)c * s.Hkv + g;
-    const float a = exp2f(parts.m[slot * s.rows + row] - mx);
-    den = fmaf(a, parts.l[slot * s.rows + row], den);
-    const f32x4 o = *reinterpret_cast<const f32x4*>(parts.o + (slot * s.rows + row) * s.D + d);
-    num += a * o;
-  }
-  const int j = row / s.group;
-  const int h = g * s.group + (row - j * s.group);
-  OutT* dst = out + (((int64_t)req * s.G + j) * s.Hq + h) * s.D + d;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) store_out(dst + e, num[e] / den);
+  combine_block<OutT>(s, bt, parts, out, blockIdx.x, blockIdx.y, blockIdx.z, threadIdx.x);
 }
 
 template <int RB, int D, bool TREE, bool PAGED>
@@ -801,12 +765,12 @@ hipError_t launch_attention(int dtype, const AttnShape& s, const AttnBatch& bt, 
 hipError_t launch_attention_combine(int dtype, const AttnShape& s, const AttnBatch& bt,
                                     AttnPartials parts, void* out, hipStream_t stream) {
   if (bt.nreq <= 0) return hipSuccess;
-  const dim3 grid(bt.nreq, s.Hkv, (s.rows * (s.D / 4) + kAttnThreads - 1) / kAttnThreads);
+  const dim3 grid(bt.nreq, s.Hkv, combine_zblocks(s));
   if (dtype == 0)
-    hipLaunchKernelGGL(attn_combine_kernel<float>, grid, dim3(kAttnThreads), 0, stream, s, bt, parts,
+    hipLaunchKernelGGL(attn_combine_kernel<float>, grid, dim3(kCombineThreads), 0, stream, s, bt, parts,
                        static_cast<float*>(out));
   else
-    hipLaunchKernelGGL(attn_combine_kernel<uint16_t>, grid, dim3(kAttnThreads), 0, stream, s, bt, parts,
+    hipLaunchKernelGGL(attn_combine_kernel<uint16_t>, grid, dim3(kCombineThreads), 0, stream, s, bt, parts,
                        static_cast<uint16_t*>(out));
   return hipGetLastError();
 }

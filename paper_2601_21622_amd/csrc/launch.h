@@ -124,12 +124,14 @@ size_t accept_workspace_bytes(int B, int V);
 // segment-sum kernel.
 // With `warp` (one WarpRow per row, from launch_warp) x holds logits and the
 // test and correction use the warped p'; row_lse and partials are then unused.
+// With `combine`, the pick launch also carries that attention merge.
+struct CombineJob;
 hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& batch, const float* x,
                          const float* row_lse, const float2* partials, int ntiles,
                          const float* q_draft, const int32_t* draft_tok, const float* u, void* ws,
                          int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
                          hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop,
-                         const WarpRow* warp = nullptr);
+                         const WarpRow* warp = nullptr, const CombineJob* combine = nullptr);
 
 // Tree verification (N = gamma nodes, position 0 the root, position i + 1 node
 // i): walk the candidate tree, then draw the final token.  ws holds
