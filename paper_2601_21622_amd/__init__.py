@@ -28,6 +28,7 @@ from ._binding import (  # noqa: F401
     exported_symbols,
     library,
     library_path,
+    prepare_acceptance_rate,
     prepare_verify_step,
     prepare_verify_step_paged,
     prepare_verify_step_sampled,

@@ -301,10 +301,19 @@ def sd_tree_commit_kv(dims: Dims, k_pool, v_pool, kv_off, kv_len, out_node, acce
     _check(st, "sd_tree_commit_kv")
 
 
+def _rate_args(dims, logits_or_probs, row_lse, q_draft, beta, workspace, stream=None):
+    return (ctypes.byref(dims), _ptr(logits_or_probs), _ptr(row_lse), _ptr(q_draft), _ptr(beta), _ptr(workspace),
+            _nbytes(workspace), _stream(stream))
+
+
 def sd_acceptance_rate(dims: Dims, logits_or_probs, row_lse, q_draft, beta, workspace, stream=None) -> None:
-    st = library().sd_acceptance_rate(ctypes.byref(dims), _ptr(logits_or_probs), _ptr(row_lse), _ptr(q_draft),
-                                      _ptr(beta), _ptr(workspace), _nbytes(workspace), _stream(stream))
-    _check(st, "sd_acceptance_rate")
+    _check(library().sd_acceptance_rate(*_rate_args(dims, logits_or_probs, row_lse, q_draft, beta, workspace, stream)),
+           "sd_acceptance_rate")
+
+
+def prepare_acceptance_rate(*a, **kw) -> "PreparedCall":
+    """sd_acceptance_rate with the same arguments, converted once (see PreparedCall)."""
+    return PreparedCall(library().sd_acceptance_rate, _rate_args(*a, **kw), (a, kw), "sd_acceptance_rate")
 
 
 def sd_expand_layer(e: Expand, draft_logits, tokens, parent, q_child, stream=None) -> None:
