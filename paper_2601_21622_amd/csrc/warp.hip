@@ -35,6 +35,7 @@ namespace {
 constexpr int kWarpThreads = 1024;
 constexpr int kWarpWaves = kWarpThreads / kWave;
 constexpr int kBuckets = 2048;
+constexpr int kCand = 2048;  // candidates the small-k path can hold
 
 __device__ __forceinline__ float key_value(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
@@ -49,6 +50,62 @@ __device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v,
   const uint32_t lo = __shfl_xor((uint32_t)v, mask);
   const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), mask);
   return ((unsigned long long)hi << 32) | lo;
+}
+
+// Bitonic sort of one 64-bit key per lane across the wave, largest first.
+__device__ __forceinline__ unsigned long long wave_sort_desc(unsigned long long v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int size = 2; size <= kWave; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const unsigned long long o = shfl_xor_u64(v, stride);
+      const bool desc = (lane & size) == 0 || size == kWave;
+      const bool lower = (lane & stride) == 0;
+      v = (lower == desc) ? (o > v ? o : v) : (o < v ? o : v);
+    }
+  }
+  return v;
+}
+
+// The 64 largest of two lists sorted largest first, sorted largest first: the
+// lane-wise maximum of one list and the other reversed is bitonic and holds
+// them; a bitonic merge orders it.
+__device__ __forceinline__ unsigned long long wave_merge_desc(unsigned long long a, unsigned long long b) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t lo = __shfl((uint32_t)b, kWave - 1 - lane);
+  const uint32_t hi = __shfl((uint32_t)(b >> 32), kWave - 1 - lane);
+  const unsigned long long br = ((unsigned long long)hi << 32) | lo;
+  unsigned long long v = a > br ? a : br;
+#pragma unroll
+  for (int stride = kWave >> 1; stride > 0; stride >>= 1) {
+    const unsigned long long o = shfl_xor_u64(v, stride);
+    v = ((lane & stride) == 0) ? (o > v ? o : v) : (o < v ? o : v);
+  }
+  return v;
+}
+
+__device__ __forceinline__ unsigned long long shfl_u64(unsigned long long v, int src) {
+  const uint32_t lo = __shfl((uint32_t)v, src);
+  const uint32_t hi = __shfl((uint32_t)(v >> 32), src);
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ __forceinline__ unsigned long long wave_inclusive_scan_u64(unsigned long long v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t lo = __shfl_up((uint32_t)v, off);
+    const uint32_t hi = __shfl_up((uint32_t)(v >> 32), off);
+    if (lane >= off) v += ((unsigned long long)hi << 32) | lo;
+  }
+  return v;
+}
+
+// Rank key of an entry: the float32 order key, then the inverted index, so
+// that equal logits rank by increasing index and keys are unique (0: none).
+__device__ __forceinline__ unsigned long long entry_key(uint32_t k, int v) {
+  return ((unsigned long long)k << 32) | (unsigned long long)(0xffffffffu - (uint32_t)v);
 }
 
 // Calls f(v, x[v]) for every element of the row, this thread's share, with
@@ -169,6 +226,10 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
   __shared__ uint32_t s_kmax, s_bucket, s_cnt_above;
   __shared__ int s_amax;
   __shared__ unsigned long long s_mass_above, s_total;
+  __shared__ unsigned long long s_list[kWarpWaves][kWave];
+  __shared__ unsigned long long s_cand[kCand];
+  __shared__ uint32_t s_n, s_bound, s_theta, s_pdone;
+  __shared__ unsigned long long s_w;
 
   const int row = blockIdx.x;
   const float* x = logits + (int64_t)row * V;
@@ -186,6 +247,7 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
   uint32_t bk = 0;
   int bi = 0x7fffffff;
   row_pass(x, V, [&](int v, float xv) { merge(bk, bi, order_key(xv), v); });
+  const unsigned long long tkey = bi == 0x7fffffff ? 0ull : entry_key(bk, bi);  // this thread's best entry
   for (int off = 32; off >= 1; off >>= 1) merge(bk, bi, __shfl_xor(bk, off), __shfl_xor(bi, off));
   if (lane == 0) {
     w_key[wave] = bk;
@@ -214,7 +276,86 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
   // Mass of the whole row (no top-k), or of the top-k set.
   uint32_t theta = 0;
   unsigned long long W = 0;
-  if (top_k >= 1 && top_k < V) {
+  bool have_k = false, have_p = false;
+  if (top_k >= 1 && top_k <= kWave && top_k < V) {
+    // Small k: the k-th largest of the threads' best entries bounds the k-th
+    // largest logit from below (k threads reach it), so the entries at or
+    // above it hold the top-k set and all its ties.  They are collected in
+    // LDS and wave 0 sorts them in 64-key batches.
+    s_list[wave][lane] = wave_sort_desc(tkey);
+    __syncthreads();
+    if (wave == 0) {
+      unsigned long long acc = s_list[0][lane];
+      for (int w = 1; w < kWarpWaves; ++w) acc = wave_merge_desc(acc, s_list[w][lane]);
+      const unsigned long long kth = shfl_u64(acc, top_k - 1);
+      if (lane == 0) {
+        s_bound = (uint32_t)(kth >> 32);
+        s_n = 0;
+      }
+    }
+    __syncthreads();
+    const uint32_t bound = s_bound;
+    row_pass(x, V, [&](int v, float xv) {
+      const uint32_t k = order_key(xv);
+      if (k >= bound) {
+        const uint32_t i = atomicAdd(&s_n, 1u);
+        if (i < (uint32_t)kCand) s_cand[i] = entry_key(k, v);
+      }
+    });
+    __syncthreads();
+    const uint32_t n = s_n;
+    if (n <= (uint32_t)kCand) {  // otherwise (masses of ties at the bound) the radix descent below
+      if (wave == 0) {
+        unsigned long long lst = 0;
+        for (uint32_t base = 0; base < n; base += kWave)
+          lst = wave_merge_desc(lst, wave_sort_desc(base + lane < n ? s_cand[base + lane] : 0ull));
+        const uint32_t thk = (uint32_t)(shfl_u64(lst, top_k - 1) >> 32);
+        // The kept set: every candidate whose key reaches the k-th (ties kept).
+        uint32_t cnt = 0;
+        unsigned long long ms = 0;
+        for (uint32_t i = lane; i < n; i += kWave) {
+          const uint32_t k = (uint32_t)(s_cand[i] >> 32);
+          if (k >= thk) {
+            ++cnt;
+            ms += fixed_mass(key_value(k), m, inv_t, scale);
+          }
+        }
+        for (int off = 32; off >= 1; off >>= 1) {
+          cnt += __shfl_xor(cnt, off);
+          ms += shfl_xor_u64(ms, off);
+        }
+        uint32_t th = thk;
+        unsigned long long w = ms;
+        bool pdone = false;
+        if (top_p < 1.f && cnt <= (uint32_t)kWave) {
+          // Lanes [0, cnt) of the sorted list are the kept set, largest first:
+          // the cut is the first key whose running mass reaches the target.
+          unsigned long long target = (unsigned long long)ceil((double)top_p * (double)ms);
+          target = target < 1 ? 1 : (target > ms ? ms : target);
+          const uint32_t lk = (uint32_t)(lst >> 32);
+          const unsigned long long cum =
+              wave_inclusive_scan_u64(lane < (int)cnt ? fixed_mass(key_value(lk), m, inv_t, scale) : 0ull);
+          const int i = __ffsll(__ballot(lane < (int)cnt && cum >= target)) - 1;
+          th = __shfl(lk, i);
+          const int c = __popcll(__ballot(lane < (int)cnt && lk >= th));
+          w = shfl_u64(cum, c - 1);
+          pdone = true;
+        }
+        if (lane == 0) {
+          s_theta = th;
+          s_w = w;
+          s_pdone = pdone;
+        }
+      }
+      __syncthreads();
+      theta = s_theta;
+      W = s_w;
+      have_k = true;
+      have_p = s_pdone != 0;
+    }
+  }
+  if (have_k) {
+  } else if (top_k >= 1 && top_k < V) {
     uint32_t prefix = 0, krem = (uint32_t)top_k;
     unsigned long long above = 0;
     for (int level = 0; level < 3; ++level) {
@@ -258,7 +399,7 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
     W = s_total;
   }
 
-  if (top_p < 1.f) {
+  if (top_p < 1.f && !have_p) {
     unsigned long long target = (unsigned long long)ceil((double)top_p * (double)W);
     target = target < 1 ? 1 : (target > W ? W : target);
     uint32_t prefix = 0;

@@ -45,11 +45,17 @@ SHAPES = {
 }
 
 
-def _inputs(B, gamma, V, T, k, p, seed):
-    """Target logits, warped draft distributions and drafts drawn from them."""
+def _inputs(B, gamma, V, T, k, p, seed, levels=None):
+    """Target logits, warped draft distributions and drafts drawn from them;
+    with ``levels``, the target logits are rounded onto that many steps of
+    their range, so that large sets of them tie."""
     rng = np.random.default_rng(seed)
     G = gamma + 1
     logits = (rng.standard_normal((B * G, V)) * 2.0).astype(np.float32)
+    if levels is not None:
+        lo, hi = float(logits.min()), float(logits.max())
+        step = (hi - lo) / levels
+        logits = (np.round((logits - lo) / step) * step + lo).astype(np.float32)
     q = np.empty((B, gamma, V), dtype=np.float32)
     draft = np.empty((B, gamma), dtype=np.int32)
     for b in range(B):
@@ -147,6 +153,39 @@ def test_sampled_step_matches_oracle():
                                   cut=_gpu_cut(logits, T, g_lse, g_min))
     near = assert_accept_parity(to_np(db.accept_len), to_np(db.out_tok), to_np(db.new_kv_len), ref)
     announce(f"sampled step: requests in band {near}")
+
+
+@pytest.mark.parametrize("levels,k,p", [(3, 40, 0.9), (12, 40, 0.9), (12, 64, 1.0), (3000, 64, 0.5)])
+def test_sampled_ties_match_oracle(levels, k, p):
+    """Target logits on a few levels, so that the cut falls inside a large
+    tie: kept sets above 64 entries (the top-p cut by radix descent) and
+    candidate sets above 2048 (the top-k cut by radix descent) as well as the
+    small-k selection."""
+    B, gamma, V = 4, 3, 32000
+    T = 0.9
+    G = gamma + 1
+    announce(f"sampled ties case levels={levels} k={k} p={p} B={B} gamma={gamma} V={V}")
+    logits, q, draft, u = _inputs(B, gamma, V, T, k, p, seed=levels * 131 + k, levels=levels)
+    kv_len = np.full(B, 100, dtype=np.int32)
+    cfg = get_config("tiny").replace(batch=B, gamma=gamma, vocab=V)
+    dims = sd.Dims.of(cfg)
+    dev = "cuda"
+    lse = torch.empty(B * G, dtype=torch.float32, device=dev)
+    mn = torch.empty(B * G, dtype=torch.float32, device=dev)
+    acc = torch.empty(B, dtype=torch.int32, device=dev)
+    tok = torch.empty((B, G), dtype=torch.int32, device=dev)
+    new = torch.empty(B, dtype=torch.int32, device=dev)
+    ws = torch.empty(sd.sd_workspace_bytes(dims, 100), dtype=torch.uint8, device=dev)
+    sd.sd_accept_resample_sampled(dims, sd.Sampling(T, k, p), torch.from_numpy(logits).to(dev),
+                                  torch.from_numpy(q).to(dev), torch.from_numpy(draft).to(dev),
+                                  torch.from_numpy(u).to(dev), kv_len, lse, mn, acc, tok, new, ws)
+    torch.cuda.synchronize()
+    g_lse, g_min = to_np(lse), to_np(mn)
+    _check_cut(logits, T, k, p, g_lse, g_min)
+    ref = accept_resample_sampled(logits, q, draft, u, T, k, p, kv_len, cut=_gpu_cut(logits, T, g_lse, g_min))
+    assert_accept_parity(to_np(acc), to_np(tok), to_np(new), ref)
+    kept = [int(np.sum(logits[r] >= g_min[r])) for r in range(B * G)]
+    announce(f"ties levels={levels} k={k} p={p}: kept set sizes {min(kept)}..{max(kept)}")
 
 
 def test_sampled_accept_is_deterministic():
