@@ -165,7 +165,9 @@ __device__ __forceinline__ double segment_total(const float (&r)[kPerLane]) {
 }
 
 // Totals of segments [sg0, sg1) into out[]: wave w takes sg0 + w, sg0 + w +
-// nwaves, ..., issuing the loads of kSegBatch segments before reducing any.
+// nwaves, ..., issuing the loads of up to kSegBatch segments before reducing
+// any.  Batch entries past sg1 are skipped (wave-uniform), so a wave with a
+// single segment issues and reduces only that one.
 template <int PM, bool RES>
 __device__ __forceinline__ void segment_totals_t(const float* xrow, const float* qrow, const RowP& rp, int V, int sg0,
                                                  int sg1, int nwaves, double* out) {
@@ -174,14 +176,16 @@ __device__ __forceinline__ void segment_totals_t(const float* xrow, const float*
   for (int s0 = sg0 + wave; s0 < sg1; s0 += nwaves * kSegBatch) {
     float xs[kSegBatch][kPerLane], qs[kSegBatch][kPerLane];
 #pragma unroll
-    for (int k = 0; k < kSegBatch; ++k) segment_issue<RES>(xrow, qrow, V, min(s0 + k * nwaves, sg1 - 1), xs[k], qs[k]);
+    for (int k = 0; k < kSegBatch; ++k)
+      if (s0 + k * nwaves < sg1) segment_issue<RES>(xrow, qrow, V, s0 + k * nwaves, xs[k], qs[k]);
 #pragma unroll
     for (int k = 0; k < kSegBatch; ++k) {
       const int sg = s0 + k * nwaves;
+      if (sg >= sg1) break;
       float r[kPerLane];
       segment_finish<PM, RES>(rp, V, sg, xs[k], qs[k], r);
       const double t = segment_total(r);
-      if (lane == 0 && sg < sg1) out[sg] = t;
+      if (lane == 0) out[sg] = t;
     }
   }
 }
