@@ -233,10 +233,14 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
     return;
   }
 
-  // 1. Test operands first, then the row log-sum-exp fold.
+  // 1. Test operands (gathered by the last wave, whose second load waits on
+  // the draft tokens), and the row log-sum-exp folds (row j on wave j mod
+  // kSumWaves, so the last wave folds none while gamma + 1 < kSumWaves and
+  // the other waves' partial loads issue at once).
+  constexpr int kTestWave = kSumWaves - 1;
   float xv = 0.f, qv = 0.f, uv = 0.f;
   bool valid = false;
-  if (wave == 0 && lane < a.gamma) {
+  if (wave == kTestWave && lane < a.gamma) {
     const int tok = a.draft[(int64_t)req * a.gamma + lane];
     valid = tok >= 0 && tok < a.V;
     if (valid) {
@@ -262,7 +266,7 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
   __syncthreads();
 
   // 2. Ratio tests in float64; l = number of leading accepts.
-  if (wave == 0) {
+  if (wave == kTestWave) {
     bool fail = false;
     if (lane < a.gamma) {
       double ratio = 0.0;

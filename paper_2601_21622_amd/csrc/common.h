@@ -85,36 +85,81 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Cross-lane moves inside rows of 16 lanes (DPP; GFX9 control codes) and
+// reads of single lanes.  The wave reductions and the scan below are built
+// from them rather than from LDS-routed shuffles (ds_bpermute), which cost an
+// LDS round trip per step on the latency-bound paths.  The order of
+// operations is fixed, and every lane of a reduction ends with the same bits
+// (pairs are combined commutatively inside a row, and the four row results
+// are read into scalars and combined once).
+constexpr int kDppXor1 = 0xB1;           // quad_perm [1,0,3,2]: lane i <- i ^ 1
+constexpr int kDppXor2 = 0x4E;           // quad_perm [2,3,0,1]: lane i <- i ^ 2
+constexpr int kDppRowHalfMirror = 0x141;  // lane i <- 7 - i within each 8 lanes
+constexpr int kDppRowMirror = 0x140;      // lane i <- 15 - i within each row
+constexpr int kDppRowShr = 0x110;         // + n: lane i <- i - n inside the row, 0 before its start
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __builtin_bit_cast(float, dpp_u32<CTRL>(__builtin_bit_cast(uint32_t, v)));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint64_t lo = dpp_u32<CTRL>((uint32_t)b), hi = dpp_u32<CTRL>((uint32_t)(b >> 32));
+  return __builtin_bit_cast(double, (hi << 32) | lo);
+}
+__device__ __forceinline__ float lane_f32(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+__device__ __forceinline__ double lane_f64(double v, int l) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
+  return __builtin_bit_cast(double, (hi << 32) | lo);
+}
+
+// Reductions over the 64 lanes of a wave; every lane must be active.
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  v = fmaxf(v, dpp_f32<kDppXor1>(v));
+  v = fmaxf(v, dpp_f32<kDppXor2>(v));
+  v = fmaxf(v, dpp_f32<kDppRowHalfMirror>(v));
+  v = fmaxf(v, dpp_f32<kDppRowMirror>(v));
+  return fmaxf(fmaxf(lane_f32(v, 0), lane_f32(v, 16)), fmaxf(lane_f32(v, 32), lane_f32(v, 48)));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v += dpp_f32<kDppXor1>(v);
+  v += dpp_f32<kDppXor2>(v);
+  v += dpp_f32<kDppRowHalfMirror>(v);
+  v += dpp_f32<kDppRowMirror>(v);
+  return (lane_f32(v, 0) + lane_f32(v, 16)) + (lane_f32(v, 32) + lane_f32(v, 48));
 }
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v += dpp_f64<kDppXor1>(v);
+  v += dpp_f64<kDppXor2>(v);
+  v += dpp_f64<kDppRowHalfMirror>(v);
+  v += dpp_f64<kDppRowMirror>(v);
+  return (lane_f64(v, 0) + lane_f64(v, 16)) + (lane_f64(v, 32) + lane_f64(v, 48));
 }
 
-// Inclusive prefix sum across the 64 lanes (Hillis-Steele, fixed order).
+// Inclusive prefix sum across the 64 lanes, fixed order: Hillis-Steele inside
+// each row of 16, then the totals of the rows before are added.
 __device__ __forceinline__ double wave_inclusive_scan_f64(double v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    double n = __shfl_up(v, o);
-    if (lane >= o) v += n;
-  }
-  return v;
+  v += dpp_f64<kDppRowShr + 1>(v);
+  v += dpp_f64<kDppRowShr + 2>(v);
+  v += dpp_f64<kDppRowShr + 4>(v);
+  v += dpp_f64<kDppRowShr + 8>(v);
+  const double t0 = lane_f64(v, 15), t1 = lane_f64(v, 31), t2 = lane_f64(v, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  const double before = row == 0 ? 0.0 : (row == 1 ? t0 : (row == 2 ? t0 + t1 : (t0 + t1) + t2));
+  return row == 0 ? v : v + before;
 }
 
-// Wait for this wave's outstanding LDS operations (wave-private LDS staging).
 __device__ __forceinline__ void lds_wait() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
@@ -148,8 +193,8 @@ __device__ __forceinline__ void lds_barrier() {
 // float64, lse = m + log(sum).  Each lane holds tiles lane, lane + 64, ...;
 // loads take clamped indexes and masks so a round of kR per lane is in flight
 // at once (rows of up to kR * 64 tiles are read once), the lane sums are added
-// by a fixed butterfly and lane 0's value is broadcast, so the result is
-// deterministic and every lane returns the same bits.  ntiles >= 1.
+// by the fixed-order wave reduction, so the result is deterministic and
+// every lane returns the same bits.  ntiles >= 1.
 __device__ __forceinline__ float row_lse_from_partials(const float2* p, int ntiles) {
   const int lane = threadIdx.x & 63;
   constexpr int kR = 16;  // tiles per lane held in registers per round
@@ -176,8 +221,7 @@ __device__ __forceinline__ float row_lse_from_partials(const float2* p, int ntil
     for (int j = 0; j < kR; ++j) s += (double)v[j].y * (double)expf(v[j].x - mx);
   }
   s = wave_sum_f64(s);
-  const float r = (float)((double)mx + log(s));
-  return __shfl(r, 0);
+  return (float)((double)mx + log(s));  // mx and s are the same on every lane
 }
 
 }  // namespace sdv
