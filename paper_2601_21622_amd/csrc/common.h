@@ -112,6 +112,16 @@ __device__ __forceinline__ double dpp_f64(double v) {
   const uint64_t lo = dpp_u32<CTRL>((uint32_t)b), hi = dpp_u32<CTRL>((uint32_t)(b >> 32));
   return __builtin_bit_cast(double, (hi << 32) | lo);
 }
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+  const uint64_t lo = dpp_u32<CTRL>((uint32_t)v), hi = dpp_u32<CTRL>((uint32_t)(v >> 32));
+  return (hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return (hi << 32) | lo;
+}
 __device__ __forceinline__ float lane_f32(float v, int l) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
 }
@@ -155,9 +165,27 @@ __device__ __forceinline__ double wave_inclusive_scan_f64(double v) {
   v += dpp_f64<kDppRowShr + 4>(v);
   v += dpp_f64<kDppRowShr + 8>(v);
   const double t0 = lane_f64(v, 15), t1 = lane_f64(v, 31), t2 = lane_f64(v, 47);
+  // Rows before this lane's, without branches (as in the integer scan): the
+  // 0/1 factors are exact, so row r adds ((t0 + t1) + t2) truncated to its
+  // first r terms, and row 0 adds +0.
   const int row = (threadIdx.x & 63) >> 4;
-  const double before = row == 0 ? 0.0 : (row == 1 ? t0 : (row == 2 ? t0 + t1 : (t0 + t1) + t2));
-  return row == 0 ? v : v + before;
+  const double before = (t0 * (double)(row > 0) + t1 * (double)(row > 1)) + t2 * (double)(row > 2);
+  return v + before;
+}
+
+// Inclusive prefix sum of 64-bit integers across the 64 lanes (exact, so the
+// order does not matter): inside each row of 16, then the rows before.
+__device__ __forceinline__ uint64_t wave_inclusive_scan_u64(uint64_t v) {
+  v += dpp_u64<kDppRowShr + 1>(v);
+  v += dpp_u64<kDppRowShr + 2>(v);
+  v += dpp_u64<kDppRowShr + 4>(v);
+  v += dpp_u64<kDppRowShr + 8>(v);
+  const uint64_t t0 = lane_u64(v, 15), t1 = lane_u64(v, 31), t2 = lane_u64(v, 47);
+  // Rows before this lane's, without branches: divergent control flow here
+  // would put an exec-mask change between this scan and the next DPP move.
+  const int row = (threadIdx.x & 63) >> 4;
+  const uint64_t m1 = 0ull - (uint64_t)(row > 0), m2 = 0ull - (uint64_t)(row > 1), m3 = 0ull - (uint64_t)(row > 2);
+  return v + ((t0 & m1) + (t1 & m2) + (t2 & m3));
 }
 
 __device__ __forceinline__ void lds_wait() {

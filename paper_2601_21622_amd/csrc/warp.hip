@@ -91,17 +91,6 @@ __device__ __forceinline__ unsigned long long shfl_u64(unsigned long long v, int
   return ((unsigned long long)hi << 32) | lo;
 }
 
-__device__ __forceinline__ unsigned long long wave_inclusive_scan_u64(unsigned long long v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const uint32_t lo = __shfl_up((uint32_t)v, off);
-    const uint32_t hi = __shfl_up((uint32_t)(v >> 32), off);
-    if (lane >= off) v += ((unsigned long long)hi << 32) | lo;
-  }
-  return v;
-}
-
 // Rank key of an entry: the float32 order key, then the inverted index, so
 // that equal logits rank by increasing index and keys are unique (0: none).
 __device__ __forceinline__ unsigned long long entry_key(uint32_t k, int v) {
@@ -170,45 +159,44 @@ __device__ __forceinline__ Level level_of(int level) {
 // Wave 0: scanning the buckets from the top, the first bucket at which the
 // running total (of counts, or of masses with BY_MASS) reaches `need`, and the
 // count and mass of the buckets above it.  need >= 1 and the buckets hold at
-// least `need` in total.
+// least `need` in total (otherwise the lowest bucket is returned).  Lane l
+// totals the l-th group of nb/64 buckets from the top (reading them in a
+// lane-rotated order, so the lanes hit different LDS banks); a wave scan and
+// a ballot find the group, and the same inside the group finds the bucket.
 template <bool BY_MASS>
 __device__ void select_bucket(const uint32_t* hcnt, const unsigned long long* hmass, int nb, unsigned long long need,
-                              uint32_t* lcnt, unsigned long long* lmass, uint32_t* s_bucket, uint32_t* s_cnt_above,
-                              unsigned long long* s_mass_above) {
+                              uint32_t* s_bucket, uint32_t* s_cnt_above, unsigned long long* s_mass_above) {
   const int lane = threadIdx.x & 63;
-  const int per = nb / kWave;
+  const int per = nb / kWave;  // 32 or 16: a power of two
   const int top = nb - 1 - lane * per;
-  uint32_t c = 0;
-  unsigned long long ms = 0;
+  uint64_t c = 0, ms = 0;
   for (int i = 0; i < per; ++i) {
-    c += hcnt[top - i];
-    ms += hmass[top - i];
+    const int b = top - ((i + lane) & (per - 1));
+    c += hcnt[b];
+    ms += hmass[b];
   }
-  lcnt[lane] = c;
-  lmass[lane] = ms;
-  lds_wait();
+  const uint64_t inc_c = wave_inclusive_scan_u64(c), inc_m = wave_inclusive_scan_u64(ms);
+  const unsigned long long hit = __ballot((BY_MASS ? inc_m : inc_c) >= need);
+  const int L = hit ? __ffsll(hit) - 1 : kWave - 1;
+  const uint64_t c_above = lane_u64(inc_c, L) - lane_u64(c, L);
+  const uint64_t m_above = lane_u64(inc_m, L) - lane_u64(ms, L);
+  // Inside group L: lane i < per takes bucket nb - 1 - L*per - i.
+  // Loads clamped rather than predicated, and every lane read taken before
+  // the store, so no divergent branch sits between the scans and their reads.
+  const int b = max(nb - 1 - L * per - lane, 0);
+  const uint64_t in_group = 0ull - (uint64_t)(lane < per);
+  const uint64_t cb = (uint64_t)hcnt[b] & in_group;
+  const uint64_t mb = (uint64_t)hmass[b] & in_group;
+  const uint64_t ic = wave_inclusive_scan_u64(cb), im = wave_inclusive_scan_u64(mb);
+  const unsigned long long hit2 = __ballot(lane < per - 1 && (BY_MASS ? m_above + im : c_above + ic) >= need);
+  const int I = hit2 ? __ffsll(hit2) - 1 : per - 1;
+  const uint32_t bucket = (uint32_t)(nb - 1 - L * per - I);
+  const uint32_t cnt_above = (uint32_t)(c_above + lane_u64(ic, I) - lane_u64(cb, I));
+  const uint64_t mass_above = m_above + lane_u64(im, I) - lane_u64(mb, I);
   if (lane == 0) {
-    uint32_t cnt_run = 0;
-    unsigned long long mass_run = 0;
-    int L = 0;
-    for (; L < kWave - 1; ++L) {
-      const unsigned long long v = BY_MASS ? lmass[L] : (unsigned long long)lcnt[L];
-      const unsigned long long run = BY_MASS ? mass_run : (unsigned long long)cnt_run;
-      if (run + v >= need) break;
-      cnt_run += lcnt[L];
-      mass_run += lmass[L];
-    }
-    int b = nb - 1 - L * per;
-    for (int i = 0; i < per - 1; ++i, --b) {
-      const unsigned long long v = BY_MASS ? hmass[b] : (unsigned long long)hcnt[b];
-      const unsigned long long run = BY_MASS ? mass_run : (unsigned long long)cnt_run;
-      if (run + v >= need) break;
-      cnt_run += hcnt[b];
-      mass_run += hmass[b];
-    }
-    *s_bucket = (uint32_t)b;
-    *s_cnt_above = cnt_run;
-    *s_mass_above = mass_run;
+    *s_bucket = bucket;
+    *s_cnt_above = cnt_above;
+    *s_mass_above = mass_above;
   }
 }
 
@@ -218,8 +206,6 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
                  float* __restrict__ row_min_logit) {
   __shared__ uint32_t hcnt[kBuckets];
   __shared__ unsigned long long hmass[kBuckets];
-  __shared__ uint32_t lcnt[kWave];
-  __shared__ unsigned long long lmass[kWave];
   __shared__ uint32_t w_key[kWarpWaves];
   __shared__ int w_idx[kWarpWaves];
   __shared__ unsigned long long w_sum[kWarpWaves];
@@ -374,7 +360,7 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
         }
       });
       __syncthreads();
-      if (wave == 0) select_bucket<false>(hcnt, hmass, lv.nb, krem, lcnt, lmass, &s_bucket, &s_cnt_above, &s_mass_above);
+      if (wave == 0) select_bucket<false>(hcnt, hmass, lv.nb, krem, &s_bucket, &s_cnt_above, &s_mass_above);
       __syncthreads();
       const uint32_t b = s_bucket;
       krem -= s_cnt_above;
@@ -421,7 +407,7 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
       });
       __syncthreads();
       if (wave == 0)
-        select_bucket<true>(hcnt, hmass, lv.nb, target - above, lcnt, lmass, &s_bucket, &s_cnt_above, &s_mass_above);
+        select_bucket<true>(hcnt, hmass, lv.nb, target - above, &s_bucket, &s_cnt_above, &s_mass_above);
       __syncthreads();
       const uint32_t b = s_bucket;
       above += s_mass_above;
