@@ -181,8 +181,8 @@ __device__ __forceinline__ uint64_t wave_inclusive_scan_u64(uint64_t v) {
   v += dpp_u64<kDppRowShr + 4>(v);
   v += dpp_u64<kDppRowShr + 8>(v);
   const uint64_t t0 = lane_u64(v, 15), t1 = lane_u64(v, 31), t2 = lane_u64(v, 47);
-  // Rows before this lane's, without branches: divergent control flow here
-  // would put an exec-mask change between this scan and the next DPP move.
+  // Rows before this lane's, without branches: compiled as divergent
+  // branches, this tail followed by further DPP scans gave wrong sums.
   const int row = (threadIdx.x & 63) >> 4;
   const uint64_t m1 = 0ull - (uint64_t)(row > 0), m2 = 0ull - (uint64_t)(row > 1), m3 = 0ull - (uint64_t)(row > 2);
   return v + ((t0 & m1) + (t1 & m2) + (t2 & m3));

@@ -182,7 +182,8 @@ __device__ void select_bucket(const uint32_t* hcnt, const unsigned long long* hm
   const uint64_t m_above = lane_u64(inc_m, L) - lane_u64(ms, L);
   // Inside group L: lane i < per takes bucket nb - 1 - L*per - i.
   // Loads clamped rather than predicated, and every lane read taken before
-  // the store, so no divergent branch sits between the scans and their reads.
+  // the single-lane store: with the reads inside that branch, the compiled
+  // selection returned a wrong mass above the bucket.
   const int b = max(nb - 1 - L * per - lane, 0);
   const uint64_t in_group = 0ull - (uint64_t)(lane < per);
   const uint64_t cb = (uint64_t)hcnt[b] & in_group;
