@@ -97,6 +97,7 @@ constexpr int kDppXor2 = 0x4E;           // quad_perm [2,3,0,1]: lane i <- i ^ 2
 constexpr int kDppRowHalfMirror = 0x141;  // lane i <- 7 - i within each 8 lanes
 constexpr int kDppRowMirror = 0x140;      // lane i <- 15 - i within each row
 constexpr int kDppRowShr = 0x110;         // + n: lane i <- i - n inside the row, 0 before its start
+constexpr int kDppWaveShr1 = 0x138;       // lane i <- i - 1 across the wave, lane 0 <- 0
 
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {

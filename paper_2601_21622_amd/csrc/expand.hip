@@ -28,7 +28,7 @@ namespace {
 
 constexpr int kExpThreads = 1024;
 constexpr int kExpWaves = kExpThreads / kWave;
-constexpr int kExpUnroll = 8;  // 64-entry steps whose loads a wave issues together
+constexpr int kExpUnroll = 32;  // 64-entry steps whose loads a wave issues together (a 32000-entry row: one round)
 
 __device__ __forceinline__ uint64_t rank_key(float x, int v) {
   return ((uint64_t)order_key(x) << 32) | (uint64_t)(0xffffffffu - (uint32_t)v);
@@ -36,19 +36,21 @@ __device__ __forceinline__ uint64_t rank_key(float x, int v) {
 
 // Offer this lane's key to the wave's sorted list (lane i < k holds the i-th
 // best key so far, 0 below; thr is the k-th best, 0 while the list is short).
-// Keys are unique and never 0 for a real entry.
+// Keys are unique and never 0 for a real entry.  Every cross-lane move is a
+// lane read (uniform source lane) or a one-lane DPP shift, so an insertion
+// costs no LDS round trip.
 __device__ __forceinline__ void offer(uint64_t key, int k, uint64_t& lst, uint64_t& thr) {
   const int lane = threadIdx.x & 63;
   unsigned long long cand = __ballot(key > thr);
   while (cand) {
     const int c = __ffsll(cand) - 1;
     cand &= cand - 1;
-    const uint64_t kc = __shfl(key, c);
+    const uint64_t kc = lane_u64(key, c);
     if (kc <= thr) continue;
     const int pos = __popcll(__ballot(lane < k && lst > kc));
-    const uint64_t up = __shfl_up(lst, 1);
+    const uint64_t up = dpp_u64<kDppWaveShr1>(lst);
     lst = lane == pos ? kc : (lane > pos && lane < k ? up : lst);
-    thr = __shfl(lst, k - 1);
+    thr = lane_u64(lst, k - 1);
   }
 }
 
