@@ -601,7 +601,7 @@ size_t accept_tree_workspace_bytes(int B, int V) {
 hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
                               const int32_t* tokens, const int32_t* parent, const float* u, void* ws,
                               int32_t* accept_len, int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len,
-                              hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                              hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop, const CombineJob* combine) {
   if (bt.nreq <= 0) return hipSuccess;
   AcceptArgs a;
   a.gamma = N;
@@ -633,7 +633,8 @@ hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& bt, const 
   if (e != hipSuccess) return e;
   CombineJob cj;
   memset(&cj, 0, sizeof(cj));
-  hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq), dim3(kCombineThreads), 0, stream, nullptr, ev_stop, 0, a,
+  if (combine != nullptr) cj = *combine;
+  hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq + cj.nblocks), dim3(kCombineThreads), 0, stream, nullptr, ev_stop, 0, a,
                         bt, accept_len, out_tok, new_kv_len, cj);
   return hipGetLastError();
 }

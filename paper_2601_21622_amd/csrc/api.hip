@@ -223,7 +223,8 @@ size_t accept_stage_ws(const sd_dims_t* d) { return std::max(accept_ws(d) + warp
 int run_accept_tree(const sd_dims_t* d, const float* x, const float* row_lse, const int32_t* tokens,
                     const int32_t* parent, const float* u, const int32_t* kv_len, int32_t* accept_len,
                     int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len, void* ws, hipStream_t stream,
-                    hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
+                    hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr,
+                    const std::vector<CombineJob>* merges = nullptr) {
   for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
     AcceptBatch bt;
     memset(&bt, 0, sizeof(bt));
@@ -233,9 +234,10 @@ int run_accept_tree(const sd_dims_t* d, const float* x, const float* row_lse, co
     if (kv_len != nullptr)
       for (int i = 0; i < bt.nreq; ++i) bt.kv_len[i] = kv_len[r0 + i];
     const bool first = r0 == 0, last = r0 + kMaxReqPerLaunch >= d->batch;
+    const CombineJob* cj = merges != nullptr ? &(*merges)[r0 / kMaxReqPerLaunch] : nullptr;
     hipError_t e = launch_accept_tree(d->gamma, d->vocab, d->batch, bt, x, row_lse, tokens, parent, u, ws, accept_len,
                                       out_tok, out_node, new_kv_len, stream, first ? ev_start : nullptr,
-                                      last ? ev_stop : nullptr);
+                                      last ? ev_stop : nullptr, cj);
     if (e != hipSuccess) return SD_ERR_HIP;
   }
   return SD_OK;
@@ -276,8 +278,8 @@ extern "C" {
 size_t sd_workspace_bytes(const sd_dims_t* dims, int32_t max_kv_len) {
   if (check_dims(dims) != SD_OK || max_kv_len < dims->gamma + 1) return 0;
   const int64_t chunks = attn_max_chunks(dims->dtype, dims->n_kv_heads, dims->batch, max_kv_len);
-  return std::max({tree_ws(dims) + attention_ws(dims, chunks),
-                   attention_ws(dims, chunks) + logits_ws(dims) + accept_stage_ws(dims), rate_ws(dims)});
+  return std::max({tree_ws(dims) + attention_ws(dims, chunks) + logits_ws(dims) + accept_stage_ws(dims),
+                   rate_ws(dims)});
 }
 
 int sd_verify_attention(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
@@ -571,8 +573,14 @@ int sd_verify_step_tree(const sd_dims_t* dims, const void* q, const void* k_pool
   st = check_kv(dims, kv_off, kv_len);
   if (st != SD_OK) return st;
   const AttnShape s = attn_shape(dims, scale, kv_len);
-  const size_t need = std::max(tree_ws(dims) + attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys)),
-                               logits_ws(dims) + accept_stage_ws(dims));
+  const size_t attn_bytes = tree_ws(dims) + attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys));
+  // As in the chain step: with the caller's hidden rows the attention merge
+  // rides in the acceptance's last launch, and the masks and partials keep
+  // their region: [masks][partials][projection][acceptance].
+  const bool defer = hidden != nullptr;
+  const size_t base = defer ? attn_bytes : 0;
+  const size_t need = defer ? attn_bytes + logits_ws(dims) + accept_stage_ws(dims)
+                            : std::max(attn_bytes, logits_ws(dims) + accept_stage_ws(dims));
   if (workspace_bytes < need) return SD_ERR_WORKSPACE;
 
   hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
@@ -581,14 +589,17 @@ int sd_verify_step_tree(const sd_dims_t* dims, const void* q, const void* k_pool
   hipStream_t stm = static_cast<hipStream_t>(stream);
   uint64_t* masks = static_cast<uint64_t*>(workspace);
   if (launch_tree_masks(dims->batch, dims->gamma, parent, masks, stm) != hipSuccess) return SD_ERR_HIP;
+  std::vector<CombineJob> merges;
   st = run_attention(dims, q, k_pool, v_pool, kv_off, kv_len, scale, attn_out,
-                     static_cast<char*>(workspace) + tree_ws(dims), stm, ev[0], ev[1], masks);
+                     static_cast<char*>(workspace) + tree_ws(dims), stm, ev[0], ev[1], masks, nullptr,
+                     defer ? &merges : nullptr);
   if (st != SD_OK) return st;
-  st = run_logits(dims, hidden != nullptr ? hidden : attn_out, w_vocab, logits, row_lse, workspace, stm, ev[2],
-                  ev[3]);
+  void* vws = static_cast<char*>(workspace) + base;
+  st = run_logits(dims, hidden != nullptr ? hidden : attn_out, w_vocab, logits, row_lse, vws, stm, ev[2], ev[3]);
   if (st != SD_OK) return st;
   return run_accept_tree(dims, logits, row_lse, tokens, parent, u, kv_len, accept_len, out_tok, out_node,
-                         new_kv_len, static_cast<char*>(workspace) + logits_ws(dims), stm, ev[4], ev[5]);
+                         new_kv_len, static_cast<char*>(vws) + logits_ws(dims), stm, ev[4], ev[5],
+                         defer ? &merges : nullptr);
 }
 
 int sd_tree_commit_kv(const sd_dims_t* dims, void* k_pool, void* v_pool, const int64_t* kv_off,

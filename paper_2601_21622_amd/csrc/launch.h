@@ -141,7 +141,8 @@ size_t accept_tree_workspace_bytes(int B, int V);
 hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& batch, const float* x, const float* row_lse,
                               const int32_t* tokens, const int32_t* parent, const float* u, void* ws,
                               int32_t* accept_len, int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len,
-                              hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+                              hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr,
+                              const CombineJob* combine = nullptr);
 
 // Acceptance rate of every draft position: beta[b * gamma + i] = sum_v
 // min(p(v), q_draft[b][i][v]), p from row b * (gamma + 1) + i of x (logits

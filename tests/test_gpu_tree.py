@@ -162,17 +162,21 @@ def test_tree_accept_matches_oracle(name, B, N, V, probs_mode):
     announce(f"tree accept case={name}: near-threshold {near}, mean depth {got[0].mean():.2f}")
 
 
-def test_tree_step_matches_oracle():
+@pytest.mark.parametrize("projection_input", ["hidden", "attention"])
+def test_tree_step_matches_oracle(projection_input):
+    """The projection reads the caller's hidden rows (the attention merge then
+    rides in the acceptance's last launch) or the attention output."""
     cfg = get_config("llama3_8b").replace(batch=3, gamma=9, n_q_heads=8, n_kv_heads=2, hidden=1024, vocab=4099,
                                           lengths=("explicit", (10, 700, 1500)))
-    announce(f"tree step case=gqa_small B={cfg.batch} nodes={cfg.gamma} V={cfg.vocab}")
+    announce(f"tree step case=gqa_small input={projection_input} B={cfg.batch} nodes={cfg.gamma} V={cfg.vocab}")
     x = make_inputs(cfg)
     rng = np.random.default_rng(11)
     parent = random_parents(rng, cfg.batch, cfg.gamma)
     tokens = rng.integers(0, cfg.vocab, size=(cfg.batch, cfg.gamma)).astype(np.int32)
     db = DeviceBatch(x)
     node = torch.empty_like(db.out_tok)
-    sd.sd_verify_step_tree(db.dims, db.q, db.k, db.v, x.kv_off, x.kv_len, tensor(parent), db.scale, db.hidden, db.w,
+    hidden = db.hidden if projection_input == "hidden" else None
+    sd.sd_verify_step_tree(db.dims, db.q, db.k, db.v, x.kv_off, x.kv_len, tensor(parent), db.scale, hidden, db.w,
                            tensor(tokens), db.u, db.attn, db.logits, db.lse, db.accept_len, db.out_tok, node,
                            db.new_kv_len, db.ws)
     torch.cuda.synchronize()
