@@ -256,13 +256,13 @@ def main() -> int:
         if args.sampling is not None:
             print("--tree-nodes and --sampling are separate modes", file=sys.stderr)
             return 2
+        cfg = cfg.replace(gamma=args.tree_nodes)
     if args.paged and (args.tree_nodes or args.sampling is not None):
         print("--paged applies to the plain verification step", file=sys.stderr)
         return 2
     if args.starsd is not None and (args.tree_nodes or args.sampling is not None):
         print("--starsd applies to the plain verification step", file=sys.stderr)
         return 2
-        cfg = cfg.replace(gamma=args.tree_nodes)
     B, G, M, V, K = cfg.batch, cfg.positions, cfg.rows, cfg.vocab, cfg.hidden
     log(f"generating workload {cfg.name}")
     x = make_inputs(cfg)
