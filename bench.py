@@ -238,7 +238,7 @@ def main() -> int:
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the verification step "
-              "does not shard across GPUs in this build)", file=sys.stderr)
+              "runs on a single GPU and does not shard across GPUs)", file=sys.stderr)
         return 2
 
     import numpy as np
