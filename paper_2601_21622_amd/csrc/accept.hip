@@ -397,7 +397,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
       const double v = i < nseg ? seg[i] : 0.0;
       const double c = wave_inclusive_scan_f64(v) + carry;
       if (i < nseg) seg[i] = c;
-      carry = __shfl(c, 63);
+      carry = lane_f64(c, 63);  // a scalar: branches on the total stay uniform
     }
     lds_wait();
     return carry;

@@ -311,6 +311,9 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
           cnt += __shfl_xor(cnt, off);
           ms += shfl_xor_u64(ms, off);
         }
+        // Equal on every lane; as scalars, the branch below is uniform.
+        cnt = (uint32_t)__builtin_amdgcn_readfirstlane((int)cnt);
+        ms = lane_u64(ms, 0);
         uint32_t th = thk;
         unsigned long long w = ms;
         bool pdone = false;
