@@ -15,7 +15,8 @@
 //      and 10 bits per level, with per-bucket counts and masses in LDS; the
 //      bucket where the running count from the top reaches k holds the cut;
 //   3. top-p: the same descent over the kept tokens, on masses, against
-//      ceil(top_p * kept mass);
+//      ceil(top_p * kept mass) (with no top-k cut, the kept mass is the
+//      total of the first level's histogram, which holds every entry);
 //   4. lse = max / T + log(kept mass).
 // Masses are exp((logit - max) / T) in float32, scaled by 2^S and truncated to
 // 64-bit integers (S = 62 - ceil(log2 V), so a whole row cannot overflow);
@@ -35,6 +36,7 @@ namespace {
 constexpr int kWarpThreads = 1024;
 constexpr int kWarpWaves = kWarpThreads / kWave;
 constexpr int kBuckets = 2048;
+static_assert(kBuckets == 2 * kWarpThreads, "the level-0 total reads two buckets per thread");
 constexpr int kCand = 2048;  // candidates the small-k path can hold
 
 __device__ __forceinline__ float key_value(uint32_t k) {
@@ -264,6 +266,7 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
   uint32_t theta = 0;
   unsigned long long W = 0;
   bool have_k = false, have_p = false;
+  bool w_known = true;  // W holds the kept mass (false: the first top-p level supplies it)
   if (top_k >= 1 && top_k <= kWave && top_k < V) {
     // Small k: the k-th largest of the threads' best entries bounds the k-th
     // largest logit from below (k threads reach it), so the entries at or
@@ -374,6 +377,10 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
       __syncthreads();
     }
     theta = prefix;
+  } else if (top_p < 1.f) {
+    // No top-k cut: the first level of the top-p descent histograms every
+    // entry, and W is the total of that histogram (no pass of its own).
+    w_known = false;
   } else {
     unsigned long long sum = 0;
     row_pass(x, V, [&](int, float xv) { sum += fixed_mass(xv, m, inv_t, scale); });
@@ -390,8 +397,12 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
   }
 
   if (top_p < 1.f && !have_p) {
-    unsigned long long target = (unsigned long long)ceil((double)top_p * (double)W);
-    target = target < 1 ? 1 : (target > W ? W : target);
+    unsigned long long target = 0;
+    auto set_target = [&]() {
+      target = (unsigned long long)ceil((double)top_p * (double)W);
+      target = target < 1 ? 1 : (target > W ? W : target);
+    };
+    if (w_known) set_target();
     uint32_t prefix = 0;
     unsigned long long above = 0;
     for (int level = 0; level < 3; ++level) {
@@ -410,6 +421,21 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
         }
       });
       __syncthreads();
+      if (!w_known) {  // level 0 over every entry: W = the histogram's total
+        unsigned long long t = hmass[tid] + hmass[tid + kWarpThreads];
+        for (int off = 32; off >= 1; off >>= 1) t += shfl_xor_u64(t, off);
+        if (lane == 0) w_sum[wave] = t;
+        __syncthreads();
+        if (tid == 0) {
+          unsigned long long tt = 0;
+          for (int w = 0; w < kWarpWaves; ++w) tt += w_sum[w];
+          s_total = tt;
+        }
+        __syncthreads();
+        W = s_total;
+        w_known = true;
+        set_target();
+      }
       if (wave == 0)
         select_bucket<true>(hcnt, hmass, lv.nb, target - above, &s_bucket, &s_cnt_above, &s_mass_above);
       __syncthreads();
