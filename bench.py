@@ -205,7 +205,22 @@ def starsd_leg(sd, dims, cfg, copies, ms_step, args) -> dict:
             "time_unit": "ms", "standalone_rate": rate, "model": rep.as_dict()}
 
 
-def main() -> int:
+def workload_config(args, get_config):
+    """The workload of this run and its mode checks: (config, None), or
+    (None, message) when the options do not go together."""
+    if args.tree_nodes and args.sampling is not None:
+        return None, "--tree-nodes and --sampling are separate modes"
+    if args.paged and (args.tree_nodes or args.sampling is not None):
+        return None, "--paged applies to the plain verification step"
+    if args.starsd is not None and (args.tree_nodes or args.sampling is not None):
+        return None, "--starsd applies to the plain verification step"
+    cfg = get_config(args.workload)
+    if args.tree_nodes:
+        cfg = cfg.replace(gamma=args.tree_nodes)
+    return cfg, None
+
+
+def parser() -> argparse.ArgumentParser:
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
@@ -235,7 +250,11 @@ def main() -> int:
                          "optionally a standalone target rate in tokens/ms (gives N_max)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a device copy of known size (counter calibration)")
-    args = ap.parse_args()
+    return ap
+
+
+def main() -> int:
+    args = parser().parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the verification step "
               "runs on a single GPU and does not shard across GPUs)", file=sys.stderr)
@@ -251,17 +270,9 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
-    cfg = get_config(args.workload)
-    if args.tree_nodes:
-        if args.sampling is not None:
-            print("--tree-nodes and --sampling are separate modes", file=sys.stderr)
-            return 2
-        cfg = cfg.replace(gamma=args.tree_nodes)
-    if args.paged and (args.tree_nodes or args.sampling is not None):
-        print("--paged applies to the plain verification step", file=sys.stderr)
-        return 2
-    if args.starsd is not None and (args.tree_nodes or args.sampling is not None):
-        print("--starsd applies to the plain verification step", file=sys.stderr)
+    cfg, problem = workload_config(args, get_config)
+    if problem is not None:
+        print(problem, file=sys.stderr)
         return 2
     B, G, M, V, K = cfg.batch, cfg.positions, cfg.rows, cfg.vocab, cfg.hidden
     log(f"generating workload {cfg.name}")

@@ -1,0 +1,48 @@
+"""bench.py's option handling, on the CPU: the workload each mode runs and
+the combinations it refuses (no GPU needed)."""
+
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from workloads import get_config  # noqa: E402
+
+
+def _cfg(*argv):
+    return bench.workload_config(bench.parser().parse_args(list(argv)), get_config)
+
+
+def test_default_workload_is_the_chain_step():
+    cfg, problem = _cfg()
+    assert problem is None
+    assert cfg.name == "vicuna7b" and cfg.gamma == get_config("vicuna7b").gamma
+
+
+@pytest.mark.parametrize("nodes", [15, 31, 63])
+def test_tree_nodes_set_the_node_count(nodes):
+    cfg, problem = _cfg("--workload", "llama3_8b", "--tree-nodes", str(nodes))
+    assert problem is None
+    assert cfg.gamma == nodes and cfg.batch == get_config("llama3_8b").batch
+
+
+@pytest.mark.parametrize("argv", [
+    ("--tree-nodes", "15", "--sampling", "0.8,40,0.9"),
+    ("--paged", "64", "--tree-nodes", "15"),
+    ("--paged", "64", "--sampling", "1.0,0,0.9"),
+    ("--starsd", "1.46,0.5", "--tree-nodes", "15"),
+    ("--starsd", "1.46,0.5", "--sampling", "0.8,40,0.9"),
+])
+def test_modes_that_do_not_combine_are_refused(argv):
+    cfg, problem = _cfg(*argv)
+    assert cfg is None and problem
+
+
+def test_more_than_one_gpu_is_refused(monkeypatch, capsys):
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--gpus", "2"])
+    assert bench.main() == 2
+    assert "one GPU" in capsys.readouterr().err
