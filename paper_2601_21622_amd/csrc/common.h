@@ -224,9 +224,9 @@ __device__ __forceinline__ void lds_barrier() {
 // at once (rows of up to kR * 64 tiles are read once), the lane sums are added
 // by the fixed-order wave reduction, so the result is deterministic and
 // every lane returns the same bits.  ntiles >= 1.
-__device__ __forceinline__ float row_lse_from_partials(const float2* p, int ntiles) {
+template <int kR>  // tiles per lane held in registers per round
+__device__ __forceinline__ float row_lse_from_partials_r(const float2* p, int ntiles) {
   const int lane = threadIdx.x & 63;
-  constexpr int kR = 16;  // tiles per lane held in registers per round
   float2 v[kR];
   auto load = [&](int base) {
 #pragma unroll
@@ -251,6 +251,12 @@ __device__ __forceinline__ float row_lse_from_partials(const float2* p, int ntil
   }
   s = wave_sum_f64(s);
   return (float)((double)mx + log(s));  // mx and s are the same on every lane
+}
+
+// Rows of at most 512 tiles (vocabularies up to 131072 at 256-wide tiles)
+// take one round of 8 loads per lane; longer rows rounds of 16.
+__device__ __forceinline__ float row_lse_from_partials(const float2* p, int ntiles) {
+  return ntiles <= 8 * kWave ? row_lse_from_partials_r<8>(p, ntiles) : row_lse_from_partials_r<16>(p, ntiles);
 }
 
 }  // namespace sdv
