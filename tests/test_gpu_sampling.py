@@ -155,12 +155,14 @@ def test_sampled_step_matches_oracle():
     announce(f"sampled step: requests in band {near}")
 
 
-@pytest.mark.parametrize("levels,k,p", [(3, 40, 0.9), (12, 40, 0.9), (12, 64, 1.0), (3000, 64, 0.5)])
+@pytest.mark.parametrize("levels,k,p", [(3, 40, 0.9), (12, 40, 0.9), (12, 64, 1.0), (3000, 64, 0.5), (12, 0, 0.9),
+                                        (3, 0, 0.5)])
 def test_sampled_ties_match_oracle(levels, k, p):
     """Target logits on a few levels, so that the cut falls inside a large
-    tie: kept sets above 64 entries (the top-p cut by radix descent) and
-    candidate sets above 2048 (the top-k cut by radix descent) as well as the
-    small-k selection."""
+    tie: kept sets above 64 entries (the top-p cut by radix descent),
+    candidate sets above 2048 (the top-k cut by radix descent), the small-k
+    selection, and top-p with no top-k (the row's mass from the first radix
+    level)."""
     B, gamma, V = 4, 3, 32000
     T = 0.9
     G = gamma + 1
