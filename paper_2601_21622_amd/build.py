@@ -32,6 +32,14 @@ HIPCC_FLAGS = [
     "-I", os.path.join(ROOT, "include"),
 ]
 
+# Per-source additions.  Attention: IEEE mode off with relaxed NaN handling,
+# so the row maxima of MFMA scores need no NaN-quieting instruction per score
+# (masking uses -inf, never NaN; NaN-sensitive decisions live in accept.hip).
+EXTRA_FLAGS = {
+    "attention.hip": ["-fno-honor-nans", "-mno-amdgpu-ieee"],
+}
+
+
 def _hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if cand and os.path.exists(cand):
@@ -60,7 +68,7 @@ def build(verbose: bool = False) -> str:
 
     def compile_one(src):
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        _run([hipcc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        _run([hipcc, *HIPCC_FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj], verbose)
         return obj
 
     with ThreadPoolExecutor(min(len(SOURCES), os.cpu_count() or 1)) as ex:

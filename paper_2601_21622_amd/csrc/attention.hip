@@ -28,6 +28,10 @@
 // pieces so that the fragment reads are free of bank conflicts.
 #include <hip/hip_ext.h>
 
+#include <atomic>
+#include <climits>
+#include <type_traits>
+
 #include "combine.h"
 #include "common.h"
 #include "launch.h"
@@ -53,6 +57,22 @@ constexpr int64_t kAttnTargetItemsMany = 4096;
 // that spill into a second workgroup on some CUs were measured slower).
 constexpr int kRoundMinKeys = 160;
 constexpr int64_t kRoundWorkgroups = 256;
+// Start-up cost of one work item (query rows, pipeline fill, partial write),
+// in keys of streaming, for the round estimate of the multi-block kernel.
+constexpr int64_t kItemStartKeys = 256;
+
+// Compute units of the current device (cached per device; 256 on MI355X).
+int64_t device_cu_count() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
 
 
 __device__ __forceinline__ int find_request(const AttnBatch& bt, int c) {
@@ -75,105 +95,243 @@ __device__ __forceinline__ bool key_visible(int key, int pend, uint64_t anc) {
 
 __device__ __forceinline__ uint64_t chain_mask(int j) { return j >= 63 ? ~0ull : ((2ull << j) - 1ull); }
 
-// Online softmax of one 16-row block over a 32-key tile, in the log2 domain:
-// the lane owns row lr of the block and keys k0 + kb*16 + lg*4 + e.  With
-// LAZY the reference maximum m of the rows moves lazily: only when some row's
-// tile maximum exceeds it by more than kLazyLog2 does the wave move m to the
-// new maxima and rescale the sums and O (rows whose maximum did not grow get
-// alpha = 1).  Otherwise p = 2^(s*scale - m) stays below 2^kLazyLog2, well
-// inside float32 and bfloat16 range, and O and the sum share the same m, so
-// the normalised result is unchanged.  Masking (key_visible) applies only
-// when `masked` (always without LAZY, which keeps the step one branch-free
-// block); a fully masked row gives p = 0.
+// Online softmax over a 32-key tile, in the log2 domain, for RB 16-row
+// blocks at once: in block rb the lane owns row lr and keys
+// k0 + kb*16 + lg*4 + e.  The reference maximum m of each row moves lazily:
+// only when some row's tile maximum exceeds its m by more than kLazyLog2 does
+// the wave (one uniform branch for all blocks) move every m to the new maxima
+// and rescale the sums and O (rows whose maximum did not grow get alpha = 1).
+// Otherwise p = 2^(s*scale - m) stays below 2^kLazyLog2, well inside float32
+// and bfloat16 range, and O and the sum share the same m, so the normalised
+// result is unchanged.  The branch is rarely taken after the first tiles of a
+// chunk, so O's accumulators are normally touched by the MFMAs alone.
+// Masking (key_visible) depends on MK: never (tiles every row sees whole),
+// always (tiles that reach past some row's causal limit), or at run time
+// when `masked` is set; a fully masked row gives p = 0.
 // Requires scale_log2 > 0 (the row maximum is taken before scaling).
 constexpr float kLazyLog2 = 8.f;
-// Up to this many row blocks the rescale branch costs nothing; with more, the
-// output accumulators no longer fit beside the rest in plain registers and
-// the branch makes the compiler move them every tile, so the rescale runs on
-// every tile instead (alpha is 1 whenever the maximum did not grow).
-constexpr int kLazyMaxBlocks = 2;
+// Growth of a row's maximum (log2 domain) that makes the multi-block kernel
+// restart an item (it never rescales O in place).
+constexpr float kRestartLog2 = 64.f;
+enum { kMaskNever = 0, kMaskAlways = 1, kMaskRuntime = 2 };
 
 __device__ __forceinline__ float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// TREE = false promises chain rows, whose test is one comparison with the
-// row's last visible key lim (-1: nothing visible); pend and anc are then unused.
-template <int DB, bool LAZY, bool TREE>
-__device__ __forceinline__ bf16x8 softmax_tile(const f32x4 (&sc)[2], float scale_log2, bool masked, int k0, int pend,
-                                               uint64_t anc, int lim, float& m, float& lsum, f32x4 (&o)[DB]) {
+// max over the four 16-lane groups of a wave (lanes l, l^16, l^32, l^48),
+// with the gfx950 lane-swap moves (VALU, no LDS round trip).
+__device__ __forceinline__ float max_over_lane_groups(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
+
+// The phases of folding one 32-key tile into the running state of a wave's
+// rows.  TREE = false promises chain rows, whose test is one comparison with
+// the row's last visible key lim (-1: nothing visible); pend and anc are then
+// unused.
+
+// Scores of the tile (masked per MK) and each row's scaled tile maximum;
+// returns whether some row's maximum exceeds its reference by more than
+// kLazyLog2 (the same answer on every lane).
+template <int RB, int MK, bool TREE>
+__device__ __forceinline__ bool tile_scores(const f32x4 (&sc)[RB][2], float scale_log2, bool masked, int k0,
+                                            const int (&pend)[RB], const uint64_t (&anc)[RB], const int (&lim)[RB],
+                                            const float (&m)[RB], float (&raw)[RB][8], float (&mx)[RB],
+                                            float thr = kLazyLog2) {
   const int lg = (threadIdx.x & 63) >> 4;
-  float raw[8];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) raw[kb * 4 + e] = sc[kb][e];
-  if (!LAZY || masked) {
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (TREE ? !key_visible(k0 + kb * 16 + lg * 4 + e, pend, anc) : k0 + kb * 16 + lg * 4 + e > lim)
-          raw[kb * 4 + e] = -INFINITY;
-  }
-  float mx = fmaxf(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])),
-                   fmaxf(fmaxf(raw[4], raw[5]), fmaxf(raw[6], raw[7])));
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  mx *= scale_log2;
-  if (!LAZY || __ballot(mx > m + kLazyLog2) != 0) {
-    const float mn = fmaxf(m, mx);
-    const float alpha = exp2_raw(m - mn);
-    m = mn;
-    lsum *= alpha;
+      for (int e = 0; e < 4; ++e) raw[rb][kb * 4 + e] = sc[rb][kb][e];
+  if (MK == kMaskAlways || (MK == kMaskRuntime && masked)) {
 #pragma unroll
-    for (int db = 0; db < DB; ++db) o[db] *= alpha;
-  }
-  const float mneg = -m;
-  bf16x8 pf;
-  float ps = 0.f;
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const __bf16 pb = (__bf16)exp2_raw(fmaf(raw[e], scale_log2, mneg));
-    pf[e] = pb;
-    ps += (float)pb;
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = k0 + kb * 16 + lg * 4 + e;
+          if (TREE ? !key_visible(key, pend[rb], anc[rb]) : key > lim[rb]) raw[rb][kb * 4 + e] = -INFINITY;
+        }
   }
-  lsum += ps;
-  return pf;
+  bool grow = false;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const float* r = raw[rb];
+    float t = fmaxf(fmaxf(fmaxf(r[0], r[1]), r[2]), fmaxf(fmaxf(r[3], r[4]), r[5]));
+    t = fmaxf(t, fmaxf(r[6], r[7]));
+    mx[rb] = max_over_lane_groups(t) * scale_log2;
+    grow |= mx[rb] > m[rb] + thr;
+  }
+  return __ballot(grow) != 0;
 }
 
-// K or V tile of one wave in LDS: 32 keys x D, row r (D*2 bytes) holding its
-// 16-byte pieces rotated by rot(r) pieces.  K: rot(r) = r*P/16 (mod P), so a
-// piece read by 16 consecutive keys hits 16 distinct bank groups.  V:
-// rot(r) = 2*(r*P/16) (mod P), so the four rows a 16-lane group touches in one
-// transposing read fall on distinct banks.
-template <int D, bool IS_V>
-struct KVTile {
-  static constexpr int kPieces = D / 8;          // 16-byte pieces per row
-  static constexpr int kBytes = kTile * D * 2;   // one tile
-  static constexpr int kRowsPerDma = 64 / kPieces;
-  static constexpr int kDmas = kTile / kRowsPerDma;  // DMA instructions per tile
-  __device__ static constexpr int rot(int r) {
-    return ((IS_V ? 2 : 1) * ((r * kPieces) >> 4)) % kPieces;
-  }
-  // Byte offset of element d of row r.
-  __device__ static constexpr int at(int r, int d) {
-    return r * D * 2 + (((d >> 3) + rot(r)) % kPieces) * 16 + (d & 7) * 2;
-  }
-  // DMA instruction i of a tile: lane l brings row r = i*kRowsPerDma +
-  // l/kPieces, the global piece that belongs in LDS slot l%kPieces.  t0 is
-  // key k0's row; rows past the request's last key L - 1 repeat it.  A dead
-  // tile (past the item's last, issued only to keep the pipeline shape) has
-  // every lane read the same 16 bytes: one cache line per instruction.
-  __device__ static void load(const uint16_t* t0, int k0, int L, unsigned char* tile, int lane, bool dead = false) {
+// Move each row's reference maximum to its new maximum and rescale its sum
+// and O (alpha = 1 for rows whose maximum did not grow).
+template <int RB, int DB>
+__device__ __forceinline__ void tile_rescale(const float (&mx)[RB], float (&m)[RB], float (&lsum)[RB],
+                                             f32x4 (&o)[RB][DB]) {
 #pragma unroll
-    for (int i = 0; i < kDmas; ++i) {
-      const int r = i * kRowsPerDma + lane / kPieces;
-      const int piece = (lane % kPieces - rot(r) + kPieces) % kPieces;
-      const int key = min(k0 + r, L - 1);
-      const int src = dead ? 0 : (key - k0) * D + piece * 8;
-      dma_16B_to_lds_opaque(t0 + src, tile + i * 1024);
+  for (int rb = 0; rb < RB; ++rb) {
+    const float mn = fmaxf(m[rb], mx[rb]);
+    const float alpha = exp2_raw(m[rb] - mn);
+    m[rb] = mn;
+    lsum[rb] *= alpha;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+  }
+}
+
+// p = 2^(s*scale - m) rounded to bfloat16 (the P fragments, B operand of
+// O^T += V^T P^T); the rounded p of the lane's keys are added to lsum, so
+// the normaliser matches the weights O accumulates.
+template <int RB>
+__device__ __forceinline__ void tile_probs(const float (&raw)[RB][8], float scale_log2, const float (&m)[RB],
+                                           float (&lsum)[RB], bf16x8 (&pf)[RB]) {
+  const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const float mneg = -m[rb];
+    float acc = lsum[rb];
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const f32x2 x = {exp2_raw(fmaf(raw[rb][e], scale_log2, mneg)), exp2_raw(fmaf(raw[rb][e + 1], scale_log2, mneg))};
+      const bf16x2 pb = __builtin_convertvector(x, bf16x2);
+      pf[rb][e] = pb[0];
+      pf[rb][e + 1] = pb[1];
+      acc = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, acc, false);
     }
+    lsum[rb] = acc;
+  }
+}
+
+// Staging layout of a 32-key tile of K or V in LDS.  The tile is split into
+// 1 KB blocks n = q * kHalves + h: keys 8q .. 8q + 7 of the tile, bytes
+// 128h .. 128h + 127 of each key row (one 128-byte line per row).  A wave
+// fills a block with one 16-byte load (or DMA) per lane, lane l bringing a
+// 16-byte unit of row l / 8, so every load instruction reads eight whole
+// cache lines.  In the block, row r sits at byte 128r and its unit u at slot
+// (u + rot) mod 8:
+//   K: rot = r + (q & 1), so the 16 keys one fragment read touches (two
+//      blocks, one unit each) fall on 16 distinct 16-byte bank groups;
+//   V: rot = r & ~1, which keeps the two units of a 32-byte column block
+//      adjacent, and the 8 rows one half-wave of the transposing read
+//      ds_read_b64_tr_b16 touches (32 bytes each) cover all 256 bytes of
+//      the bank space once.
+// The per-lane offsets below depend on the lane and at most two bits of
+// the block or fragment index, so loads and reads take a few fixed per-lane
+// registers plus scalar or immediate offsets.
+template <int D>
+struct Tile {
+  static constexpr int kRow = D * 2;            // bytes per key row
+  static constexpr int kHalves = D / 64;        // 128-byte half rows per row
+  static constexpr int kBlocks = 4 * kHalves;   // blocks per tile of K (or V)
+  static constexpr int kBytes = kBlocks * 1024;
+  static_assert(kBytes == kTile * kRow, "a tile is 32 rows");
+  // Global byte offset of block n in the tile.
+  __device__ static constexpr int block_global(int n) { return (n / kHalves) * 8 * kRow + (n % kHalves) * 128; }
+  // Global byte offset (from block_global) of the unit lane l loads for a
+  // K block with q & 1 == qodd, and for any V block.
+  __device__ static uint32_t k_load(int l, int qodd) {
+    const int r = l >> 3;
+    return r * kRow + (((l & 7) - r - qodd) & 7) * 16;
+  }
+  __device__ static uint32_t v_load(int l) {
+    const int r = l >> 3;
+    return r * kRow + (((l & 7) - (r & ~1)) & 7) * 16;
+  }
+  // The same with the row clamped to the tile's last existing row `last`
+  // (global offset from the tile start).
+  __device__ static uint32_t k_load_clamped(int l, int n, int last) {
+    const int q = n / kHalves, r = l >> 3;
+    return min(8 * q + r, last) * kRow + (n % kHalves) * 128 + (((l & 7) - r - (q & 1)) & 7) * 16;
+  }
+  __device__ static uint32_t v_load_clamped(int l, int n, int last) {
+    const int q = n / kHalves, r = l >> 3;
+    return min(8 * q + r, last) * kRow + (n % kHalves) * 128 + (((l & 7) - (r & ~1)) & 7) * 16;
+  }
+  // K fragment (16-key block kb, 32-wide step ds) of lane (lg, lr): key
+  // 16kb + lr, elements 32ds + 8lg .. +8.  LDS offset = k_read(lane, ds & 1)
+  // + k_read_imm(kb, ds).
+  __device__ static uint32_t k_read(int lane, int dsodd) {
+    const int lg = lane >> 4, lr = lane & 15, r = lr & 7, qodd = lr >> 3;
+    return qodd * kHalves * 1024 + r * 128 + ((4 * dsodd + lg + r + qodd) & 7) * 16;
+  }
+  __device__ static constexpr int k_read_imm(int kb, int ds) { return kb * 2 * kHalves * 1024 + (ds / 2) * 1024; }
+  // Transposing read of V for output block db and key half hk: lane (lg, j)
+  // addresses key 16hk + 4lg + j/4, elements 16db + 4(j%4) .. +3.  LDS
+  // offset = v_read(lane, db % 4) + v_read_imm(db, hk).
+  __device__ static uint32_t v_read(int lane, int dbm) {
+    const int lg = lane >> 4, j = lane & 15, r = 4 * (lg & 1) + (j >> 2);
+    return (lg >> 1) * kHalves * 1024 + r * 128 + ((2 * dbm + ((j >> 1) & 1) + (r & ~1)) & 7) * 16 + 8 * (j & 1);
+  }
+  __device__ static constexpr int v_read_imm(int db, int hk) { return hk * 2 * kHalves * 1024 + (db / 4) * 1024; }
+};
+
+// Per-lane offsets of the staging layout, computed once per wave.
+template <int D>
+struct TileLane {
+  uint32_t kload[2], vload, kread[2], vread[4];
+  __device__ explicit TileLane(int lane) {
+    using T = Tile<D>;
+    kload[0] = T::k_load(lane, 0);
+    kload[1] = T::k_load(lane, 1);
+    vload = T::v_load(lane);
+    kread[0] = T::k_read(lane, 0);
+    kread[1] = T::k_read(lane, 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) vread[i] = T::v_read(lane, i);
   }
 };
+
+// LDS DMA of one 1 KB block: lane l copies the 16 bytes at gbase + voff into
+// LDS bytes lds + 16l .. +15.  gbase and lds are wave-uniform (scalar
+// registers).  Issued from inline assembly, so the compiler neither tracks it
+// nor inserts waits for it: the kernel's own vmcnt waits order it against the
+// LDS reads.  It sets M0 itself, so the kernel uses M0 for nothing else.  The
+// load carries the nontemporal hint (every row is read once).
+// Both scalars pass through readfirstlane (free when the compiler already
+// holds them in scalar registers), since the instruction takes them only
+// from scalar registers.
+__device__ __forceinline__ void dma_block(uint32_t lds, const void* gbase, uint32_t voff) {
+  const uint64_t g = (uint64_t)(uintptr_t)gbase;
+  const uint64_t gu = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(g >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)g);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"((const void*)(uintptr_t)gu)
+               : "memory");
+}
+
+// DMA of one tile (rows at kt / vt) into the wave's LDS stage (kl / vl);
+// `last` >= 31 when every row of the tile exists, else its last row.
+template <int D>
+__device__ __forceinline__ void dma_tile(const uint16_t* kt, const uint16_t* vt, uint32_t kl, uint32_t vl,
+                                         const TileLane<D>& tl, int last) {
+  using T = Tile<D>;
+  const int lane = threadIdx.x & 63;
+  const char* kb = reinterpret_cast<const char*>(kt);
+  const char* vb = reinterpret_cast<const char*>(vt);
+  if (last >= kTile - 1) {
+#pragma unroll
+    for (int n = 0; n < T::kBlocks; ++n) {
+      dma_block(kl + n * 1024, kb + T::block_global(n), tl.kload[(n / T::kHalves) & 1]);
+      dma_block(vl + n * 1024, vb + T::block_global(n), tl.vload);
+    }
+  } else {
+#pragma unroll
+    for (int n = 0; n < T::kBlocks; ++n) {
+      dma_block(kl + n * 1024, kb, T::k_load_clamped(lane, n, last));
+      dma_block(vl + n * 1024, vb, T::v_load_clamped(lane, n, last));
+    }
+  }
+}
 
 // Where the K and V rows of one (request, KV head) live.  Contiguous: the
 // request's segment [Hkv][L][D] at kv_off.  Paged: pages [num_pages][Hkv][P][D]
@@ -231,89 +389,98 @@ struct AttnRows {
   f32x4 o[RB][D / 16];    // running O^T blocks
 };
 
-// Fold one staged 32-key tile (keys from k0, K in ksrc, V in vsrc) into the
-// running state of a wave's rows: S^T = K Q^T, online softmax, O^T += V^T P^T.
-// `masked` says whether some key of the tile may lie past a row's causal
-// limit (only then are the limits applied); a tile with live == false
-// contributes nothing (all of its keys are masked).
-template <int RB, int D, bool TREE>
-__device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2, int k0, bool masked,
-                                          const unsigned char* __restrict__ ksrc,
-                                          const unsigned char* __restrict__ vsrc, bool live = true) {
-  constexpr int DS = D / 32;
-  constexpr int DB = D / 16;
-  using KT = KVTile<D, false>;
-  using VT = KVTile<D, true>;
-  const int lane = threadIdx.x & 63;
-  const int lr = lane & 15;
-  const int lg = lane >> 4;
-
-  // K fragments (A operand): lane holds key kb*16 + lr, d = ds*32 + lg*8 .. +8.
-  bf16x8 kf[2][DS];
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds)
-      kf[kb][ds] = __builtin_bit_cast(
-          bf16x8, *reinterpret_cast<const u32x4*>(ksrc + KT::at(kb * 16 + lr, ds * 32 + lg * 8)));
-  f32x4 sc[RB][2];
+// S^T = K Q^T for the tile's 32 keys (K fragments kf) and the wave's rows.
+template <int RB, int D>
+__device__ __forceinline__ void tile_qk(const AttnRows<RB, D>& st, const bf16x8 (&kf)[2][D / 32], f32x4 (&sc)[RB][2]) {
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) acc = mfma16x16x32(kf[kb][ds], st.qf[rb][ds], acc);
+      for (int ds = 0; ds < D / 32; ++ds) acc = mfma16x16x32(kf[kb][ds], st.qf[rb][ds], acc);
       sc[rb][kb] = acc;
     }
+}
 
-  bf16x8 pf[RB];
+// O^T += V^T P^T with V staged at vsrc.  V^T fragments (A operand): lane
+// (lg, lr) receives d = db*16 + lr and keys {lg*4 .. +3} (first half),
+// {16 + lg*4 .. +3} (second half), the P fragment's k-slots.
+// V^T fragments (A operand of O^T += V^T P^T) of a tile staged in LDS:
+// vf[db] of lane (lg, lr) holds d = db*16 + lr and keys {lg*4 .. +3}, then
+// {16 + lg*4 .. +3}, the P fragment's k-slots.
+template <int D>
+__device__ __forceinline__ void read_v_frags(const unsigned char* __restrict__ vsrc, const TileLane<D>& tl,
+                                             bf16x8 (&vf)[D / 16]) {
+  using T = Tile<D>;
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-    pf[rb] = softmax_tile<DB, (RB <= kLazyMaxBlocks), TREE>(sc[rb], scale_log2, masked || !live, k0,
-                                                            live ? st.pend[rb] : -1, live ? st.anc[rb] : 0ull,
-                                                            live ? st.lim[rb] : -1, st.m[rb], st.lsum[rb], st.o[rb]);
-
-  // V^T fragments (A operand of O^T += V^T P^T): lane (lg, lr) needs
-  // d = db*16 + lr and keys {lg*4 .. +3} then {16 + lg*4 .. +3}, the
-  // P fragment's k-slots.  Lane j of the 16-lane group lg points at row
-  // 4*lg + j/4 (+16), d = db*16 + 4*(j%4) .. +3.
-  const int jr = 4 * lg + (lr >> 2);
-  const int jd = 4 * (lr & 3);
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const s16x4 lo = lds_read_tr16(vsrc + VT::at(jr, db * 16 + jd));
-    const s16x4 hi = lds_read_tr16(vsrc + VT::at(16 + jr, db * 16 + jd));
-    const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) st.o[rb][db] = mfma16x16x32(vf, pf[rb], st.o[rb][db]);
+  for (int db = 0; db < D / 16; ++db) {
+    const s16x4 lo = lds_read_tr16(vsrc + tl.vread[db & 3] + T::v_read_imm(db, 0));
+    const s16x4 hi = lds_read_tr16(vsrc + tl.vread[db & 3] + T::v_read_imm(db, 1));
+    vf[db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   }
 }
 
-// One step of a wave's software pipeline: start the DMAs of the next tile
-// (keys from k0_next, rows at kn / vn) into (kdst, vdst), wait until only those are in flight,
-// then fold the current tile.  The stage pointers are restrict-qualified, so
-// the compiler knows the new DMAs cannot write what this step reads and
-// leaves the ordering to the explicit wait.
-template <int RB, int D, bool TREE>
-__device__ __forceinline__ void attn_step(AttnRows<RB, D>& st, float scale_log2, const uint16_t* kn,
-                                          const uint16_t* vn, int L, int k0_next, bool next_dead, int k0,
-                                          bool masked, unsigned char* __restrict__ kdst,
-                                          unsigned char* __restrict__ vdst, const unsigned char* __restrict__ ksrc,
-                                          const unsigned char* __restrict__ vsrc) {
-  using KT = KVTile<D, false>;
-  using VT = KVTile<D, true>;
-  const int lane = threadIdx.x & 63;
-  KT::load(kn, k0_next, L, kdst, lane, next_dead);
-  VT::load(vn, k0_next, L, vdst, lane, next_dead);
-  wait_vmcnt<KT::kDmas + VT::kDmas>();
-  attn_fold<RB, D, TREE>(st, scale_log2, k0, masked, ksrc, vsrc);
+// O^T += V^T P^T.
+template <int RB, int D>
+__device__ __forceinline__ void tile_pv(AttnRows<RB, D>& st, const bf16x8 (&pf)[RB], const bf16x8 (&vf)[D / 16]) {
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) st.o[rb][db] = mfma16x16x32(vf[db], pf[rb], st.o[rb][db]);
+}
+
+// Fold one 32-key tile (keys from k0; K fragments kf, V staged at vsrc)
+// into the running state, the rescale inline.  `masked` says whether some
+// key of the tile may lie past a row's causal limit (used when MK is
+// kMaskRuntime); a tile with live == false contributes nothing.
+template <int RB, int D, bool TREE, int MK>
+__device__ __forceinline__ void attn_fold(AttnRows<RB, D>& st, float scale_log2, int k0, bool masked,
+                                          const bf16x8 (&kf)[2][D / 32], const unsigned char* __restrict__ vsrc,
+                                          const TileLane<D>& tl, bool live = true) {
+  f32x4 sc[RB][2];
+  tile_qk<RB, D>(st, kf, sc);
+  float raw[RB][8], mx[RB];
+  bool grow;
+  if (MK == kMaskRuntime && !live) {
+    // A dead tile: every key masked.
+    int pend[RB], lim[RB];
+    uint64_t anc[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      pend[rb] = -1;
+      lim[rb] = -1;
+      anc[rb] = 0ull;
+    }
+    grow = tile_scores<RB, kMaskAlways, TREE>(sc, scale_log2, true, k0, pend, anc, lim, st.m, raw, mx);
+  } else {
+    grow = tile_scores<RB, MK, TREE>(sc, scale_log2, masked, k0, st.pend, st.anc, st.lim, st.m, raw, mx);
+  }
+  if (__builtin_expect(grow, 0)) tile_rescale<RB, D / 16>(mx, st.m, st.lsum, st.o);
+  bf16x8 pf[RB];
+  tile_probs<RB>(raw, scale_log2, st.m, st.lsum, pf);
+  bf16x8 vf[D / 16];
+  read_v_frags<D>(vsrc, tl, vf);
+  tile_pv<RB, D>(st, pf, vf);
+}
+
+// K fragments of a tile staged in LDS.
+template <int D>
+__device__ __forceinline__ void read_k_frags(const unsigned char* __restrict__ ksrc, const TileLane<D>& tl,
+                                             bf16x8 (&kf)[2][D / 32]) {
+  using T = Tile<D>;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int ds = 0; ds < D / 32; ++ds)
+      kf[kb][ds] = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(ksrc + tl.kread[ds & 1] + T::k_read_imm(kb, ds)));
 }
 
 // Item of wave `wave` in workgroup blockIdx.x: (chunk, KV head), KV head
 // fastest.  Returns false past the last item.
 __device__ __forceinline__ bool attn_item(const AttnShape& s, const AttnBatch& bt, int& c_local, int& g) {
-  const int item = blockIdx.x * kAttnWaves + (threadIdx.x >> 6);
+  const int item = blockIdx.x * kAttnWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   c_local = item / s.Hkv;
   g = item - c_local * s.Hkv;
   return c_local < bt.chunk_prefix[bt.nreq];
@@ -386,63 +553,107 @@ __global__ __launch_bounds__(kAttnThreads, 1)
 void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
                       const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
                       AttnPartials parts) {
-  constexpr int DS = D / 32;  // 32-wide steps of the q.k contraction
-  constexpr int DB = D / 16;  // 16-wide blocks of the output
-  using KT = KVTile<D, false>;
-  using VT = KVTile<D, true>;
-  constexpr size_t kStage = (size_t)kAttnWaves * kTile * D * 2;  // one stage of K or V, all waves
-  // Two stages of K and V tiles, each its own object.
-  __shared__ __align__(16) unsigned char ks0[kStage];
-  __shared__ __align__(16) unsigned char ks1[kStage];
-  __shared__ __align__(16) unsigned char vs0[kStage];
-  __shared__ __align__(16) unsigned char vs1[kStage];
+  using T = Tile<D>;
+  constexpr int kStage = kAttnWaves * T::kBytes;  // one stage of K or V, all waves
+  constexpr int kDmas = 2 * T::kBlocks;           // DMA instructions per tile (K and V)
+  // Two stages of K and V tiles.
+  __shared__ __align__(1024) unsigned char kst[2 * kStage];
+  __shared__ __align__(1024) unsigned char vst[2 * kStage];
 
   int c_local, g;
   if (!attn_item(s, bt, c_local, g)) return;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int lr = lane & 15;  // row (or column) within a 16-block
-  const int lg = lane >> 4;  // lane group: k-slice of MFMA operands
 
-  const int b = find_request(bt, c_local);
-  const int L = bt.kv_len[b];
+  // The item's scalars are wave-uniform; readfirstlane lets the compiler
+  // keep them (and the loop control and tile pointers built from them) in
+  // scalar registers.
+  const int b = __builtin_amdgcn_readfirstlane(find_request(bt, c_local));
+  const int L = __builtin_amdgcn_readfirstlane(bt.kv_len[b]);
   const int req = bt.req0 + b;
-  const int k_begin = (c_local - bt.chunk_prefix[b]) * s.chunk_keys;
+  const int k_begin = __builtin_amdgcn_readfirstlane((c_local - bt.chunk_prefix[b]) * s.chunk_keys);
   const int k_end = min(L, k_begin + s.chunk_keys);
   const KVSrc<D, PAGED> src = kv_src<D, PAGED>(s, bt, kp, vp, b, g, L, k_begin);
 
   AttnRows<RB, D> st;
   init_rows<RB, D>(st, s, bt.anc, q, req, g, L, 0);
 
-  // Tile i of the item starts at key k_begin + 32i; the load past the last
-  // tile is dead (one cache line per instruction, never folded in).  Tile i+1 loads while
-  // tile i is folded in; the two stages swap after every tile.
+  // Tile i of the item starts at key k_begin + 32i and is staged in stage
+  // i & 1; tile i + 1 loads while tile i is folded in.  (Loading two tiles
+  // ahead, with the fragments moved to registers first to free the stage,
+  // measured slower: the CU's outstanding-miss limit, not the depth of a
+  // wave's prefetch, bounds the stream, and a longer queue of DMAs only
+  // delays the wave at issue.)  Every row sees every key up to L - G (the root's
+  // position), so the tiles that end there or before take no mask; the rest
+  // (the last few tiles of the request's last chunk, including a partial tile
+  // reaching past L - 1, whose missing rows repeat row L - 1 and are masked)
+  // do.
   const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
-  unsigned char* k0s = ks0 + wave * KT::kBytes;
-  unsigned char* k1s = ks1 + wave * KT::kBytes;
-  unsigned char* v0s = vs0 + wave * VT::kBytes;
-  unsigned char* v1s = vs1 + wave * VT::kBytes;
-  auto key0 = [&](int i) { return k_begin + min(i, ntiles - 1) * kTile; };
-  const int64_t t0 = src.tile(key0(0));
-  KT::load(src.k + t0, key0(0), L, k0s, lane);
-  VT::load(src.v + t0, key0(0), L, v0s, lane);
-  for (int i = 0; i < ntiles; ++i) {
-    const int64_t tn = src.tile(key0(i + 1));
-    attn_step<RB, D, TREE>(st, s.scale_log2, src.k + tn, src.v + tn, L, key0(i + 1), i + 1 >= ntiles, key0(i),
-                           key0(i) + kTile - 1 > L - s.G, k1s, v1s, k0s, v0s);
-    unsigned char* t = k0s;
-    k0s = k1s;
-    k1s = t;
-    t = v0s;
-    v0s = v1s;
-    v1s = t;
+  const int nplain = min(ntiles, max(0, (L - s.G + 1 - k_begin) / kTile));
+  const uint32_t kl0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)kst + wave * T::kBytes;
+  const uint32_t vl0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)vst + wave * T::kBytes;
+  const TileLane<D> tl(lane);
+  auto issue = [&](int i) {
+    const int k0 = k_begin + i * kTile;
+    const int64_t t = src.tile(k0);
+    const uint32_t so = (uint32_t)(i & 1) * kStage;
+    dma_tile<D>(src.k + t, src.v + t, kl0 + so, vl0 + so, tl, L - 1 - k0);
+  };
+  // The reference maxima never move by a rescale of O here (a rescale branch
+  // in this loop made the compiler copy O between register files on every
+  // tile).  The first tile sets them (nothing is accumulated yet); after
+  // that p = 2^(s*scale - m) may exceed 1 by up to 2^kRestartLog2, far inside
+  // float32 range for O and the sums.  A row whose maximum grows beyond that
+  // restarts the item from its first tile with the grown maxima and O, sums
+  // cleared.  Each restart raises a reference by more than kRestartLog2, so
+  // restarts are finitely many (none for scores of any ordinary range).
+  for (;;) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      st.lsum[rb] = 0.f;
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) st.o[rb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    issue(0);
+    bool fresh = true, restart = false;
+    for (int i = 0; i < ntiles; ++i) {
+      if (i + 1 < ntiles) {
+        issue(i + 1);  // into the stage tile i - 1 was read from
+        wait_vmcnt<kDmas>();  // tile i landed
+      } else {
+        wait_vmcnt<0>();
+      }
+      const int so = (i & 1) * kStage + wave * T::kBytes;
+      bf16x8 kf[2][D / 32];
+      read_k_frags<D>(kst + so, tl, kf);
+      f32x4 sc[RB][2];
+      tile_qk<RB, D>(st, kf, sc);
+      float raw[RB][8], mx[RB];
+      const bool grow = tile_scores<RB, kMaskRuntime, TREE>(sc, s.scale_log2, i >= nplain, k_begin + i * kTile,
+                                                            st.pend, st.anc, st.lim, st.m, raw, mx,
+                                                            fresh ? 0.f : kRestartLog2);
+      if (grow) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) st.m[rb] = fmaxf(st.m[rb], mx[rb]);
+        if (!fresh) {
+          restart = true;
+          break;
+        }
+      }
+      fresh = false;
+      bf16x8 pf[RB], vf[D / 16];
+      tile_probs<RB>(raw, s.scale_log2, st.m, st.lsum, pf);
+      read_v_frags<D>(vst + so, tl, vf);
+      tile_pv<RB, D>(st, pf, vf);
+    }
+    if (!restart) break;
+    wait_vmcnt<0>();  // the tile after the one that restarted may still be in flight
   }
-  wait_vmcnt<0>();
   write_partial<RB, D>(s, bt, parts, c_local, g, st.m, st.lsum, st.o);
 }
 
-// Register-staged variant: whole K and V rows go HBM -> registers ->
-// wave-private LDS tiles (rotated rows) -> MFMA fragments.  All loads land in
+// Register-staged variant: K and V blocks go HBM -> registers -> the wave's
+// LDS tiles in the staging layout -> MFMA fragments.  All loads land in
 // registers, so the compiler's own vmcnt accounting covers the pipeline, and
 // two tiles of each wave are in flight while it folds.  With one 16-row block
 // (multi-head attention) two workgroups share a CU.
@@ -451,23 +662,23 @@ __global__ __launch_bounds__(kAttnThreads, (RB == 1 ? 2 : 1))
 void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __restrict__ q,
                           const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
                           AttnPartials parts) {
-  constexpr int LPR = D / 8;       // lanes per row (16 bytes each)
-  constexpr int KPI = 64 / LPR;    // rows per wave-wide load
-  constexpr int NV = kTile / KPI;  // loads of K (and of V) per tile
-  using VT = KVTile<D, true>;
-  using KT = KVTile<D, false>;
-  __shared__ __align__(16) unsigned char vsm[kAttnWaves * VT::kBytes];
-  __shared__ __align__(16) unsigned char ksm[kAttnWaves * KT::kBytes];
+  using T = Tile<D>;
+  constexpr int NB = T::kBlocks;
+  __shared__ __align__(1024) unsigned char ksm[kAttnWaves * T::kBytes];
+  __shared__ __align__(1024) unsigned char vsm[kAttnWaves * T::kBytes];
 
   int c_local, g;
   if (!attn_item(s, bt, c_local, g)) return;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
 
-  const int b = find_request(bt, c_local);
-  const int L = bt.kv_len[b];
+  // The item's scalars are wave-uniform; readfirstlane lets the compiler
+  // keep them (and the loop control and tile pointers built from them) in
+  // scalar registers.
+  const int b = __builtin_amdgcn_readfirstlane(find_request(bt, c_local));
+  const int L = __builtin_amdgcn_readfirstlane(bt.kv_len[b]);
   const int req = bt.req0 + b;
-  const int k_begin = (c_local - bt.chunk_prefix[b]) * s.chunk_keys;
+  const int k_begin = __builtin_amdgcn_readfirstlane((c_local - bt.chunk_prefix[b]) * s.chunk_keys);
   const int k_end = min(L, k_begin + s.chunk_keys);
   const KVSrc<D, PAGED> src = kv_src<D, PAGED>(s, bt, kp, vp, b, g, L, k_begin);
 
@@ -475,34 +686,42 @@ void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
   init_rows<RB, D>(st, s, bt.anc, q, req, g, L, 0);
 
   const int ntiles = (k_end - k_begin + kTile - 1) / kTile;
-  unsigned char* vt = vsm + wave * VT::kBytes;
-  unsigned char* kt = ksm + wave * KT::kBytes;
+  unsigned char* kt = ksm + wave * T::kBytes;
+  unsigned char* vt = vsm + wave * T::kBytes;
   auto key0 = [&](int i) { return k_begin + min(i, ntiles - 1) * kTile; };
+  const TileLane<D> tl(lane);
 
-  // Whole K and V rows, KPI rows per wave-wide load (full cache lines),
-  // streamed with the nontemporal hint: every row is read once.
-  u32x4 kr[2][NV], vr[2][NV];
-  // A dead tile (past the item's last) has every lane read one cache line.
+  // Blocks of two tiles, streamed with the nontemporal hint (every row is
+  // read once).  A dead tile (past the item's last) has every lane read the
+  // tile's first 16 bytes (one cache line per load); rows past L - 1 repeat
+  // row L - 1.
+  u32x4 kr[2][NB], vr[2][NB];
   auto issue = [&](int set, int i) {
     const int k0 = key0(i);
     const bool dead = i >= ntiles;
-    const int64_t t = src.tile(k0);
+    const int last = L - 1 - k0;
+    const char* kb = reinterpret_cast<const char*>(src.k + src.tile(k0));
+    const char* vb = reinterpret_cast<const char*>(src.v + src.tile(k0));
 #pragma unroll
-    for (int it = 0; it < NV; ++it) {
-      const int row = dead ? 0 : (min(k0 + it * KPI + lane / LPR, L - 1) - k0) * D + (lane % LPR) * 8;
-      kr[set][it] = load_u32x4_stream(src.k + t + row);
-      vr[set][it] = load_u32x4_stream(src.v + t + row);
+    for (int n = 0; n < NB; ++n) {
+      const uint32_t ko = dead ? 0u : (last >= kTile - 1 ? T::block_global(n) + tl.kload[(n / T::kHalves) & 1]
+                                                         : T::k_load_clamped(lane, n, last));
+      const uint32_t vo = dead ? 0u : (last >= kTile - 1 ? T::block_global(n) + tl.vload
+                                                         : T::v_load_clamped(lane, n, last));
+      kr[set][n] = load_u32x4_stream(kb + ko);
+      vr[set][n] = load_u32x4_stream(vb + vo);
     }
   };
   // Fold tile (set, k0) into the running state; live == false masks it.
   auto fold = [&](int set, int k0, bool live) {
 #pragma unroll
-    for (int it = 0; it < NV; ++it) {
-      const int r = it * KPI + lane / LPR, d = (lane % LPR) * 8;
-      *reinterpret_cast<u32x4*>(kt + KT::at(r, d)) = kr[set][it];
-      *reinterpret_cast<u32x4*>(vt + VT::at(r, d)) = vr[set][it];
+    for (int n = 0; n < NB; ++n) {
+      *reinterpret_cast<u32x4*>(kt + n * 1024 + lane * 16) = kr[set][n];
+      *reinterpret_cast<u32x4*>(vt + n * 1024 + lane * 16) = vr[set][n];
     }
-    attn_fold<RB, D, TREE>(st, s.scale_log2, k0, k0 + kTile - 1 > L - s.G, kt, vt, live);
+    bf16x8 kf[2][D / 32];
+    read_k_frags<D>(kt, tl, kf);
+    attn_fold<RB, D, TREE, kMaskRuntime>(st, s.scale_log2, k0, k0 + kTile - 1 > L - s.G, kf, vt, tl, live);
   };
 
   // Tile i+1 loads while tile i is folded in; the body always folds two
@@ -702,6 +921,28 @@ int attn_chunk_keys(int dtype, int rows, int Hkv, const int32_t* kv_len, int B) 
       for (int b = 0; b < B; ++b) items += (kv_len[b] + r - 1) / r;
       if ((items * Hkv + kAttnWaves - 1) / kAttnWaves <= kRoundWorkgroups) return r;
     }
+  }
+  if (rows > 16 && kv_len != nullptr) {
+    // The multi-block kernel runs one workgroup (four near-equal items) per
+    // CU, so a launch takes ceil(workgroups / CUs) rounds of one item each:
+    // a chunk count just past a multiple of the CU count leaves most CUs idle
+    // in the last round.  Among chunks at least as long as the default (so
+    // the workspace bound still holds), take the one with the shortest
+    // rounds * (chunk + per-item start-up) estimate.
+    const int64_t cus = device_cu_count();
+    int best = def;
+    int64_t best_t = INT64_MAX;
+    for (int c2 = def; c2 <= kMaxChunkKeys; c2 += kTile) {
+      int64_t chunks = 0;
+      for (int b = 0; b < B; ++b) chunks += (kv_len[b] + c2 - 1) / c2;
+      const int64_t wgs = (chunks * Hkv + kAttnWaves - 1) / kAttnWaves;
+      const int64_t t = (wgs + cus - 1) / cus * (c2 + kItemStartKeys);
+      if (t < best_t) {
+        best_t = t;
+        best = c2;
+      }
+    }
+    return best;
   }
   return def;
 }
