@@ -190,14 +190,24 @@ def accept_resample_sampled(logits, q_draft, draft, u, temperature, top_k=0, top
     return out
 
 
-def near_threshold(trace: AcceptTrace, band: float = 1e-6) -> bool:
-    """True when a draw lies within ``band`` of a decision boundary: an evaluated
-    test with |u - ratio| < band, or a final draw with u*Z within band*Z of the
+# Decision bands of the comparison with another implementation: a ratio test
+# whose draw lies within RATIO_BAND of its threshold, or a final draw whose
+# u * Z lies within FINAL_BAND * Z of an end of the chosen token's CDF
+# interval, may legitimately go either way under a different (correct)
+# rounding of p.  The final-draw band covers an inverse CDF built in float64
+# from float64 values of p (relative differences of order 1e-13 of Z).
+RATIO_BAND = 1e-6
+FINAL_BAND = 1e-9
+
+
+def near_threshold(trace: AcceptTrace, band: float = RATIO_BAND, final_band: float = FINAL_BAND) -> bool:
+    """True when a draw lies within a decision band: an evaluated test with
+    |u - ratio| < band, or a final draw with u*Z within final_band*Z of the
     chosen token's CDF interval ends."""
     for ui, ri in zip(trace.draws, trace.ratios):
         if math.isfinite(ri) and abs(ui - ri) < band:
             return True
     z = trace.z
-    if (trace.threshold - trace.c_before) < band * z or (trace.c_at - trace.threshold) < band * z:
+    if (trace.threshold - trace.c_before) < final_band * z or (trace.c_at - trace.threshold) < final_band * z:
         return True
     return False

@@ -38,6 +38,8 @@ from typing import List, Tuple
 
 import numpy as np
 
+from .accept import FINAL_BAND, RATIO_BAND
+
 
 def ancestor_masks(parent) -> np.ndarray:
     """[G] uint64: bit a of mask[g] is set iff position a is position g itself,
@@ -191,14 +193,16 @@ def accept_tree(logits_or_probs, row_lse, tokens, parent, u, kv_len=None):
             "traces": traces}
 
 
-def tree_near_threshold(trace, band: float = 1e-6) -> bool:
+def tree_near_threshold(trace, band: float = RATIO_BAND, final_band: float = FINAL_BAND) -> bool:
     """A draw within ``band`` of a test threshold, or the final draw within
-    band * Z of the chosen token's CDF interval ends."""
+    final_band * Z of the chosen token's CDF interval ends (the bands of
+    ``oracle.accept``)."""
     for ui, thr in trace["tests"]:
         if 0.0 < thr and abs(ui - thr) < band:
             return True
     z = trace["z"]
-    return (trace["threshold"] - trace["c_before"]) < band * z or (trace["c_at"] - trace["threshold"]) < band * z
+    return ((trace["threshold"] - trace["c_before"]) < final_band * z
+            or (trace["c_at"] - trace["threshold"]) < final_band * z)
 
 
 def tree_commit_kv(k_pool, v_pool, kv_off, kv_len, n_kv_heads, head_dim, out_node, accept_len, N):

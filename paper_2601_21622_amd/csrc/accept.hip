@@ -17,8 +17,7 @@
 // prefix-sums the segment totals (Z is the last), finds the segment holding
 // u * Z, scans it in token order for the first entry whose running sum
 // exceeds u * Z, and writes the emitted tokens and the new cache length.
-// p(v) = exp(logit - lse) keeps the difference exact (TwoSum) so its error is
-// a few float32 ulp, far below the 1e-6 decision band.
+// p(v) = exp(logit - lse) is evaluated in float64 from the float32 inputs.
 #include <hip/hip_ext.h>
 #include <string.h>
 
@@ -62,12 +61,17 @@ struct RowP {
   int argmax;
 };
 
+// p(v) in float64 from the row's float32 entry: the difference (or product
+// and difference) of float32 operands is exact in float64, so p is within an
+// ulp of float64 of exp(logit - lse) -- the value a float64 evaluation of the
+// same inputs gives -- and the inverse CDF built from it agrees with one to
+// about 1e-13 of Z.  A masked logit (-inf) gives 0.
 template <int PM>
-__device__ __forceinline__ float p_of(const RowP& rp, float x, int v) {
-  if (PM == kProbs) return x;
-  if (PM == kLogits) return exp_diff(x, rp.lse);
-  const float w = order_key(x) >= rp.theta ? exp_diff(x * rp.inv_t, rp.lse) : 0.f;
-  return v == rp.argmax ? 1.f : w;
+__device__ __forceinline__ double p_of(const RowP& rp, float x, int v) {
+  if (PM == kProbs) return (double)x;
+  if (PM == kLogits) return exp((double)x - (double)rp.lse);
+  const double w = order_key(x) >= rp.theta ? exp((double)x * (double)rp.inv_t - (double)rp.lse) : 0.0;
+  return v == rp.argmax ? 1.0 : w;
 }
 
 __device__ __forceinline__ RowP row_p(const AcceptArgs& a, int64_t row, float lse) {
@@ -105,23 +109,23 @@ __device__ __forceinline__ void segment_issue(const float* xrow, const float* qr
 
 template <int PM, bool RES>
 __device__ __forceinline__ void segment_finish(const RowP& rp, int V, int sg, const float (&xs)[kPerLane],
-                                               const float (&qs)[kPerLane], float (&r)[kPerLane]) {
+                                               const float (&qs)[kPerLane], double (&r)[kPerLane]) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int e = 0; e < kPerLane; ++e) {
     const int v = sg * kSeg + e * kWave + lane;
-    float pv = p_of<PM>(rp, xs[e], v);
+    double pv = p_of<PM>(rp, xs[e], v);
     if (RES) {
-      const float d = pv - qs[e];
-      pv = d > 0.f ? d : 0.f;
+      const double d = pv - (double)qs[e];
+      pv = d > 0.0 ? d : 0.0;
     }
-    r[e] = v < V ? pv : 0.f;
+    r[e] = v < V ? pv : 0.0;
   }
 }
 
 template <int PM, bool RES>
 __device__ __forceinline__ void segment_r(const float* xrow, const float* qrow, const RowP& rp, int V, int sg,
-                                          float (&r)[kPerLane]) {
+                                          double (&r)[kPerLane]) {
   float xs[kPerLane], qs[kPerLane];
   segment_issue<RES>(xrow, qrow, V, sg, xs, qs);
   segment_finish<PM, RES>(rp, V, sg, xs, qs, r);
@@ -131,7 +135,7 @@ __device__ __forceinline__ int p_mode(const AcceptArgs& a) {
   return a.warp != nullptr ? kWarped : (a.lse != nullptr ? kLogits : kProbs);
 }
 
-__device__ __forceinline__ float p_of_mode(const AcceptArgs& a, const RowP& rp, float x, int v) {
+__device__ __forceinline__ double p_of_mode(const AcceptArgs& a, const RowP& rp, float x, int v) {
   switch (p_mode(a)) {
     case kWarped: return p_of<kWarped>(rp, x, v);
     case kLogits: return p_of<kLogits>(rp, x, v);
@@ -140,7 +144,7 @@ __device__ __forceinline__ float p_of_mode(const AcceptArgs& a, const RowP& rp, 
 }
 
 __device__ __forceinline__ void segment_load(const AcceptArgs& a, const float* xrow, const float* qrow, const RowP& rp,
-                                             bool residual, int sg, float (&r)[kPerLane]) {
+                                             bool residual, int sg, double (&r)[kPerLane]) {
   switch (p_mode(a)) {
     case kWarped:
       if (residual) segment_r<kWarped, true>(xrow, qrow, rp, a.V, sg, r);
@@ -157,10 +161,10 @@ __device__ __forceinline__ void segment_load(const AcceptArgs& a, const float* x
 }
 
 // Float64 sum of one segment: per lane in order of e, then across the lanes.
-__device__ __forceinline__ double segment_total(const float (&r)[kPerLane]) {
+__device__ __forceinline__ double segment_total(const double (&r)[kPerLane]) {
   double acc = 0.0;
 #pragma unroll
-  for (int e = 0; e < kPerLane; ++e) acc += (double)r[e];
+  for (int e = 0; e < kPerLane; ++e) acc += r[e];
   return wave_sum_f64(acc);
 }
 
@@ -182,7 +186,7 @@ __device__ __forceinline__ void segment_totals_t(const float* xrow, const float*
     for (int k = 0; k < kSegBatch; ++k) {
       const int sg = s0 + k * nwaves;
       if (sg >= sg1) break;
-      float r[kPerLane];
+      double r[kPerLane];
       segment_finish<PM, RES>(rp, V, sg, xs[k], qs[k], r);
       const double t = segment_total(r);
       if (lane == 0) out[sg] = t;
@@ -372,7 +376,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   // The p of each rejected candidate, evaluated as the segment sums did, is
   // taken out of its segment (in candidate order, so deterministically).
   __shared__ int s_rej[kWave];
-  const double rej_p = (tree && rej >= 0) ? (double)p_of_mode(a, rp, xrow[rej], rej) : 0.0;
+  const double rej_p = (tree && rej >= 0) ? p_of_mode(a, rp, xrow[rej], rej) : 0.0;
   s_rej[lane] = rej;
   lds_wait();
   for (int k = 0; k < nrej; ++k) {
@@ -421,14 +425,14 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   }
   int t = -1;
   if (found >= 0) {
-    float rv[kPerLane];
+    double rv[kPerLane];
     segment_load(a, xrow, qrow, rp, residual, found, rv);
     double c = found > 0 ? seg[found - 1] : 0.0;
     int last_pos = -1;
 #pragma unroll
     for (int e = 0; e < kPerLane; ++e) {
       const int v = found * kSeg + e * kWave + lane;
-      const double r = excluded(v) ? 0.0 : (double)rv[e];
+      const double r = excluded(v) ? 0.0 : rv[e];
       const double cum = wave_inclusive_scan_f64(r) + c;
       const unsigned long long hit = __ballot(v < a.V && r > 0.0 && cum > thr);
       if (hit && t < 0) t = found * kSeg + e * kWave + __ffsll(hit) - 1;
@@ -441,10 +445,10 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   if (t < 0) {
     // No prefix sum exceeds u * Z: the largest token with mass.
     for (int sg = nseg - 1; sg >= 0 && t < 0; --sg) {
-      float rv[kPerLane];
+      double rv[kPerLane];
       segment_load(a, xrow, qrow, rp, residual, sg, rv);
       for (int e = kPerLane - 1; e >= 0 && t < 0; --e) {
-        const unsigned long long pos = __ballot(rv[e] > 0.f && !excluded(sg * kSeg + e * kWave + lane));
+        const unsigned long long pos = __ballot(rv[e] > 0.0 && !excluded(sg * kSeg + e * kWave + lane));
         if (pos) t = sg * kSeg + e * kWave + 63 - __clzll(pos);
       }
     }

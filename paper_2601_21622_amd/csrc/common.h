@@ -52,21 +52,6 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const void* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
 }
 
-// The same DMA issued from inline assembly: the compiler neither tracks it
-// nor inserts waits for it, so the kernel's own vmcnt waits alone order it
-// against the LDS reads (the compiler's conservative handling of tracked LDS
-// DMA can otherwise drain every load in flight before an unrelated LDS read).
-// It sets M0 itself: use it only in kernels that leave M0 to it (no other LDS
-// DMA, no indexed register moves).
-// The load carries the nontemporal hint: the data is read once.
-__device__ __forceinline__ void dma_16B_to_lds_opaque(const void* g, void* lds) {
-  const uint32_t l = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds;
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt"
-               :
-               : "s"(__builtin_amdgcn_readfirstlane(l)), "v"(g)
-               : "memory");
-}
-
 // s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -194,13 +179,15 @@ __device__ __forceinline__ void lds_wait() {
 }
 
 // exp(a - b), with a - b carried exactly as s + err (TwoSum), so that the
-// result is within a few float32 ulp of the exact exp(a - b).
+// result is within a few float32 ulp of the exact exp(a - b).  A masked
+// entry (a = -inf, finite b) gives exactly 0: there s = -inf and err is NaN
+// ((-inf) - (-inf)), so the correction is skipped whenever exp(s) is 0.
 __device__ __forceinline__ float exp_diff(float a, float b) {
   const float s = a - b;
   const float bb = s - a;
   const float err = (a - (s - bb)) + (-b - bb);
   const float e = expf(s);
-  return fmaf(e, err, e);
+  return e == 0.f ? 0.f : fmaf(e, err, e);
 }
 
 // 32-bit key whose unsigned order is the order of the float32 values (-0

@@ -105,10 +105,19 @@ def assert_close_rows(gpu: np.ndarray, ref: np.ndarray, rtol: float, what: str):
     return float((err / np.maximum(np.abs(r), rms)).max())
 
 
+def max_excluded(batch: int) -> int:
+    """Requests a parity test may set aside as near-threshold: a draw falls
+    within 1e-6 of a boundary with probability of order 1e-5 per request, so
+    more than max(1, 1% of the batch) means the band helper over-fires."""
+    return max(1, batch // 100)
+
+
 def assert_accept_parity(gpu_len, gpu_tok, gpu_new, ref, band=1e-6):
     """Bit-exact accept lengths, emitted tokens and new lengths, excluding
-    requests whose draws fall within ``band`` of a decision boundary."""
+    requests whose draws fall within ``band`` of a decision boundary (at most
+    max_excluded of them)."""
     near = np.array([near_threshold(t, band) for t in ref["traces"]])
+    assert int(near.sum()) <= max_excluded(len(near)), f"{int(near.sum())} of {len(near)} requests near a boundary"
     keep = ~near
     assert np.array_equal(gpu_len[keep], ref["accept_len"][keep]), (gpu_len, ref["accept_len"])
     assert np.array_equal(gpu_tok[keep], ref["out_tok"][keep]), (gpu_tok, ref["out_tok"])

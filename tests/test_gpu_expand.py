@@ -19,7 +19,7 @@ import torch
 import paper_2601_21622_amd as sd
 from oracle import expand_layer, full_tree_layout
 
-from gpu_util import announce, tensor, to_np
+from gpu_util import announce, max_excluded, tensor, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -105,7 +105,32 @@ def test_full_tree_then_tree_acceptance():
     sd.sd_accept_tree(dims, tensor(logits), tensor(lse), tok, par, tensor(u), None, acc, otok, onode, None, ws)
     torch.cuda.synchronize()
     ref = accept_tree(logits, lse, rt, rp, u)
-    keep = ~np.array([tree_near_threshold(t) for t in ref["traces"]])
+    near = np.array([tree_near_threshold(t) for t in ref["traces"]])
+    assert int(near.sum()) <= max_excluded(len(near))
+    keep = ~near
     assert np.array_equal(to_np(acc)[keep], ref["accept_len"][keep])
     assert np.array_equal(to_np(otok)[keep], ref["out_tok"][keep])
     announce(f"expanded tree: {N} nodes, accept lengths {to_np(acc).tolist()}")
+
+
+def test_expand_masked_children():
+    """Every token is a child (k = V), so masked (-inf) tokens are among them:
+    their draft probability is exactly 0, the others match the oracle."""
+    rng = np.random.default_rng(1234)
+    B, F, V = 3, 2, 9
+    x = (rng.standard_normal((B, F, V)) * 2.0).astype(np.float32)
+    x[:, :, [2, 7]] = -np.inf
+    k = V
+    frontier0, first = 0, F
+    N = first + F * k
+    tok, par, q = _run_layer(x, k, frontier0, first, N)
+    torch.cuda.synchronize()
+    rt, rp, rq = expand_layer(x, k, frontier0, first, N)
+    assert np.array_equal(to_np(tok), rt)
+    assert np.array_equal(to_np(par), rp)
+    gq = to_np(q).astype(np.float64)
+    sl = slice(first, N)
+    assert np.all(np.isfinite(gq[:, sl]))
+    masked = np.isin(to_np(tok)[:, sl], [2, 7])
+    assert np.all(gq[:, sl][masked] == 0.0) and np.all(rq[:, sl][masked] == 0.0)
+    assert np.all(np.abs(gq[:, sl] - rq[:, sl]) <= 2e-6 * rq[:, sl] + 1e-30)

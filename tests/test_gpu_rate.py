@@ -110,3 +110,18 @@ def test_rate_is_deterministic_and_exact_cases():
     got, ref = _run(B, gamma, V, logits, lse, q_same, True)
     assert np.abs(got - ref).max() <= 1e-12
     assert np.abs(got - 1.0).max() <= 1e-5
+
+
+def test_rate_with_masked_logits():
+    """-inf logits (masked tokens) have p = 0, so they add nothing to
+    sum min(p, q) even where q > 0."""
+    B, gamma, V = 6, 4, 3000
+    logits, _, q = _inputs(91, B, gamma, V, (0.5, 2.0))
+    rng = np.random.default_rng(92)
+    logits[rng.random(logits.shape) < 0.35] = -np.inf
+    l64 = logits.astype(np.float64)
+    mx = l64.max(axis=1, keepdims=True)
+    lse = (mx[:, 0] + np.log(np.exp(l64 - mx).sum(axis=1))).astype(np.float32)
+    got, ref = _run(B, gamma, V, logits, lse, q, False)
+    assert np.all(np.isfinite(got))
+    assert float(np.abs(got - ref).max()) <= 1e-6

@@ -24,7 +24,7 @@ import paper_2601_21622_amd as sd
 from oracle import accept_resample_sampled, order_keys, warp_row
 from workloads import get_config, make_inputs
 
-from gpu_util import DeviceBatch, announce, assert_accept_parity, to_np
+from gpu_util import DeviceBatch, announce, assert_accept_parity, max_excluded, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -86,6 +86,7 @@ def _check_cut(logits, T, k, p, gpu_lse, gpu_min):
             continue
         assert abs(float(gpu_lse[r]) - wr.lse) <= 1e-5 * max(1.0, abs(wr.lse)), (r, gpu_lse[r], wr.lse)
     assert bad_cut == 0, f"{bad_cut} rows cut differently from the oracle outside the band"
+    assert flagged <= max_excluded(logits.shape[0]), f"{flagged} rows with a top-p cut in the band"
     return flagged
 
 
