@@ -29,6 +29,7 @@ from ._binding import (  # noqa: F401
     library,
     library_path,
     prepare_acceptance_rate,
+    prepare_verify_attention,
     prepare_verify_step,
     prepare_verify_step_paged,
     prepare_verify_step_sampled,

@@ -238,14 +238,25 @@ def sd_pack_vocab(dims: Dims, w_vocab, w_packed, stream=None) -> None:
     _check(st, "sd_pack_vocab")
 
 
-def sd_verify_attention(dims: Dims, q, k_pool, v_pool, kv_off: Sequence[int], kv_len: Sequence[int],
-                        scale: float, out, workspace, stream=None) -> None:
+def _attn_args(dims: Dims, q, k_pool, v_pool, kv_off: Sequence[int], kv_len: Sequence[int], scale: float, out,
+               workspace, stream=None):
     _off, off_p = _host(kv_off, np.int64)
     _len, len_p = _host(kv_len, np.int32)
-    st = library().sd_verify_attention(ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p,
-                                       float(scale), _ptr(out), _ptr(workspace), _nbytes(workspace),
-                                       _stream(stream))
-    _check(st, "sd_verify_attention")
+    args = (ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p, float(scale), _ptr(out),
+            _ptr(workspace), _nbytes(workspace), _stream(stream))
+    return args, (_off, _len)
+
+
+def sd_verify_attention(dims: Dims, q, k_pool, v_pool, kv_off: Sequence[int], kv_len: Sequence[int],
+                        scale: float, out, workspace, stream=None) -> None:
+    args, _keep = _attn_args(dims, q, k_pool, v_pool, kv_off, kv_len, scale, out, workspace, stream)
+    _check(library().sd_verify_attention(*args), "sd_verify_attention")
+
+
+def prepare_verify_attention(*a, **kw) -> "PreparedCall":
+    """sd_verify_attention with the same arguments, converted once (see PreparedCall)."""
+    args, keep = _attn_args(*a, **kw)
+    return PreparedCall(library().sd_verify_attention, args, (keep, a, kw), "sd_verify_attention")
 
 
 def sd_verify_attention_tree(dims: Dims, q, k_pool, v_pool, kv_off: Sequence[int], kv_len: Sequence[int], parent,

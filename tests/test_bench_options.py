@@ -17,10 +17,32 @@ def _cfg(*argv):
     return bench.workload_config(bench.parser().parse_args(list(argv)), get_config)
 
 
-def test_default_workload_is_the_chain_step():
+def test_default_workload_is_the_largest_single_gpu_share():
     cfg, problem = _cfg()
     assert problem is None
-    assert cfg.name == "vicuna7b" and cfg.gamma == get_config("vicuna7b").gamma
+    assert cfg.name == "llama70b_share" and cfg.gamma == get_config("llama70b_share").gamma
+
+
+def test_counter_digest_covers_included_headers():
+    files = bench.source_files("attention.hip")
+    assert files[0] == "attention.hip"
+    assert {"common.h", "launch.h", "combine.h"} <= set(files)
+    assert len(files) == len(set(files))
+    assert bench.source_digest("attention.hip") != bench.source_digest("vocab.hip")
+
+
+def test_cpu_baseline_is_bounded_and_reports_stages():
+    from workloads import make_inputs
+
+    x = make_inputs(get_config("vicuna7b").replace(batch=3, n_q_heads=4, n_kv_heads=2, hidden=512, vocab=3000,
+                                                   lengths=("explicit", (40, 90, 70))))
+    out = bench.cpu_baseline(x, budget_s=0.0)          # stops after the first request
+    assert out["requests"] == 1 and out["kind"] == "oracle"
+    assert out["cores"] == len(os.sched_getaffinity(0))
+    assert set(out["stage_s"]) == {"attention", "logits_softmax", "accept"}
+    assert out["value"] > 0 and out["cpu_model"]
+    full = bench.cpu_baseline(x, budget_s=1e9)         # the whole batch
+    assert full["requests"] == 3
 
 
 @pytest.mark.parametrize("nodes", [15, 31, 63])
