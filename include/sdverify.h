@@ -216,6 +216,28 @@ SD_API int sd_verify_step(const sd_dims_t* dims, const void* q, const void* k_po
                    void* const* kernel_events);
 
 /*
+ * sd_verify_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The step's scratch is a static device
+ * array of SD_STATIC_SCRATCH_BYTES per device, which the library holds on
+ * every device it runs on until the process ends; the call itself allocates
+ * nothing.  Arguments, layout and results are those of sd_verify_step (no
+ * kernel events).  A problem whose step needs more scratch than
+ * SD_STATIC_SCRATCH_BYTES (sd_workspace_bytes gives an upper bound) returns
+ * SD_ERR_WORKSPACE before any device work.  Every call on one device shares
+ * that device's array: calls that overlap on one device (other streams,
+ * other host threads) race and must not be issued; calls in stream order are
+ * fine, and no part of the array needs clearing between them.
+ */
+#define SD_STATIC_SCRATCH_BYTES ((size_t)96 << 20)
+SD_API int sd_verify_step_static(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
+                                 const int64_t* kv_off, const int32_t* kv_len, float scale,
+                                 const void* hidden, const void* w_vocab, const float* q_draft,
+                                 const int32_t* draft_tok, const float* u, void* attn_out, float* logits,
+                                 float* row_lse, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
+                                 sd_stream_t stream);
+
+/*
  * Sampled verification.  The test and correction of sd_accept_resample run on
  * a warped target p' instead of p (the Leviathan test of Sec. 2 is lossless
  * with respect to whichever target it is given).  q_draft must then hold the

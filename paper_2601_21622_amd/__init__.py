@@ -47,6 +47,7 @@ from ._binding import (  # noqa: F401
     sd_verify_attention_tree,
     sd_verify_logits,
     sd_verify_step,
+    sd_verify_step_static,
     sd_verify_step_paged,
     sd_verify_step_sampled,
     sd_verify_step_tree,

@@ -118,6 +118,8 @@ def library() -> ctypes.CDLL:
     lib.sd_accept_resample.restype = ctypes.c_int
     lib.sd_verify_step.argtypes = [DP, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P, P]
     lib.sd_verify_step.restype = ctypes.c_int
+    lib.sd_verify_step_static.argtypes = [DP, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P, P, P]
+    lib.sd_verify_step_static.restype = ctypes.c_int
     lib.sd_verify_attention_tree.argtypes = [DP, P, P, P, P, P, P, F, P, P, SZ, P]
     lib.sd_verify_attention_tree.restype = ctypes.c_int
     lib.sd_accept_tree.argtypes = [DP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
@@ -382,6 +384,19 @@ def sd_verify_step(dims: Dims, q, k_pool, v_pool, kv_off, kv_len, scale: float, 
                              u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, workspace, stream,
                              kernel_events)
     _check(library().sd_verify_step(*args), "sd_verify_step")
+
+
+def sd_verify_step_static(dims: Dims, q, k_pool, v_pool, kv_off, kv_len, scale: float, hidden, w_vocab, q_draft,
+                          draft_tok, u, attn_out, logits, row_lse, accept_len, out_tok, new_kv_len,
+                          stream=None) -> None:
+    """sd_verify_step on the library's static per-device scratch (no workspace)."""
+    off, off_p = _host(kv_off, np.int64)
+    ln, len_p = _host(kv_len, np.int32)
+    st = library().sd_verify_step_static(ctypes.byref(dims), _ptr(q), _ptr(k_pool), _ptr(v_pool), off_p, len_p,
+                                         float(scale), _ptr(hidden), _ptr(w_vocab), _ptr(q_draft), _ptr(draft_tok),
+                                         _ptr(u), _ptr(attn_out), _ptr(logits), _ptr(row_lse), _ptr(accept_len),
+                                         _ptr(out_tok), _ptr(new_kv_len), _stream(stream))
+    _check(st, "sd_verify_step_static")
 
 
 def _step_sampled_args(dims, sampling, q, k_pool, v_pool, kv_off, kv_len, scale, hidden, w_vocab, q_draft,

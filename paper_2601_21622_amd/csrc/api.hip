@@ -13,6 +13,14 @@
 #include "combine.h"
 #include "launch.h"
 
+#include <mutex>
+
+// Scratch of sd_verify_step_static, for callers that cannot allocate: one
+// copy per device, kept until the process ends.  Host code never uses this
+// name as an address; it uses the device address hipGetSymbolAddress returns
+// for the current device (static_scratch below).
+static __device__ __align__(256) unsigned char scratch[SD_STATIC_SCRATCH_BYTES];
+
 namespace {
 
 using namespace sdv;
@@ -271,6 +279,44 @@ int verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const 
                 int32_t* new_kv_len, void* workspace, size_t workspace_bytes, sd_stream_t stream,
                 void* const* kernel_events);
 
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+int static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SD_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SD_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return SD_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SD_OK;
+}
+
+// Workspace of one step's attention partials for these lengths.
+size_t step_attention_ws(const sd_dims_t* dims, const int32_t* kv_len, float scale, const sd_kv_pages_t* pages) {
+  const AttnShape s = attn_shape(dims, scale, kv_len, pages != nullptr ? pages->page_size : 0);
+  return attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys));
+}
+
+// Workspace one step needs (arguments already checked).  With the caller's
+// hidden rows the projection does not read the attention output, so the
+// attention merge rides in the acceptance's last launch and its partials
+// keep their own region: [partials][projection][acceptance].  Otherwise the
+// stages reuse one region in stream order.
+size_t step_ws(const sd_dims_t* dims, const int32_t* kv_len, float scale, const void* hidden,
+               const sd_kv_pages_t* pages) {
+  const size_t attn_bytes = step_attention_ws(dims, kv_len, scale, pages);
+  return hidden != nullptr ? attn_bytes + logits_ws(dims) + accept_stage_ws(dims)
+                           : std::max(attn_bytes, logits_ws(dims) + accept_stage_ws(dims));
+}
+
 }  // namespace
 
 extern "C" {
@@ -420,17 +466,9 @@ int verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const 
   if (st != SD_OK) return st;
   st = pages != nullptr ? check_pages(dims, pages, kv_len) : check_kv(dims, kv_off, kv_len);
   if (st != SD_OK) return st;
-  const AttnShape s = attn_shape(dims, scale, kv_len, pages != nullptr ? pages->page_size : 0);
-  const size_t attn_bytes = attention_ws(dims, total_chunks(kv_len, dims->batch, s.chunk_keys));
-  // With the caller's hidden rows the projection does not read the attention
-  // output, so the attention merge rides in the acceptance's last launch and
-  // its partials keep their own region: [partials][projection][acceptance].
-  // Otherwise the stages reuse one region in stream order.
   const bool defer = hidden != nullptr;
-  const size_t base = defer ? attn_bytes : 0;
-  const size_t need = defer ? attn_bytes + logits_ws(dims) + accept_stage_ws(dims)
-                            : std::max(attn_bytes, logits_ws(dims) + accept_stage_ws(dims));
-  if (workspace_bytes < need) return SD_ERR_WORKSPACE;
+  const size_t base = defer ? step_attention_ws(dims, kv_len, scale, pages) : 0;
+  if (workspace_bytes < step_ws(dims, kv_len, scale, hidden, pages)) return SD_ERR_WORKSPACE;
 
   hipEvent_t ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   if (kernel_events != nullptr)
@@ -675,6 +713,27 @@ int sd_pack_vocab(const sd_dims_t* dims, const void* w_vocab, void* w_packed, sd
   const size_t nb = vocab_packed_bytes(dims->hidden, dims->vocab);
   if (a < b + nb && b < a + na) return SD_ERR_INVALID_ARGUMENT;  // overlapping buffers
   return hip_status(launch_pack_vocab(dims->hidden, dims->vocab, w_vocab, w_packed, static_cast<hipStream_t>(stream)));
+}
+
+int sd_verify_step_static(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
+                          const int64_t* kv_off, const int32_t* kv_len, float scale, const void* hidden,
+                          const void* w_vocab, const float* q_draft, const int32_t* draft_tok, const float* u,
+                          void* attn_out, float* logits, float* row_lse, int32_t* accept_len, int32_t* out_tok,
+                          int32_t* new_kv_len, sd_stream_t stream) {
+  // The checks the step's size depends on, then the size against the static
+  // maximum, on the host before anything touches a device.
+  int st = check_dims(dims);
+  if (st != SD_OK) return st;
+  st = check_kv(dims, kv_off, kv_len);
+  if (st != SD_OK) return st;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return SD_ERR_INVALID_ARGUMENT;
+  if (step_ws(dims, kv_len, scale, hidden, nullptr) > SD_STATIC_SCRATCH_BYTES) return SD_ERR_WORKSPACE;
+  void* ws = nullptr;
+  st = static_scratch(&ws);
+  if (st != SD_OK) return st;
+  return verify_step(dims, q, k_pool, v_pool, kv_off, nullptr, kv_len, scale, hidden, w_vocab, q_draft, draft_tok, u,
+                     attn_out, logits, row_lse, accept_len, out_tok, new_kv_len, ws, SD_STATIC_SCRATCH_BYTES, stream,
+                     nullptr);
 }
 
 const char* sd_status_string(int status) {

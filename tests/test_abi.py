@@ -31,7 +31,7 @@ def test_library_loads_and_exports_header_symbols():
                           "sd_acceptance_rate", "sd_verify_attention_paged", "sd_verify_step_paged",
                           "sd_kv_pool_create", "sd_kv_pool_destroy", "sd_kv_pool_reserve", "sd_kv_pool_truncate",
                           "sd_kv_pool_release", "sd_kv_pool_free_pages", "sd_kv_pool_tag_pages",
-                          "sd_kv_pool_block_table", "sd_expand_layer"}
+                          "sd_kv_pool_block_table", "sd_expand_layer", "sd_verify_step_static"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2
@@ -234,3 +234,27 @@ def test_binding_requires_device_tensors():
     d = dims()
     with pytest.raises((TypeError, ValueError)):
         sd.sd_verify_logits(d, torch.zeros(4), torch.zeros(4), torch.zeros(4), torch.zeros(4), torch.zeros(4))
+
+
+@cpu_only
+def test_static_step_rejects_before_any_device_work():
+    """The no-workspace step checks its arguments and its scratch need on the
+    host: a problem beyond the static maximum, a missing length table or a bad
+    scale return their status before the device is touched."""
+    lib = sd.library()
+    args = (P, P, P)
+
+    def call(d, off, ln, scale=0.088):
+        return lib.sd_verify_step_static(ctypes.byref(d), *args, off, ln, scale, P, P, P, P, P, P, P, P, P, P, P, None)
+
+    big = dims(batch=64, gamma=8, n_q_heads=64, n_kv_heads=8, hidden=8192, vocab=128256)
+    L = 32768
+    off = (ctypes.c_int64 * 64)(*[i * 8 * 128 * L for i in range(64)])
+    ln = (ctypes.c_int32 * 64)(*([L] * 64))
+    assert call(big, off, ln) == sd.SD_ERR_WORKSPACE
+    small = dims()
+    off2 = (ctypes.c_int64 * 2)(0, 8 * 128 * 2 * 64)
+    ln2 = (ctypes.c_int32 * 2)(64, 64)
+    assert call(small, off2, None) == sd.SD_ERR_INVALID_ARGUMENT
+    assert call(small, off2, ln2, scale=0.0) == sd.SD_ERR_INVALID_ARGUMENT
+    assert call(dims(head_dim=96), off2, ln2) == sd.SD_ERR_UNSUPPORTED
