@@ -77,6 +77,7 @@ struct VocabPlan {
   int mtiles;      // workgroups along the hidden rows
   int mblocks;     // bf16 row blocks per M-tile: of 16 rows (shallow), of 32 (deep)
   int nbw;         // 16-entry vocabulary blocks per wave (bf16)
+  int waves;       // waves per workgroup
   bool deep;       // bf16 deep-pipelined 32x32 schedule (more than 64 rows)
   bool packed;     // W in the fragment-order layout of launch_pack_vocab
 };

@@ -248,28 +248,38 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
 }
 
 // Deep schedule (more than 64 rows) on MFMA 32x32x16: the accumulators of up
-// to 448 rows pin one workgroup of four waves to a CU, and a single wave per
+// to 384 rows pin one workgroup of four waves to a CU, and a single wave per
 // SIMD keeps the 32x32 MFMA pipe full where the 16x16 one would stall.  The
 // workgroup covers MB blocks of 32 hidden rows and 4 x NB blocks of 32
 // vocabulary entries; wave w owns blocks (tile*4 + w)*NB .. +NB, i.e.
-// MB x NB accumulators of 16 registers.  K goes in 32-wide chunks of two
-// 16-wide MFMA steps.
+// MB x NB accumulators of 16 registers (at most 320).  K goes in 32-wide
+// chunks of two 16-wide MFMA steps.
 //
-// Pipeline, chunk c of the loop (kStages = 6, kAhead = 5):
-//   * issue chunk c+5: its hidden chunk goes straight from global memory into
-//     LDS buffer (c+5) % 6 (LDS DMA, no registers), its W fragments into the
-//     register ring slot (c+5) % 6; both slots last served chunk c-1, whose
-//     fragments every wave read before the previous step's barrier;
-//   * read the hidden fragments of chunk c+1 from LDS into registers;
-//   * multiply chunk c (W ring slot c % 6, fragments read one chunk earlier);
-//   * wait until this wave's DMA of chunk c+2 has landed, then barrier, so
-//     chunk c+2 is readable by every wave in the next step.
-// Memory operations complete in issue order, so the wait leaves the loads of
-// chunks c+3 .. c+5 (and the W of c+2) in flight: four chunks of W and three
-// of hidden are always on the way while the MFMAs run, and no MFMA waits on
-// an LDS read issued in the same step.  Loads past the last chunk re-read the
-// last chunk (in bounds) and chunks past the end multiply a zero W, which
-// keeps the loop free of branches around memory operations.
+// The rate that bounds this kernel is how fast one CU pulls lines in: a CU
+// keeps a bounded number of line misses in flight, so its inflow is that
+// number over the latency, and a W line (a miss to HBM) holds its place about
+// twice as long as a hidden line (an L2 hit).  Every workgroup reads its W
+// slice once and the whole M-tile of hidden rows once, so wider vocabulary
+// tiles cut the hidden bytes per CU; vocab_plan picks NB per shape.
+//
+// Pipeline over S stages, chunk c of the loop:
+//   * issue chunk c+S-1: its hidden chunk goes straight from global memory
+//     into LDS stage (c-1) % S (LDS DMA, no registers), its W fragments into
+//     register ring slot (c-1) % S; both slots last served chunk c-1, which
+//     every wave finished before the previous step's barrier;
+//   * multiply chunk c (ring slot c % S); its hidden fragments were read from
+//     LDS stage c % S during the previous step (one wave per SIMD), or are
+//     read now, a few MFMAs ahead of their first use (two waves per SIMD);
+//   * in the first case, read the fragments of chunk c+1 and wait until this
+//     wave's DMA of chunk c+2 has landed; in the second, wait until its loads
+//     of chunk c+1 have landed; then barrier, so that chunk is readable by
+//     every wave in the next step.
+// Memory operations complete in issue order, so the wait leaves the later
+// chunks in flight while the next one is multiplied, and no MFMA waits on an
+// LDS read issued in the same step when registers allow the read ahead.
+// Loads past the last chunk re-read the last chunk (in bounds) and chunks past
+// the end multiply a zero W, which keeps the loop free of branches around
+// memory operations.
 //
 // The hidden rows are first repacked (pack_hidden_kernel) into fragments of 32
 // rows x 16 k in lane order (lane l: row l%32, k 8*(l/32) .. +8), so every
@@ -277,24 +287,49 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
 // fragments (32 vocabulary rows x 16 k, same lane order) are read either from
 // the row-major [V][K] layout or gathered from the packed 16x16x32 fragment
 // layout.
-constexpr int kStages = 6;
-constexpr int kAhead = kStages - 1;  // chunks issued ahead of the one multiplied
-
-template <int MB, int NB>
+template <int MB, int NB, int S, int NW>
 struct Deep32Cfg {
   static constexpr int kRows = MB * 32;
-  static constexpr int kFrags = 2 * MB;               // hidden fragments per chunk
-  static constexpr int kDmaPerWave = (kFrags + 3) / 4;  // the same count on every wave
-  static constexpr int kBufBytes = 4 * kDmaPerWave * 1024;
+  static constexpr int kFrags = 2 * MB;                     // hidden fragments per chunk
+  static constexpr int kDmaPerWave = (kFrags + NW - 1) / NW;  // the same count on every wave
+  static constexpr int kBufBytes = NW * kDmaPerWave * 1024;
+  static constexpr int kAhead = S - 1;  // chunks issued ahead of the one multiplied
+  // With one wave per SIMD the hidden fragments of chunk c+1 are read into
+  // registers while chunk c is multiplied (two register sets of 2*MB
+  // fragments); with two waves per SIMD, whose registers hold no second
+  // set, each fragment is read a few MFMAs ahead of its first use and the
+  // other wave of the SIMD covers what latency is left.
+  static constexpr bool kNextChunk = NW == 4;
   // Memory operations a wave issues per chunk, and the most that may still be
-  // outstanding once the DMA of the chunk two steps ahead has landed (its W,
-  // then chunks c+3 .. c+kAhead).
+  // outstanding at the end of step c: once the hidden chunk c+2 has landed
+  // (its W, then chunks c+3 .. c+kAhead) when the next chunk's fragments are
+  // read ahead, else once chunk c+1 has landed (chunks c+2 .. c+kAhead).
   static constexpr int kOpsPerChunk = kDmaPerWave + 2 * NB;
-  static constexpr int kInFlight = 2 * NB + (kAhead - 2) * kOpsPerChunk;
+  static constexpr int kInFlight = kNextChunk ? 2 * NB + (kAhead - 2) * kOpsPerChunk : (kAhead - 1) * kOpsPerChunk;
+  static constexpr int kMfmas = 2 * MB * NB;  // per chunk and wave
+  // Just-in-time reads: fragments read ahead of the MFMA that first uses one.
+  static constexpr int kReadAhead = NB >= 4 ? 2 : (NB == 2 ? 3 : 5);
+  static_assert(S >= (kNextChunk ? 4 : 3) && S <= 6, "LDS stages");
+  static_assert(NW == 4 || NW == 8, "one or two waves per SIMD");
   static_assert(kInFlight <= 63, "vmcnt holds 6 bits");
+  static_assert(kOpsPerChunk <= kMfmas, "memory operations ride between MFMAs");
 };
 
-template <int MB, int NB>
+// Fixed-order combination of the NW per-wave values of row r.
+template <int NW, int R>
+__device__ __forceinline__ float waves_max(const float (*red)[R], int r) {
+  float x = fmaxf(fmaxf(red[0][r], red[1][r]), fmaxf(red[2][r], red[3][r]));
+  if (NW == 8) x = fmaxf(x, fmaxf(fmaxf(red[4][r], red[5][r]), fmaxf(red[6][r], red[7][r])));
+  return x;
+}
+template <int NW, int R>
+__device__ __forceinline__ float waves_sum(const float (*red)[R], int r) {
+  float x = (red[0][r] + red[1][r]) + (red[2][r] + red[3][r]);
+  if (NW == 8) x += (red[4][r] + red[5][r]) + (red[6][r] + red[7][r]);
+  return x;
+}
+
+template <int MB, int NB, int NW>
 __device__ __forceinline__ void tile_epilogue32(const f32x16 (&acc)[MB][NB], int M, int V, int ntiles, int tile,
                                                 int m0, int blk0, float* __restrict__ logits,
                                                 float2* __restrict__ partials, float (*red)[MB * 32]) {
@@ -335,7 +370,7 @@ __device__ __forceinline__ void tile_epilogue32(const f32x16 (&acc)[MB][NB], int
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     const int r = mb * 32 + j;
-    tmax[mb] = fmaxf(fmaxf(red[0][r], red[1][r]), fmaxf(red[2][r], red[3][r]));
+    tmax[mb] = waves_max<NW, MB * 32>(red, r);
   }
   __syncthreads();
 #pragma unroll
@@ -358,26 +393,28 @@ __device__ __forceinline__ void tile_epilogue32(const f32x16 (&acc)[MB][NB], int
       const int r = mb * 32 + j;
       const int m = m0 + r;
       if (m < M) {
-        const float sm = (red[0][r] + red[1][r]) + (red[2][r] + red[3][r]);
+        const float sm = waves_sum<NW, MB * 32>(red, r);
         partials[(int64_t)m * ntiles + tile] = make_float2(tmax[mb], sm);
       }
     }
   }
 }
 
-template <int MB, int NB, bool PACKED>
-__global__ __launch_bounds__(kVThreads, 1)
+template <int MB, int NB, int S, int NW, bool PACKED>
+__global__ __launch_bounds__(NW * kWave, 1)
 void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const uint16_t* __restrict__ hpacked,
                             const uint16_t* __restrict__ w, float* __restrict__ logits,
                             float2* __restrict__ partials) {
-  using C = Deep32Cfg<MB, NB>;
+  using C = Deep32Cfg<MB, NB, S, NW>;
   constexpr int ND = C::kDmaPerWave;
+  constexpr int kA = C::kAhead;
+  constexpr int kB = C::kBufBytes;
   // One LDS object per stage: the compiler then sees that a fragment read
   // and a DMA into another stage cannot alias, and leaves the ordering to the
   // explicit vmcnt waits below.
-  __shared__ __align__(1024) unsigned char lds0[C::kBufBytes], lds1[C::kBufBytes], lds2[C::kBufBytes],
-      lds3[C::kBufBytes], lds4[C::kBufBytes], lds5[C::kBufBytes];
-  __shared__ float red[4][C::kRows];
+  __shared__ __align__(1024) unsigned char lds0[kB], lds1[kB], lds2[kB], lds3[S > 3 ? kB : 16],
+      lds4[S > 4 ? kB : 16], lds5[S > 5 ? kB : 16];
+  __shared__ float red[NW][C::kRows];
   auto abuf = [&](int stage) -> unsigned char* {
     switch (stage) {
       case 0: return lds0;
@@ -399,7 +436,7 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int nblk = (V + 15) / 16;
-  const int blk0 = (tile * 4 + wave) * NB;  // first 32-entry vocabulary block of the wave
+  const int blk0 = (tile * NW + wave) * NB;  // first 32-entry vocabulary block of the wave
   // W source of this lane for 16-wide k-step ks of chunk 0; chunk c adds c*wstep.
   const uint16_t* wsrc[NB][2];
 #pragma unroll
@@ -420,7 +457,7 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
   const int64_t wstep = PACKED ? (int64_t)nblk * 64 * 8 : 32;
   const int nchunks = K / 32;
 
-  // DMA i of this wave moves fragment f = wave + 4*i (2*mb + ks) of a chunk:
+  // DMA i of this wave moves fragment f = wave + NW*i (2*mb + ks) of a chunk:
   // 1 KB contiguous in the packed hidden (lane l: row mb*32 + l%32, k
   // 16*ks + 8*(l/32) .. +8).  Fragment numbers past the chunk's 2*MB keep
   // every wave's operation count equal: all their lanes read the same 16
@@ -433,15 +470,14 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
   int hoff[ND];
 #pragma unroll
   for (int i = 0; i < ND; ++i) {
-    const int f = wave + 4 * i;
+    const int f = wave + NW * i;
     const int fs = min(f, C::kFrags - 1);
     const int mbg = min(mbt - 1, m0 / 32 + (fs >> 1));
     hsrc[i] = hpacked + (((int64_t)(fs & 1) * mbt + mbg) * 64 + (f < C::kFrags ? lane : 0)) * 8;
     hoff[i] = f * 1024;
   }
 
-  bf16x8 wreg[kStages][NB][2];
-  bf16x8 af[2][C::kFrags];
+  bf16x8 wreg[S][NB][2];
   // Memory operation j (0 <= j < kOpsPerChunk) of chunk c: the hidden DMAs
   // first, then the W loads, always in this order (the vmcnt accounting
   // relies on it).
@@ -454,8 +490,11 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
       wreg[slot][nb][ks] = load_bf16x8_stream(wsrc[nb][ks] + (int64_t)c * wstep);  // read once
     }
   };
-  auto read_frag = [&](int set, int slot, int f) {
-    af[set][f] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(abuf(slot) + f * 1024 + lane * 16));
+  // Hidden fragment number q of a chunk in MFMA order (q = ks*MB + mb) is
+  // LDS fragment 2*mb + ks.
+  auto read_frag = [&](int stage, int q) -> bf16x8 {
+    const int f = 2 * (q % MB) + q / MB;
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(abuf(stage) + f * 1024 + lane * 16));
   };
 
   f32x16 acc[MB][NB];
@@ -467,47 +506,86 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
 #pragma unroll
-  for (int c = 0; c < kAhead; ++c)
+  for (int c = 0; c < kA; ++c)
 #pragma unroll
     for (int j = 0; j < C::kOpsPerChunk; ++j) issue_op(j, c, c);
-  wait_vmcnt<2 * NB + (kAhead - 2) * C::kOpsPerChunk>();  // chunks 0 and 1 have landed
-  lds_barrier();
+  if constexpr (C::kNextChunk) {
+    bf16x8 af[2][C::kFrags];
+    wait_vmcnt<2 * NB + (kA - 2) * C::kOpsPerChunk>();  // chunks 0 and 1 have landed
+    lds_barrier();
 #pragma unroll
-  for (int f = 0; f < C::kFrags; ++f) read_frag(0, 0, f);
-  for (int c0 = 0; c0 < nchunks; c0 += kStages) {
+    for (int q = 0; q < C::kFrags; ++q) af[0][q] = read_frag(0, q);
+    for (int c0 = 0; c0 < nchunks; c0 += S) {
 #pragma unroll
-    for (int s = 0; s < kStages; ++s) {
-      const int c = c0 + s;
-      const bool live = c < nchunks;
-      // One MFMA, then one other instruction: the loads of chunk c+4 and the
-      // fragment reads of chunk c+1 fill the issue slots between MFMAs, so a
-      // single wave keeps the matrix pipe busy while they go out.
+      for (int s = 0; s < S; ++s) {
+        const int c = c0 + s;
+        const bool live = c < nchunks;
+        // One MFMA, then one other instruction: the loads of chunk c+S-1 and
+        // the fragment reads of chunk c+1 fill the issue slots between MFMAs,
+        // so a single wave keeps the matrix pipe busy while they go out.
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        bf16x8 wv[NB];
+        for (int ks = 0; ks < 2; ++ks) {
+          bf16x8 wv[NB];
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) wv[nb] = live ? wreg[s][nb][ks] : bf16x8{};
+          for (int nb = 0; nb < NB; ++nb) wv[nb] = live ? wreg[s][nb][ks] : bf16x8{};
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+          for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            const int i = (ks * MB + mb) * NB + nb;
-            acc[mb][nb] = mfma32x32x16(wv[nb], af[s & 1][2 * mb + ks], acc[mb][nb]);
-            if (i < C::kOpsPerChunk)
-              issue_op(i, (s + kAhead) % kStages, c + kAhead);
-            else if (i - C::kOpsPerChunk < C::kFrags)
-              read_frag((s + 1) & 1, (s + 1) % kStages, i - C::kOpsPerChunk);
-            __builtin_amdgcn_sched_barrier(0);
-          }
+            for (int nb = 0; nb < NB; ++nb) {
+              const int q = ks * MB + mb;
+              const int i = q * NB + nb;
+              acc[mb][nb] = mfma32x32x16(wv[nb], af[s & 1][q], acc[mb][nb]);
+              if (i < C::kOpsPerChunk)
+                issue_op(i, (s + kA) % S, c + kA);
+              else if (i - C::kOpsPerChunk < C::kFrags)
+                af[(s + 1) & 1][i - C::kOpsPerChunk] = read_frag((s + 1) % S, i - C::kOpsPerChunk);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+#pragma unroll
+        for (int q = C::kMfmas - C::kOpsPerChunk; q < C::kFrags; ++q)
+          if (q >= 0) af[(s + 1) & 1][q] = read_frag((s + 1) % S, q);
+        wait_vmcnt<C::kInFlight>();
+        lds_barrier();
       }
+    }
+  } else {
+    wait_vmcnt<(kA - 1) * C::kOpsPerChunk>();  // chunk 0 has landed
+    lds_barrier();
+    for (int c0 = 0; c0 < nchunks; c0 += S) {
 #pragma unroll
-      for (int f = 2 * MB * NB - C::kOpsPerChunk; f < C::kFrags; ++f)
-        if (f >= 0) read_frag((s + 1) & 1, (s + 1) % kStages, f);
-      wait_vmcnt<C::kInFlight>();
-      lds_barrier();
+      for (int s = 0; s < S; ++s) {
+        const int c = c0 + s;
+        const bool live = c < nchunks;
+        bf16x8 hf[C::kFrags];
+#pragma unroll
+        for (int q = 0; q < C::kReadAhead && q < C::kFrags; ++q) hf[q] = read_frag(s, q);
+        // One MFMA, then at most one other instruction: the loads of chunk
+        // c+S-1 and the fragment reads fill the issue slots between MFMAs.
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          bf16x8 wv[NB];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) wv[nb] = live ? wreg[s][nb][ks] : bf16x8{};
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const int q = ks * MB + mb;
+            if (q + C::kReadAhead < C::kFrags) hf[q + C::kReadAhead] = read_frag(s, q + C::kReadAhead);
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+              const int i = q * NB + nb;
+              acc[mb][nb] = mfma32x32x16(wv[nb], hf[q], acc[mb][nb]);
+              if (i < C::kOpsPerChunk) issue_op(i, (s + kA) % S, c + kA);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+        }
+        wait_vmcnt<C::kInFlight>();
+        lds_barrier();
+      }
     }
   }
-  tile_epilogue32<MB, NB>(acc, M, V, ntiles, tile, m0, blk0, logits, partials, red);
+  tile_epilogue32<MB, NB, NW>(acc, M, V, ntiles, tile, m0, blk0, logits, partials, red);
 }
 
 // Hidden rows [M][K] -> fragments [K/16][ceil(M/32)][64 lanes][8]: lane l of
@@ -626,30 +704,53 @@ hipError_t launch_shallow_mb(const VocabPlan& p, const void* hidden, const void*
   return launch_shallow<MB, 32>(p, hidden, w, logits, partials, stream, e0, e1);
 }
 
-template <int MB, int NB>
+template <int MB, int NB, int NW, int S = (NW == 8 ? 3 : 6)>
 hipError_t launch_deep(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
                        uint16_t* hpacked, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
   const int64_t pieces = (int64_t)(p.K / 16) * ((p.M + 31) / 32) * 64;
   const int pblocks = (int)std::min<int64_t>((pieces + kVThreads - 1) / kVThreads, 4096);
   hipExtLaunchKernelGGL(pack_hidden_kernel, dim3(pblocks), dim3(kVThreads), 0, stream, e0, nullptr, 0, p.M, p.K,
                         static_cast<const uint16_t*>(hidden), hpacked);
-  const dim3 grid((p.ntiles + 7) / 8 * 8 * p.mtiles), block(kVThreads);
+  const dim3 grid((p.ntiles + 7) / 8 * 8 * p.mtiles), block(NW * kWave);
   const uint16_t* wv = static_cast<const uint16_t*>(w);
   if (p.packed)
-    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, true>), grid, block, 0, stream, nullptr, e1, 0, p.M, p.K,
+    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, S, NW, true>), grid, block, 0, stream, nullptr, e1, 0, p.M, p.K,
                           p.V, p.ntiles, p.mtiles, hpacked, wv, logits, partials);
   else
-    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, false>), grid, block, 0, stream, nullptr, e1, 0, p.M, p.K,
+    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, S, NW, false>), grid, block, 0, stream, nullptr, e1, 0, p.M, p.K,
                           p.V, p.ntiles, p.mtiles, hpacked, wv, logits, partials);
   return hipGetLastError();
 }
 
-// Deep schedule: 32-entry vocabulary blocks per wave (NB) and the most 32-row
-// blocks per M-tile, keeping the accumulators (MB x NB x 16 registers) within
-// 256 registers next to the load rings.
-constexpr int kDeepMaxBlocks1 = 12;
-constexpr int kDeepMaxBlocks2 = 7;
+// Deep schedules: NB blocks of 32 vocabulary entries per wave, NW waves per
+// workgroup (one or two per SIMD), and the most 32-row blocks per M-tile
+// that keep a wave's accumulators (MB x NB x 16) in its share of the
+// accumulation registers (256 with one wave per SIMD, 160 of the 256
+// registers of each of two) next to the W ring (S x NB x 8 registers).
+struct DeepShape {
+  int nb, nw, cap;
+};
+constexpr DeepShape kDeepShapes[3] = {{1, 4, 12}, {2, 4, 7}, {2, 8, 5}};
 constexpr int kShallowMaxBlocks = 4;  // 16-row blocks of the shallow schedule
+
+// Per-CU cost of a deep plan in the inflow model of the deep kernel: the
+// workgroups a CU runs one after another (CUs of the MI355X: 256), each
+// pulling its M-tile of hidden rows (L2 hits) and its W slice, per unit of K.
+// The M-tiles of one vocabulary tile run on one XCD at the same time, so the
+// first reader of a W line misses to HBM (weight 2.1 against an L2 hit) and
+// the others find it in L2.
+constexpr int kModelCUs = 256;
+constexpr double kMissWeight = 2.1;
+
+double deep_cost(int blocks32, int V, const DeepShape& d, int* mtiles, int* mblocks) {
+  *mtiles = (blocks32 + d.cap - 1) / d.cap;
+  *mblocks = (blocks32 + *mtiles - 1) / *mtiles;
+  const int tile_n = 32 * d.nb * d.nw;
+  const long long wgs = (long long)((V + tile_n - 1) / tile_n) * *mtiles;
+  const long long rounds = (wgs + kModelCUs - 1) / kModelCUs;
+  const double w_weight = (kMissWeight + (*mtiles - 1)) / *mtiles;
+  return (double)rounds * (w_weight * tile_n + 32.0 * *mblocks);
+}
 
 }  // namespace
 
@@ -676,24 +777,33 @@ VocabPlan vocab_plan(int dtype, int M, int K, int V, bool packed) {
     p.deep = false;
     p.mblocks = 4;
     p.nbw = 1;
+    p.waves = 4;
     p.mtiles = (M + 63) / 64;
   } else if (blocks <= kShallowMaxBlocks) {
     p.deep = false;
     p.mblocks = blocks;
     p.nbw = kShallowWaves / 4;  // a 16-entry block per wave
+    p.waves = 4;
     p.mtiles = 1;
   } else {
-    // Two 32-entry blocks per wave (half the LDS reads per MFMA) when the
-    // vocabulary gives at least one 256-wide tile per CU, or when the rows
-    // need M-tiles anyway; one block per wave for small vocabularies.
+    // The deep shape the inflow model prices lowest (ties go to the
+    // narrower tile).
     const int blocks32 = (M + 31) / 32;
     p.deep = true;
-    p.nbw = (V >= 256 * 256 || blocks32 > kDeepMaxBlocks2) ? 4 : 2;  // in 16-entry blocks
-    const int cap = p.nbw == 4 ? kDeepMaxBlocks2 : kDeepMaxBlocks1;
-    p.mtiles = (blocks32 + cap - 1) / cap;
-    p.mblocks = (blocks32 + p.mtiles - 1) / p.mtiles;  // 32-row blocks
+    double best = 0.0;
+    for (int i = 0; i < 3; ++i) {
+      int mt, mb;
+      const double cost = deep_cost(blocks32, V, kDeepShapes[i], &mt, &mb);
+      if (i == 0 || cost < best) {
+        best = cost;
+        p.nbw = 2 * kDeepShapes[i].nb;
+        p.waves = kDeepShapes[i].nw;
+        p.mtiles = mt;
+        p.mblocks = mb;
+      }
+    }
   }
-  p.tile_n = 64 * p.nbw;
+  p.tile_n = 16 * p.waves * p.nbw;
   p.ntiles = (V + p.tile_n - 1) / p.tile_n;
   return p;
 }
@@ -727,17 +837,23 @@ hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const
       default: return hipErrorInvalidValue;
     }
   }
-#define SDV_D(B, N) \
-  case B: return launch_deep<B, N>(p, hidden, w, logits, partials, hpacked, stream, e0, e1);
+#define SDV_D(B, N, W) \
+  case B: return launch_deep<B, N, W>(p, hidden, w, logits, partials, hpacked, stream, e0, e1);
+  if (p.waves == 8) {
+    switch (p.mblocks) {
+      SDV_D(2, 2, 8) SDV_D(3, 2, 8) SDV_D(4, 2, 8) SDV_D(5, 2, 8)
+      default: return hipErrorInvalidValue;
+    }
+  }
   if (p.nbw == 4) {
     switch (p.mblocks) {
-      SDV_D(2, 2) SDV_D(3, 2) SDV_D(4, 2) SDV_D(5, 2) SDV_D(6, 2) SDV_D(7, 2)
+      SDV_D(2, 2, 4) SDV_D(3, 2, 4) SDV_D(4, 2, 4) SDV_D(5, 2, 4) SDV_D(6, 2, 4) SDV_D(7, 2, 4)
       default: return hipErrorInvalidValue;
     }
   }
   switch (p.mblocks) {
-    SDV_D(2, 1) SDV_D(3, 1) SDV_D(4, 1) SDV_D(5, 1) SDV_D(6, 1) SDV_D(7, 1) SDV_D(8, 1) SDV_D(9, 1)
-    SDV_D(10, 1) SDV_D(11, 1) SDV_D(12, 1)
+    SDV_D(2, 1, 4) SDV_D(3, 1, 4) SDV_D(4, 1, 4) SDV_D(5, 1, 4) SDV_D(6, 1, 4) SDV_D(7, 1, 4) SDV_D(8, 1, 4)
+    SDV_D(9, 1, 4) SDV_D(10, 1, 4) SDV_D(11, 1, 4) SDV_D(12, 1, 4)
     default: return hipErrorInvalidValue;
   }
 #undef SDV_D

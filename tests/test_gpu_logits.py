@@ -1,8 +1,9 @@
 """GPU parity: sd_verify_logits (vocabulary projection + row log-sum-exp)
-against the float64 oracle.  Shapes cover both bf16 schedules (at most 64
-rows; more rows with two or four vocabulary blocks per wave), ragged
-vocabulary tiles (V not a multiple of the tile, and not of 4), K not a multiple
-of the chunk, several M-tiles, and the tiny fp32 case."""
+against the float64 oracle.  Shapes cover the shallow bf16 schedule (at most
+64 rows) and each deep shape (one or two 32-entry vocabulary blocks per wave,
+four or eight waves per workgroup), ragged vocabulary tiles (V not a multiple
+of the tile, and not of 4), K not a multiple of the chunk, several M-tiles,
+and the tiny fp32 case."""
 
 import numpy as np
 import pytest
@@ -28,12 +29,23 @@ CASES = {
                                 lengths=("fixed", 8)),
     "m336_k256_v130": _v.replace(batch=56, gamma=5, n_q_heads=2, n_kv_heads=2, hidden=256, vocab=130,
                                  lengths=("fixed", 8)),
-    # Four vocabulary blocks per wave (V >= 65536), ragged last tile.
+    # Deep schedule, one 32-entry block per wave, ragged last tile.
     "m80_k128_v65600": _v.replace(batch=16, gamma=4, n_q_heads=2, n_kv_heads=2, hidden=128, vocab=65600,
                                   lengths=("fixed", 8)),
-    # Two M-tiles of the four-block schedule, K not a multiple of 128, V odd.
+    # Same schedule, K not a multiple of 128, V odd.
     "m272_k96_v65537": _v.replace(batch=34, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=96, vocab=65537,
                                   lengths=("fixed", 8)),
+    # Two blocks per wave, four waves (256-wide tiles): one M-tile of 7 row
+    # blocks, then two M-tiles; K of 3 and 5 chunks (the 6-stage ring runs
+    # past the last chunk), V odd.
+    "m224_k96_v100001": _v.replace(batch=32, gamma=6, n_q_heads=2, n_kv_heads=2, hidden=96, vocab=100001,
+                                   lengths=("fixed", 8)),
+    "m416_k160_v100001": _v.replace(batch=52, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=160, vocab=100001,
+                                    lengths=("fixed", 8)),
+    # Two blocks per wave, eight waves (512-wide tiles, 3-stage ring), rows
+    # not a multiple of 32, V odd.
+    "m100_k160_v100003": _v.replace(batch=20, gamma=4, n_q_heads=2, n_kv_heads=2, hidden=160, vocab=100003,
+                                    lengths=("fixed", 8)),
     "f32_m70_k128_v65": get_config("tiny").replace(batch=14, gamma=4, hidden=128, vocab=65, lengths=("fixed", 8)),
 }
 
@@ -56,7 +68,7 @@ def test_logits_match_oracle(name):
 
 
 @pytest.mark.parametrize("name", ["m18_k512_v1000", "m18_k512_v1003", "m100_k256_v777", "m336_k256_v130",
-                                  "m272_k96_v65537"])
+                                  "m272_k96_v65537", "m416_k160_v100001", "m100_k160_v100003"])
 def test_packed_vocab_matches_row_major_bitwise(name):
     """The packed layout changes where W is read from, not the arithmetic:
     logits and log-sum-exp must be bit-identical to the row-major path."""
