@@ -76,8 +76,8 @@ def source_digest(name: str) -> str:
     return h.hexdigest()
 
 
-def counter_traffic(kernel: str, workload: str, source: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+def counter_entry(kernel: str, workload: str, source: str):
+    """The committed rocprofv3 counter record of a kernel on a workload, or
     None when there is none or the kernel source changed since it was taken."""
     try:
         with open(TRAFFIC_FILE) as f:
@@ -86,10 +86,21 @@ def counter_traffic(kernel: str, workload: str, source: str):
         return None
     for e in entries:
         if e.get("kernel") == kernel and e.get("workload") == workload:
-            if e.get("source_sha256") != source_digest(source):
-                return None
-            return float(e["bytes_per_launch"])
+            return e if e.get("source_sha256") == source_digest(source) else None
     return None
+
+
+def counter_traffic(kernel: str, workload: str, source: str):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated), or None."""
+    e = counter_entry(kernel, workload, source)
+    return float(e["bytes_per_launch"]) if e is not None else None
+
+
+def counter_mfma_busy(kernel: str, workload: str, source: str):
+    """MFMA busy share of the kernel's SIMD cycles from its SQ counter run
+    (SQ_VALU_MFMA_BUSY_CYCLES over 1024 SIMDs x GRBM_GUI_ACTIVE / 8), or None."""
+    e = counter_entry(kernel, workload, source)
+    return float(e["sq_mfma_busy"]) if e is not None and "sq_mfma_busy" in e else None
 
 
 def cpu_model() -> str:
@@ -530,7 +541,8 @@ def main() -> int:
     roof_vocab = {"bound": "hbm", "achieved": vocab_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                   "frac": vocab_gbps / HBM_PEAK_GBPS, "traffic": counter_traffic(vocab_kernel, cfg.name, "vocab.hip"),
                   "kernel": vocab_kernel, "bytes_per_launch": vocab_bytes, "ms_per_launch": float(st_mean[1]),
-                  "mfma_frac": vocab_tflops / BF16_MFMA_PEAK_TFLOPS}
+                  "mfma_frac": vocab_tflops / BF16_MFMA_PEAK_TFLOPS,
+                  "mfma_busy_counters": counter_mfma_busy(vocab_kernel, cfg.name, "vocab.hip")}
     dominant = "vocab" if st_mean[1] >= st_mean[0] else "attention"
     roof = roof_vocab if dominant == "vocab" else roof_attn
 
