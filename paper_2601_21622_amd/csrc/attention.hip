@@ -8,24 +8,32 @@
 //
 // Work split: one wave per work item (request chunk of `chunk_keys` keys, KV
 // head); a workgroup holds four independent items, so no wave waits on
-// another.  The host picks the chunk length from the total work so that the
-// items fill the GPU about twice over.  Two bf16 kernels:
+// another.  The host picks the chunk length from the total work and the
+// number of workgroups a launch round holds (attn_chunk_keys).  Two bf16
+// kernels:
 //   * one 16-row block (multi-head attention: the G queries of one head):
-//     each wave loads the next 32-key tile's K fragments and V rows into its
-//     other register set while it folds in the current tile; V goes through a
-//     wave-private LDS tile so that the transposing read ds_read_b64_tr_b16
-//     hands each lane its V^T fragment;
+//     each wave loads the next 32-key tile's K rows (before it folds in the
+//     current tile) and V rows (in the middle of the fold) into its other
+//     register set; K and V then pass through wave-private LDS tiles, so that
+//     the transposing read ds_read_b64_tr_b16 hands each lane its V^T
+//     fragment;
 //   * several 16-row blocks (grouped-query attention): K and V tiles go from
 //     HBM into wave-private LDS stages by DMA (no registers, completion
-//     tracked with explicit vmcnt waits), again one tile ahead.
+//     tracked with explicit vmcnt waits), one tile ahead, the next tile's
+//     DMAs spread over the current tile's fold.
 // Both compute S^T = K Q^T and O^T += V^T P^T on MFMA 16x16x32 bf16 (the Q
 // fragments stay in registers, P comes straight from the S^T accumulator
 // layout) with the online softmax in the log2 domain, each lane owning one
-// query row (for up to two row blocks the reference maximum moves lazily, so
-// most tiles skip the rescale of O).  Each item writes one partial (max, sum, O) to the workspace; a
-// combine kernel merges the chunks of each request in fixed order and writes
-// O in the input dtype.  LDS tiles keep rows whole but rotate their 16-byte
-// pieces so that the fragment reads are free of bank conflicts.
+// query row.  The one-block kernel moves a row's reference maximum lazily
+// (O is rescaled only when the maximum grows by more than 2^8); the
+// several-block kernel never rescales O: its first tile sets the maxima, and
+// a later growth beyond 2^64 restarts the item with the grown maxima.  Each
+// item writes one partial (max, sum, O) to the workspace; a combine kernel
+// (or, in a whole step, the acceptance's last launch) merges the chunks of
+// each request in fixed order and writes O in the input dtype.  LDS tiles keep
+// rows whole but rotate their 16-byte pieces so that the fragment reads
+// mostly avoid bank conflicts (rocprofv3 counts 0.8 conflict cycles per LDS
+// instruction in the one-block kernel, 1.3 in the other).
 #include <hip/hip_ext.h>
 
 #include <atomic>

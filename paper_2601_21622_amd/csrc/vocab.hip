@@ -17,11 +17,13 @@
 //     several workgroups per CU keep enough W in flight.
 //   * deep (more rows), MFMA 32x32x16: the hidden rows are first repacked
 //     (pack_hidden_kernel) into 32-row fragments that LDS DMA moves 1 KB at a
-//     time; the accumulators of up to 384 rows pin one workgroup to a CU; W
-//     goes through a 6-slot register ring and hidden through 6 LDS stages,
-//     five 32-wide K-chunks ahead of the one multiplied, and each wave owns
-//     1 or 2 blocks of 32 vocabulary entries.  Workgroups that share a
-//     vocabulary tile (several M-tiles) are dealt to the same XCD.
+//     time; a workgroup's accumulators pin it to a CU.  Three shapes: four
+//     waves (one per SIMD) with 1 or 2 blocks of 32 vocabulary entries each,
+//     W in a 6-slot register ring and hidden in 6 LDS stages; or eight waves
+//     (two per SIMD) with 2 blocks each, a 512-wide tile on a 3-stage ring.
+//     vocab_plan picks the shape whose per-CU inflow (W misses plus hidden
+//     hits) is smallest.  Workgroups that share a vocabulary tile (several
+//     M-tiles) are dealt to the same XCD.
 // W fragments are loaded with the nontemporal hint in both schedules: W is
 // read once per launch and should not evict the hidden rows or the logits.
 // The epilogue writes the float32 logits and, per (row, tile), the tile
