@@ -66,7 +66,8 @@ AttnShape attn_shape(const sd_dims_t* d, float scale, const int32_t* kv_len = nu
   s.D = d->head_dim;
   s.group = d->n_q_heads / d->n_kv_heads;
   s.rows = s.G * s.group;
-  s.chunk_keys = attn_chunk_keys(d->dtype, s.rows, s.Hkv, kv_len, d->batch);
+  s.row_groups = attn_row_groups(d->dtype, s.rows, s.D);
+  s.chunk_keys = attn_chunk_keys(d->dtype, s.rows, s.row_groups, s.Hkv, kv_len, d->batch);
   if (page_size > 0) s.chunk_keys = (s.chunk_keys + page_size - 1) / page_size * page_size;
   s.scale_log2 = scale * 1.4426950408889634f;
   return s;

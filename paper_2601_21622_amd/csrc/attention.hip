@@ -68,6 +68,12 @@ constexpr int64_t kRoundWorkgroups = 256;
 // Start-up cost of one work item (query rows, pipeline fill, partial write),
 // in keys of streaming, for the round estimate of the multi-block kernel.
 constexpr int64_t kItemStartKeys = 256;
+// Most 16-row blocks one wave holds at head dimension 128: O takes 32
+// accumulator registers per block and the Q fragments 16, and at six blocks
+// the several-block kernel spills to scratch.  Wider row sets split over
+// row groups (each wave re-reads the item's K and V tiles, mostly from cache,
+// since the waves of one KV head share a workgroup).
+constexpr int kMaxRowBlocks = 5;
 
 // Compute units of the current device (cached per device; 256 on MI355X).
 int64_t device_cu_count() {
@@ -509,12 +515,16 @@ __device__ __forceinline__ void read_k_frags(const unsigned char* __restrict__ k
           bf16x8, *reinterpret_cast<const u32x4*>(ksrc + tl.kread[ds & 1] + T::k_read_imm(kb, ds)));
 }
 
-// Item of wave `wave` in workgroup blockIdx.x: (chunk, KV head), KV head
-// fastest.  Returns false past the last item.
-__device__ __forceinline__ bool attn_item(const AttnShape& s, const AttnBatch& bt, int& c_local, int& g) {
+// Item of wave `wave` in workgroup blockIdx.x: (chunk, KV head, row group),
+// row group fastest, then KV head, so the waves that split one head's rows
+// share a workgroup (and read the same K and V tiles at the same time).
+// Returns false past the last item.
+__device__ __forceinline__ bool attn_item(const AttnShape& s, const AttnBatch& bt, int& c_local, int& g, int& rg) {
   const int item = blockIdx.x * kAttnWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  c_local = item / s.Hkv;
-  g = item - c_local * s.Hkv;
+  const int pair = item / s.row_groups;
+  rg = item - pair * s.row_groups;
+  c_local = pair / s.Hkv;
+  g = pair - c_local * s.Hkv;
   return c_local < bt.chunk_prefix[bt.nreq];
 }
 
@@ -591,8 +601,8 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   __shared__ __align__(1024) unsigned char kst[2 * kStage];
   __shared__ __align__(1024) unsigned char vst[2 * kStage];
 
-  int c_local, g;
-  if (!attn_item(s, bt, c_local, g)) return;
+  int c_local, g, rg;
+  if (!attn_item(s, bt, c_local, g, rg)) return;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
 
@@ -607,7 +617,8 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
   const KVSrc<D, PAGED> src = kv_src<D, PAGED>(s, bt, kp, vp, b, g, L, k_begin);
 
   AttnRows<RB, D> st;
-  init_rows<RB, D>(st, s, bt.anc, q, req, g, L, 0);
+  const int row0 = __builtin_amdgcn_readfirstlane(rg * RB * 16);
+  init_rows<RB, D>(st, s, bt.anc, q, req, g, L, row0);
 
   // Tile i of the item starts at key k_begin + 32i and is staged in stage
   // i & 1; tile i + 1 loads while tile i is folded in, its DMAs spread over
@@ -689,7 +700,7 @@ void attn_bf16_kernel(const AttnShape s, const AttnBatch bt, const uint16_t* __r
     if (!restart) break;
     wait_vmcnt<0>();  // the tile after the one that restarted may still be in flight
   }
-  write_partial<RB, D>(s, bt, parts, c_local, g, st.m, st.lsum, st.o);
+  write_partial<RB, D>(s, bt, parts, c_local, g, st.m, st.lsum, st.o, row0);
 }
 
 // Register-staged variant: K and V blocks go HBM -> registers -> the wave's
@@ -709,8 +720,9 @@ void attn_bf16_reg_kernel(const AttnShape s, const AttnBatch bt, const uint16_t*
   __shared__ __align__(1024) unsigned char ksm[kAttnWaves * T::kBytes];
   __shared__ __align__(1024) unsigned char vsm[kAttnWaves * T::kBytes];
 
-  int c_local, g;
-  if (!attn_item(s, bt, c_local, g)) return;
+  int c_local, g, rg;
+  if (!attn_item(s, bt, c_local, g, rg)) return;
+  (void)rg;  // a single 16-row block: one row group
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
 
@@ -867,7 +879,7 @@ void attn_combine_kernel(const AttnShape s, const AttnBatch bt, AttnPartials par
 template <int RB, int D, bool TREE, bool PAGED>
 hipError_t launch_bf16(const AttnShape& s, const AttnBatch& bt, int nchunks, const void* q, const void* k,
                        const void* v, AttnPartials parts, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  const int items = nchunks * s.Hkv;
+  const int items = nchunks * s.Hkv * s.row_groups;
   hipExtLaunchKernelGGL((attn_bf16_kernel<RB, D, TREE, PAGED>), dim3((items + kAttnWaves - 1) / kAttnWaves), dim3(kAttnThreads), 0,
                         stream, e0, e1, 0, s, bt, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                         static_cast<const uint16_t*>(v), parts);
@@ -892,11 +904,19 @@ hipError_t dispatch_rb(int rb, const AttnShape& s, const AttnBatch& bt, int nchu
     case 3: return launch_bf16<3, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     case 4: return launch_bf16<4, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
     case 5: return launch_bf16<5, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 6: return launch_bf16<6, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 7: return launch_bf16<7, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    case 8: return launch_bf16<8, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
-    default: return hipErrorInvalidValue;
+    default: break;
   }
+  // Six to eight blocks per wave only at head dimension 64 (at 128 the rows
+  // split over row groups first).
+  if constexpr (D == 64) {
+    switch (rb) {
+      case 6: return launch_bf16<6, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+      case 7: return launch_bf16<7, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+      case 8: return launch_bf16<8, D, TREE, PAGED>(s, bt, nchunks, q, k, v, parts, stream, e0, e1);
+      default: break;
+    }
+  }
+  return hipErrorInvalidValue;
 }
 
 // Tree commit: move the K and V rows of request b's accepted nodes (tail
@@ -954,7 +974,13 @@ void tree_masks_kernel(int N, const int32_t* __restrict__ parent, uint64_t* __re
 
 }  // namespace
 
-int attn_chunk_keys(int dtype, int rows, int Hkv, const int32_t* kv_len, int B) {
+int attn_row_groups(int dtype, int rows, int D) {
+  const int rb = (rows + 15) / 16;
+  if (dtype == 0 || D != 128 || rb <= kMaxRowBlocks) return 1;
+  return (rb + kMaxRowBlocks - 1) / kMaxRowBlocks;
+}
+
+int attn_chunk_keys(int dtype, int rows, int row_groups, int Hkv, const int32_t* kv_len, int B) {
   if (dtype == 0) return kF32ChunkKeys;
   int64_t total_keys = 0;
   if (kv_len != nullptr)
@@ -985,7 +1011,7 @@ int attn_chunk_keys(int dtype, int rows, int Hkv, const int32_t* kv_len, int B) 
     for (int c2 = def; c2 <= kMaxChunkKeys; c2 += kTile) {
       int64_t chunks = 0;
       for (int b = 0; b < B; ++b) chunks += (kv_len[b] + c2 - 1) / c2;
-      const int64_t wgs = (chunks * Hkv + kAttnWaves - 1) / kAttnWaves;
+      const int64_t wgs = (chunks * Hkv * row_groups + kAttnWaves - 1) / kAttnWaves;
       const int64_t t = (wgs + cus - 1) / cus * (c2 + kItemStartKeys);
       if (t < best_t) {
         best_t = t;
@@ -1035,7 +1061,8 @@ hipError_t launch_attention(int dtype, const AttnShape& s, const AttnBatch& bt, 
                           static_cast<const float*>(v), parts);
     return hipGetLastError();
   }
-  const int rb = (s.rows + 15) / 16;
+  // 16-row blocks per wave: a KV head's blocks split over its row groups.
+  const int rb = ((s.rows + 15) / 16 + s.row_groups - 1) / s.row_groups;
   // Mask kinds: chain or tree; cache layouts: segments or pages (chain only).
   const bool tree = bt.anc != nullptr;
   const bool paged = bt.pages != nullptr;

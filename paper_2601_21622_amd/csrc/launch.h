@@ -43,6 +43,7 @@ struct AttnShape {
   int Hq, Hkv, D;
   int group;        // Hq / Hkv
   int rows;         // G * group query rows per KV head
+  int row_groups;   // waves that share a (chunk, KV head), each taking 16*RB consecutive rows
   int chunk_keys;   // keys per partial (one work item)
   float scale_log2; // softmax scale * log2(e)
 };
@@ -57,7 +58,10 @@ struct AttnPartials {
 
 // Keys per work item (chunk), from the total number of keys over the batch;
 // attn_max_chunks bounds the chunk count for any lengths up to max_kv_len.
-int attn_chunk_keys(int dtype, int rows, int Hkv, const int32_t* kv_len, int B);
+int attn_chunk_keys(int dtype, int rows, int row_groups, int Hkv, const int32_t* kv_len, int B);
+// Row groups of one (chunk, KV head): a wave holds at most kMaxRowBlocks
+// 16-row blocks of O at head dimension 128 (more would spill registers).
+int attn_row_groups(int dtype, int rows, int D);
 int64_t attn_max_chunks(int dtype, int Hkv, int B, int64_t max_kv_len);
 size_t attn_partial_bytes(int64_t total_chunks, int Hkv, int rows, int D);
 AttnPartials attn_carve(void* ws, int64_t total_chunks, int Hkv, int rows, int D);

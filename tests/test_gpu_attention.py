@@ -29,7 +29,9 @@ CASES = {
                                            vocab=256, lengths=("explicit", (5, 70, 300))),
     "many_requests_bf16": get_config("pooled").replace(batch=70, n_q_heads=2, n_kv_heads=2, hidden=256,
                                                        vocab=128, lengths=("uniform", 5, 700)),
-    # Query rows per KV head = G * group: 40 (3 blocks of 16), 56 (4, head_dim 64), 88 (6), 112 (7), 128 (8).
+    # Query rows per KV head = G * group: 40 (3 blocks of 16), 56 (4, head_dim 64), 88 (6 blocks: two row
+    # groups of 3 at head_dim 128), 112 (7: groups of 4 and 3), 128 (8: 4 and 4), 120 at head_dim 64 (8
+    # blocks in one wave).
     "rows40_bf16": get_config("llama70b_share").replace(batch=2, gamma=4, n_q_heads=16, n_kv_heads=2, hidden=2048,
                                                         vocab=256, lengths=("explicit", (5, 777))),
     "rows56_d64_bf16": get_config("llama70b_share").replace(batch=2, gamma=6, n_q_heads=16, n_kv_heads=2,
@@ -41,6 +43,9 @@ CASES = {
                                                          hidden=4096, vocab=256, lengths=("explicit", (700, 33))),
     "rows128_bf16": get_config("llama70b_share").replace(batch=2, gamma=7, n_q_heads=32, n_kv_heads=2,
                                                          hidden=4096, vocab=256, lengths=("explicit", (8, 2200))),
+    "rows120_d64_bf16": get_config("llama70b_share").replace(batch=2, gamma=14, n_q_heads=16, n_kv_heads=2,
+                                                             head_dim=64, hidden=1024, vocab=256,
+                                                             lengths=("explicit", (1500, 15))),
 }
 
 

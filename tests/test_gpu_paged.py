@@ -76,6 +76,10 @@ CASES = {
                                                        lengths=("uniform", 5, 700)), 64),
     "gqa_p4096": (get_config("llama3_8b").replace(batch=2, n_q_heads=8, n_kv_heads=2, hidden=1024, vocab=256,
                                                   lengths=("explicit", (5000, 20))), 4096),
+    # 88 rows per KV head: two row groups of 3 blocks.
+    "gqa8_rows88_p64": (get_config("llama70b_share").replace(batch=2, gamma=10, n_q_heads=16, n_kv_heads=2,
+                                                             hidden=2048, vocab=256, lengths=("explicit", (11, 1030))),
+                        64),
 }
 
 

@@ -47,6 +47,9 @@ TREE_CASES = {
                                                      vocab=256, lengths=("explicit", (700, 9))), "random"),
     "mha_n63": (get_config("vicuna7b").replace(batch=2, gamma=63, n_q_heads=2, n_kv_heads=2, hidden=256,
                                                vocab=256, lengths=("explicit", (64, 900))), "random"),
+    # 32 positions x group 4 = 128 rows per KV head: two row groups of 4 blocks.
+    "gqa4_n31": (get_config("llama3_8b").replace(batch=2, gamma=31, n_q_heads=8, n_kv_heads=2, hidden=1024,
+                                                 vocab=256, lengths=("explicit", (40, 3000))), "random"),
 }
 
 
