@@ -465,7 +465,10 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
   // every wave's operation count equal: all their lanes read the same 16
   // bytes of the last fragment (one cache line, one request) into spare LDS
   // space.  Blocks past the packed rows (last M-tile) re-read the last
-  // block, whose rows are never stored.
+  // block, whose rows are never stored.  In the last block, lanes of rows
+  // past M (zero padding) read the last row's 16 bytes instead: those lines
+  // are already requested by the same instruction, so the padding costs no
+  // inflow, and the rows it feeds are never stored either.
   const int mbt = (M + 31) / 32;
   const int64_t hstep = (int64_t)2 * mbt * 512;  // elements per 32-wide chunk
   const uint16_t* hsrc[ND];
@@ -475,7 +478,9 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
     const int f = wave + NW * i;
     const int fs = min(f, C::kFrags - 1);
     const int mbg = min(mbt - 1, m0 / 32 + (fs >> 1));
-    hsrc[i] = hpacked + (((int64_t)(fs & 1) * mbt + mbg) * 64 + (f < C::kFrags ? lane : 0)) * 8;
+    const int rlast = M - 1 - mbg * 32;  // last real row of the block (>= 0)
+    const int hl = (lane & 32) + min(lane & 31, rlast);
+    hsrc[i] = hpacked + (((int64_t)(fs & 1) * mbt + mbg) * 64 + (f < C::kFrags ? hl : 0)) * 8;
     hoff[i] = f * 1024;
   }
 
