@@ -146,6 +146,18 @@ struct VocabCfg {
   static constexpr int kPiecesPerThread = (kPieces + kThreads - 1) / kThreads;
 };
 
+// LDS slot (16 bytes) of lane s of hidden fragment ks in the shallow
+// schedule's chunk buffer: the lane holds row s % 16 and k piece g = s / 16;
+// the low four bits of the slot are XORed with 2g + (ks & 1) + 8 ((ks >> 1) &
+// 1).  Consecutive threads store consecutive 16-byte pieces of one row (g
+// fastest, then ks); without the XOR every store of a row lands on the same
+// bank group.  With it, any 8 consecutive stores, and any 8 consecutive
+// lanes' reads, cover 8 distinct 16-byte slots of a 128-byte span.
+__device__ __forceinline__ int shallow_slot(int s, int ks) {
+  const int t = 8 * ((ks >> 1) & 1) + 2 * ((s >> 4) & 3) + (ks & 1);
+  return (s & 48) | ((s & 15) ^ t);
+}
+
 template <int MB, int KC, int NW, bool PACKED>
 __global__ __launch_bounds__(NW * kWave)
 void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restrict__ hidden,
@@ -198,7 +210,7 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
         const int row = p / (KC / 8);
         const int kp = p - row * (KC / 8);
         const int mb = row >> 4, r = row & 15, ks = kp >> 2, g = kp & 3;
-        const int slot = (mb * C::kSteps + ks) * 64 + r + 16 * g;
+        const int slot = (mb * C::kSteps + ks) * 64 + shallow_slot(r + 16 * g, ks);
         *reinterpret_cast<u32x4*>(abuf[buf] + slot * 16) = areg[i];
       }
     }
@@ -234,7 +246,7 @@ void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restri
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const bf16x8 a = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(abuf[buf] + ((mb * C::kSteps + ks) * 64 + lane) * 16));
+            bf16x8, *reinterpret_cast<const u32x4*>(abuf[buf] + ((mb * C::kSteps + ks) * 64 + shallow_slot(lane, ks)) * 16));
         acc[mb][0] = mfma16x16x32(wcur[ks], a, acc[mb][0]);
       }
     }
