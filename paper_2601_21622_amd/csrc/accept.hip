@@ -1,6 +1,7 @@
 // Acceptance test, first rejection, residual resampling and output assembly.
 //
-// Two launches.  The sums kernel runs S workgroups of 8 waves per request;
+// Two launches, or one in a step.  The sums kernel runs S workgroups of 8
+// waves per request;
 // each workgroup
 //  1. gathers the ratio-test operands (draft token, its logit or probability,
 //     its draft probability, the draw) and, with the vocabulary kernel's
@@ -17,6 +18,9 @@
 // prefix-sums the segment totals (Z is the last), finds the segment holding
 // u * Z, scans it in token order for the first entry whose running sum
 // exceeds u * Z, and writes the emitted tokens and the new cache length.
+// In a whole verification step both run as one launch (accept_fused_kernel):
+// the last workgroup of each request to finish its sums, counted by an
+// arrival counter that the step's vocabulary launch clears, runs the pick.
 // p(v) = exp(logit - lse) is evaluated in float64 from the float32 inputs.
 #include <hip/hip_ext.h>
 #include <string.h>
@@ -92,6 +96,11 @@ constexpr int kPerLane = kSeg / kWave;  // lane holds entries sg*512 + e*64 + la
 constexpr int kMaxSeg = 4096;           // vocabularies up to 2,097,152 entries
 constexpr int kSegBatch = 4;            // segments whose loads a wave issues together
 constexpr int kTargetGroups = 512;      // sums-kernel workgroups aimed for per launch
+// The fused kernel keeps two workgroups per CU (at most 128 registers), like
+// the sums kernel, so its carried merge runs beside the sums; that register
+// cap takes a segment batch of 3.
+constexpr int kFusedWgsPerCu = 2;
+constexpr int kFusedSegBatch = 3;
 
 // r over one segment, per lane (entries sg*512 + e*64 + lane): the raw loads
 // (indexes past the vocabulary clamped), then r from them.
@@ -169,73 +178,75 @@ __device__ __forceinline__ double segment_total(const double (&r)[kPerLane]) {
 }
 
 // Totals of segments [sg0, sg1) into out[]: wave w takes sg0 + w, sg0 + w +
-// nwaves, ..., issuing the loads of up to kSegBatch segments before reducing
-// any.  Batch entries past sg1 are skipped (wave-uniform), so a wave with a
+// nwaves, ..., issuing the loads of up to SB segments (kSegBatch, or fewer
+// where registers are short) before reducing any.  Batch entries past sg1 are skipped (wave-uniform), so a wave with a
 // single segment issues and reduces only that one.
-template <int PM, bool RES>
+// Global totals are stored as device-scope atomic stores (written through to
+// the device-coherent level), which the fused launch's last workgroup reads
+// with device-scope atomic loads; `out` in LDS takes plain stores.
+template <int PM, bool RES, int SB>
 __device__ __forceinline__ void segment_totals_t(const float* xrow, const float* qrow, const RowP& rp, int V, int sg0,
-                                                 int sg1, int nwaves, double* out) {
+                                                 int sg1, int nwaves, double* out, bool global_out) {
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  for (int s0 = sg0 + wave; s0 < sg1; s0 += nwaves * kSegBatch) {
-    float xs[kSegBatch][kPerLane], qs[kSegBatch][kPerLane];
+  for (int s0 = sg0 + wave; s0 < sg1; s0 += nwaves * SB) {
+    float xs[SB][kPerLane], qs[SB][kPerLane];
 #pragma unroll
-    for (int k = 0; k < kSegBatch; ++k)
+    for (int k = 0; k < SB; ++k)
       if (s0 + k * nwaves < sg1) segment_issue<RES>(xrow, qrow, V, s0 + k * nwaves, xs[k], qs[k]);
 #pragma unroll
-    for (int k = 0; k < kSegBatch; ++k) {
+    for (int k = 0; k < SB; ++k) {
       const int sg = s0 + k * nwaves;
       if (sg >= sg1) break;
       double r[kPerLane];
       segment_finish<PM, RES>(rp, V, sg, xs[k], qs[k], r);
       const double t = segment_total(r);
-      if (lane == 0) out[sg] = t;
+      if (lane == 0) {
+        if (global_out) __hip_atomic_store(out + sg, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        else out[sg] = t;
+      }
     }
   }
 }
 
+template <int SB = kSegBatch>
 __device__ __forceinline__ void segment_totals(const AcceptArgs& a, const float* xrow, const float* qrow,
                                                const RowP& rp, bool residual, int sg0, int sg1, int nwaves,
-                                               double* out) {
+                                               double* out, bool global_out = true) {
   switch (p_mode(a)) {
     case kWarped:
-      if (residual) segment_totals_t<kWarped, true>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
-      else segment_totals_t<kWarped, false>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
+      if (residual) segment_totals_t<kWarped, true, SB>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out, global_out);
+      else segment_totals_t<kWarped, false, SB>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out, global_out);
       break;
     case kLogits:
-      if (residual) segment_totals_t<kLogits, true>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
-      else segment_totals_t<kLogits, false>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
+      if (residual) segment_totals_t<kLogits, true, SB>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out, global_out);
+      else segment_totals_t<kLogits, false, SB>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out, global_out);
       break;
     default:
-      if (residual) segment_totals_t<kProbs, true>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
-      else segment_totals_t<kProbs, false>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out);
+      if (residual) segment_totals_t<kProbs, true, SB>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out, global_out);
+      else segment_totals_t<kProbs, false, SB>(xrow, qrow, rp, a.V, sg0, sg1, nwaves, out, global_out);
   }
 }
 
-// Grid (S, requests); workgroup s covers segments [s * segs_per_group, ...).
-__global__ __launch_bounds__(kSumWaves * kWave)
-void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* __restrict__ partials, int ntiles,
-                        int32_t* __restrict__ accept_len) {
-  __shared__ float s_lse[kWave];
-  __shared__ WarpRow s_warp[kWave];
-  __shared__ int s_l;
-  const int s = blockIdx.x;
-  const int req = bt.req0 + blockIdx.y;
+// LDS of one request's workgroup in the sums stage.
+struct SumsLds {
+  float lse[kWave];
+  WarpRow warp[kWave];
+  int l;
+};
+
+// Steps 1-3 for workgroup s of request req (chain or warped mode), SB
+// segments' loads in flight per wave: the row
+// log-sum-exps and warps land in sl, the accept length in sl.l (and in
+// accept_len from workgroup 0), this workgroup's segment totals in a.segsum.
+template <int SB>
+__device__ __forceinline__ void sums_request(const AcceptArgs& a, const float2* __restrict__ partials, int ntiles,
+                                             int32_t* __restrict__ accept_len, int s, int req, SumsLds& sl) {
+  float* s_lse = sl.lse;
+  WarpRow* s_warp = sl.warp;
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int G = a.gamma + 1;
-
-  if (a.tree != nullptr) {
-    // Tree verification: the walk chose the row; sum its p (the rejected
-    // candidates are taken out by the pick kernel).
-    const int pos = a.tree[req].pos;
-    const int64_t row = (int64_t)req * G + pos;
-    const RowP rp = row_p(a, row, a.lse != nullptr ? a.lse[row] : 0.f);
-    const int sg0 = s * a.segs_per_group;
-    const int sg1 = min(a.nseg, sg0 + a.segs_per_group);
-    segment_totals(a, a.x + row * a.V, nullptr, rp, false, sg0, sg1, kSumWaves, a.segsum + (int64_t)req * a.nseg);
-    return;
-  }
 
   // 1. Test operands (gathered by the last wave, whose second load waits on
   // the draft tokens), and the row log-sum-exp folds (row j on wave j mod
@@ -293,12 +304,12 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
     const unsigned long long fails = __ballot(fail);
     const int l = fails ? (__ffsll(fails) - 1) : a.gamma;
     if (lane == 0) {
-      s_l = l;
+      sl.l = l;
       if (s == 0) accept_len[req] = l;
     }
   }
   __syncthreads();
-  const int l = s_l;
+  const int l = sl.l;
   RowP rp{a.lse != nullptr ? s_lse[l] : 0.f, 1.f, 0u, -1};
   if (a.warp != nullptr) {
     const WarpRow w = s_warp[l];
@@ -311,71 +322,68 @@ void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* 
   // 3. This workgroup's segment totals.
   const int sg0 = s * a.segs_per_group;
   const int sg1 = min(a.nseg, sg0 + a.segs_per_group);
-  segment_totals(a, xrow, qrow, rp, residual, sg0, sg1, kSumWaves, a.segsum + (int64_t)req * a.nseg);
+  segment_totals<SB>(a, xrow, qrow, rp, residual, sg0, sg1, kSumWaves, a.segsum + (int64_t)req * a.nseg);
 }
 
-// One wave per request: prefix of the segment totals, the segment holding
-// u * Z, and the scan of that segment in token order.  Blocks past the
-// requests carry an attention merge (cj.nblocks blocks), which then runs in
-// the idle CUs of this latency-bound launch; a request's block uses its
-// first wave only.
-__global__ __launch_bounds__(kCombineThreads)
-void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t* __restrict__ accept_len,
-                        int32_t* __restrict__ out_tok, int32_t* __restrict__ new_kv_len, const CombineJob cj) {
-  __shared__ double seg[kMaxSeg];
-  if ((int)blockIdx.x >= bt.nreq) {
-    combine_job_block(cj, blockIdx.x - bt.nreq, threadIdx.x);
+// Grid (S, requests); workgroup s covers segments [s * segs_per_group, ...).
+__global__ __launch_bounds__(kSumWaves * kWave)
+void accept_sums_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* __restrict__ partials, int ntiles,
+                        int32_t* __restrict__ accept_len) {
+  __shared__ SumsLds sl;
+  const int s = blockIdx.x;
+  const int req = bt.req0 + blockIdx.y;
+  if (a.tree != nullptr) {
+    // Tree verification: the walk chose the row; sum its p (the rejected
+    // candidates are taken out by the pick kernel).
+    const int pos = a.tree[req].pos;
+    const int64_t row = (int64_t)req * (a.gamma + 1) + pos;
+    const RowP rp = row_p(a, row, a.lse != nullptr ? a.lse[row] : 0.f);
+    const int sg0 = s * a.segs_per_group;
+    const int sg1 = min(a.nseg, sg0 + a.segs_per_group);
+    segment_totals(a, a.x + row * a.V, nullptr, rp, false, sg0, sg1, kSumWaves, a.segsum + (int64_t)req * a.nseg);
     return;
   }
-  if (threadIdx.x >= kWave) return;
-  const int b = blockIdx.x;
-  const int req = bt.req0 + b;
-  const int lane = threadIdx.x;
-  const int G = a.gamma + 1;
-  const int nseg = a.nseg;
-  const double* tot = a.segsum + (int64_t)req * nseg;
+  sums_request<kSegBatch>(a, partials, ntiles, accept_len, s, req, sl);
+}
 
-  // Segment totals into LDS, 8 loads per lane in flight; l and u alongside,
-  // and everything else that does not depend on them: the drafts to emit and
-  // each row's normaliser (lane j: row j), so that only the segment loads
-  // wait for the draw's position.
-  const int l = accept_len[req];
-  const float uu = a.u[(int64_t)req * G + a.gamma];
-  const bool tree = a.tree != nullptr;
-  const int my_draft = (!tree && lane < a.gamma) ? a.draft[(int64_t)req * a.gamma + lane] : -1;
-  float my_lse = 0.f;
-  WarpRow my_warp{1.f, 0u, 0.f, -1};
-  if (lane < G) {
-    if (a.warp != nullptr) my_warp = a.warp[(int64_t)req * G + lane];
-    else if (a.lse != nullptr) my_lse = a.lse[(int64_t)req * G + lane];
-  }
+// Segment totals tot[0, nseg) into LDS seg[] by one wave, 8 loads per lane
+// in flight (device-scope atomic loads: the totals of other workgroups of
+// the same launch).
+__device__ __forceinline__ void pick_load_totals(const double* __restrict__ tot, int nseg, double* seg) {
+  const int lane = threadIdx.x & 63;
   for (int base = 0; base < nseg; base += 8 * kWave) {
     double v[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = tot[min(base + k * kWave + lane, nseg - 1)];
+    for (int k = 0; k < 8; ++k)
+      v[k] = __hip_atomic_load(tot + min(base + k * kWave + lane, nseg - 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
     for (int k = 0; k < 8; ++k)
       if (base + k * kWave + lane < nseg) seg[base + k * kWave + lane] = v[k];
   }
-  // Chain: row l, residual after a rejection.  Tree: the walk's final row,
-  // plain p without the candidates rejected there.
-  const int pos = tree ? a.tree[req].pos : l;
-  const int nrej = tree ? a.tree[req].nrej : 0;
-  const int rej = tree && lane < nrej ? a.tree[req].rej_tok[lane] : -1;
+}
+
+// The rest of the draw of request req = bt.req0 + b on one wave, once the
+// segment totals are in seg[] (LDS) and the accept length l, the row's p
+// (rp, of position pos) and the draw uu are known: the candidates rejected at
+// a tree's final position are taken out, the totals are prefix-summed, the
+// segment holding u * Z is scanned in token order, and the outputs are
+// written.  my_draft: lane i < gamma holds draft token i (chain).  s_rej: a
+// kWave-entry LDS array.
+__device__ __forceinline__ void pick_finish(const AcceptArgs& a, const AcceptBatch& bt, int b, int l, int pos,
+                                            int nrej, int rej, const RowP& rp, float uu, int my_draft,
+                                            double* seg, int* s_rej, int32_t* __restrict__ out_tok,
+                                            int32_t* __restrict__ new_kv_len) {
+  const int req = bt.req0 + b;
+  const int lane = threadIdx.x & 63;
+  const int G = a.gamma + 1;
+  const int nseg = a.nseg;
+  const bool tree = a.tree != nullptr;
   const int64_t row = (int64_t)req * G + pos;
-  RowP rp{__shfl(my_lse, pos), 1.f, 0u, -1};
-  if (a.warp != nullptr) {
-    rp.lse = __shfl(my_warp.lse, pos);
-    rp.inv_t = __shfl(my_warp.inv_t, pos);
-    rp.theta = (uint32_t)__shfl((int)my_warp.theta, pos);
-    rp.argmax = __shfl(my_warp.argmax, pos);
-  }
   bool residual = !tree && l < a.gamma;
   const float* xrow = a.x + row * a.V;
   const float* qrow = residual ? a.q + ((int64_t)req * a.gamma + l) * a.V : nullptr;
   // The p of each rejected candidate, evaluated as the segment sums did, is
   // taken out of its segment (in candidate order, so deterministically).
-  __shared__ int s_rej[kWave];
   const double rej_p = (tree && rej >= 0) ? p_of_mode(a, rp, xrow[rej], rej) : 0.0;
   s_rej[lane] = rej;
   lds_wait();
@@ -412,7 +420,7 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
     // (tree: from the final row's p, no candidate excluded).
     residual = false;
     nexcl = 0;
-    segment_totals(a, xrow, qrow, rp, false, 0, nseg, 1, seg);
+    segment_totals(a, xrow, qrow, rp, false, 0, nseg, 1, seg, false);
     z = prefix();
   }
 
@@ -467,6 +475,109 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
     out_tok[(int64_t)req * G + lane] = v;
   }
   if (lane == 0 && new_kv_len != nullptr && bt.has_kv_len) new_kv_len[req] = bt.kv_len[b] - a.gamma + l;
+}
+
+// One wave per request: prefix of the segment totals, the segment holding
+// u * Z, and the scan of that segment in token order.  Blocks past the
+// requests carry an attention merge (cj.nblocks blocks), which then runs in
+// the idle CUs of this latency-bound launch; a request's block uses its
+// first wave only.
+__global__ __launch_bounds__(kCombineThreads)
+void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t* __restrict__ accept_len,
+                        int32_t* __restrict__ out_tok, int32_t* __restrict__ new_kv_len, const CombineJob cj) {
+  __shared__ double seg[kMaxSeg];
+  if ((int)blockIdx.x >= bt.nreq) {
+    combine_job_block(cj, blockIdx.x - bt.nreq, threadIdx.x);
+    return;
+  }
+  if (threadIdx.x >= kWave) return;
+  const int b = blockIdx.x;
+  const int req = bt.req0 + b;
+  const int lane = threadIdx.x;
+  const int G = a.gamma + 1;
+  const int nseg = a.nseg;
+  const double* tot = a.segsum + (int64_t)req * nseg;
+
+  // Segment totals into LDS, 8 loads per lane in flight; l and u alongside,
+  // and everything else that does not depend on them: the drafts to emit and
+  // each row's normaliser (lane j: row j), so that only the segment loads
+  // wait for the draw's position.
+  const int l = accept_len[req];
+  const float uu = a.u[(int64_t)req * G + a.gamma];
+  const bool tree = a.tree != nullptr;
+  const int my_draft = (!tree && lane < a.gamma) ? a.draft[(int64_t)req * a.gamma + lane] : -1;
+  float my_lse = 0.f;
+  WarpRow my_warp{1.f, 0u, 0.f, -1};
+  if (lane < G) {
+    if (a.warp != nullptr) my_warp = a.warp[(int64_t)req * G + lane];
+    else if (a.lse != nullptr) my_lse = a.lse[(int64_t)req * G + lane];
+  }
+  pick_load_totals(tot, nseg, seg);
+  // Chain: row l, residual after a rejection.  Tree: the walk's final row,
+  // plain p without the candidates rejected there.
+  const int pos = tree ? a.tree[req].pos : l;
+  const int nrej = tree ? a.tree[req].nrej : 0;
+  const int rej = tree && lane < nrej ? a.tree[req].rej_tok[lane] : -1;
+  RowP rp{__shfl(my_lse, pos), 1.f, 0u, -1};
+  if (a.warp != nullptr) {
+    rp.lse = __shfl(my_warp.lse, pos);
+    rp.inv_t = __shfl(my_warp.inv_t, pos);
+    rp.theta = (uint32_t)__shfl((int)my_warp.theta, pos);
+    rp.argmax = __shfl(my_warp.argmax, pos);
+  }
+  __shared__ int s_rej[kWave];
+  pick_finish(a, bt, b, l, pos, nrej, rej, rp, uu, my_draft, seg, s_rej, out_tok, new_kv_len);
+}
+
+// Chain and warped modes in one launch (the verification step): the sums
+// stage of accept_sums_kernel, after which the last workgroup of each request
+// to finish its segment totals (counted by a per-request arrival counter,
+// which the vocabulary launch that precedes this one in the step clears)
+// draws the request's token on its first wave, as accept_pick_kernel does.
+// Workgroups past the requests carry an attention merge, two merge blocks
+// each.
+__global__ __launch_bounds__(kSumWaves * kWave, kFusedWgsPerCu * kSumWaves / 4)  // waves per SIMD
+void accept_fused_kernel(const AcceptArgs a, const AcceptBatch bt, const float2* __restrict__ partials, int ntiles,
+                         int32_t* __restrict__ accept_len, int32_t* __restrict__ out_tok,
+                         int32_t* __restrict__ new_kv_len, int* __restrict__ arrivals, const CombineJob cj) {
+  __shared__ SumsLds sl;
+  __shared__ double seg[kMaxSeg];
+  __shared__ int s_rej[kWave];
+  __shared__ int s_last;
+  static_assert(kSumWaves * kWave == 2 * kCombineThreads, "two merge blocks per workgroup");
+  if ((int)blockIdx.y >= bt.nreq) {
+    const int k = (((int)blockIdx.y - bt.nreq) * (int)gridDim.x + (int)blockIdx.x) * 2 +
+                  ((int)threadIdx.x >= kCombineThreads ? 1 : 0);
+    if (k < cj.nblocks) combine_job_block(cj, k, threadIdx.x & (kCombineThreads - 1));
+    return;
+  }
+  const int b = blockIdx.y;
+  const int req = bt.req0 + b;
+  sums_request<kFusedSegBatch>(a, partials, ntiles, accept_len, blockIdx.x, req, sl);
+  // Count this workgroup in once its totals are published; the last of the
+  // request's gridDim.x workgroups goes on.  The totals are device-scope
+  // atomic stores; every wave waits until its stores have completed, and
+  // the barrier orders those waits before the arrival.  The last workgroup
+  // issues its device-scope atomic loads of the totals only after its own
+  // arrival returned, i.e. after every other arrival and so after every
+  // store it waits on had completed: no cache write-back or invalidation is
+  // needed on either side.
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(arrivals + req, 1) == (int)gridDim.x - 1 ? 1 : 0;
+  __syncthreads();
+  if (s_last == 0 || threadIdx.x >= kWave) return;
+  const int lane = threadIdx.x;
+  const int l = sl.l;
+  const float uu = a.u[(int64_t)req * (a.gamma + 1) + a.gamma];
+  const int my_draft = lane < a.gamma ? a.draft[(int64_t)req * a.gamma + lane] : -1;
+  pick_load_totals(a.segsum + (int64_t)req * a.nseg, a.nseg, seg);
+  RowP rp{a.lse != nullptr ? sl.lse[l] : 0.f, 1.f, 0u, -1};
+  if (a.warp != nullptr) {
+    const WarpRow w = sl.warp[l];
+    rp = RowP{w.lse, w.inv_t, w.theta, w.argmax};
+  }
+  pick_finish(a, bt, b, l, l, 0, -1, rp, uu, my_draft, seg, s_rej, out_tok, new_kv_len);
 }
 
 // Tree verification, one wave per request (N = gamma nodes, N + 1 <= 64
@@ -556,17 +667,24 @@ void tree_walk_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t* _
 
 }  // namespace
 
-size_t accept_workspace_bytes(int B, int V) {
+// Workspace: segment totals [B][nseg] (float64), then one arrival counter
+// per request (the fused launch).
+static size_t segsum_bytes(int B, int V) {
   const int nseg = (V + kSeg - 1) / kSeg;
-  return sizeof(double) * static_cast<size_t>(B) * nseg;
+  return (sizeof(double) * static_cast<size_t>(B) * nseg + 255) / 256 * 256;
+}
+
+size_t accept_workspace_bytes(int B, int V) { return segsum_bytes(B, V) + sizeof(int) * static_cast<size_t>(B); }
+
+int* accept_arrivals(void* ws, int B, int V) {
+  return reinterpret_cast<int*>(static_cast<char*>(ws) + segsum_bytes(B, V));
 }
 
 hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
                          const float2* partials, int ntiles, const float* q_draft, const int32_t* draft_tok,
                          const float* u, void* ws, int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
                          hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop, const WarpRow* warp,
-                         const CombineJob* combine) {
-  (void)B;
+                         const CombineJob* combine, bool fused) {
   if (bt.nreq <= 0) return hipSuccess;
   AcceptArgs a;
   a.gamma = gamma;
@@ -586,13 +704,21 @@ hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& bt, const f
   a.u = u;
   a.segsum = static_cast<double*>(ws);
   const int S = (a.nseg + a.segs_per_group - 1) / a.segs_per_group;
+  CombineJob cj;
+  memset(&cj, 0, sizeof(cj));
+  if (combine != nullptr) cj = *combine;
+  if (fused) {
+    // One launch; the arrival counters were cleared by an earlier launch.
+    const int extra = cj.nblocks > 0 ? ((cj.nblocks + 1) / 2 + S - 1) / S : 0;
+    hipExtLaunchKernelGGL(accept_fused_kernel, dim3(S, bt.nreq + extra), dim3(kSumWaves * kWave), 0, stream, ev_start,
+                          ev_stop, 0, a, bt, warp != nullptr ? nullptr : partials, ntiles, accept_len, out_tok,
+                          new_kv_len, accept_arrivals(ws, B, V), cj);
+    return hipGetLastError();
+  }
   hipExtLaunchKernelGGL(accept_sums_kernel, dim3(S, bt.nreq), dim3(kSumWaves * kWave), 0, stream, ev_start, nullptr,
                         0, a, bt, warp != nullptr ? nullptr : partials, ntiles, accept_len);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  CombineJob cj;
-  memset(&cj, 0, sizeof(cj));
-  if (combine != nullptr) cj = *combine;
   hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq + cj.nblocks), dim3(kCombineThreads), 0, stream, nullptr,
                         ev_stop, 0, a, bt, accept_len, out_tok, new_kv_len, cj);
   return hipGetLastError();
@@ -620,8 +746,8 @@ hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& bt, const 
   a.q = nullptr;
   a.draft = nullptr;
   a.u = u;
-  // Workspace: segment totals [B][nseg], then one TreeFinal per request (all
-  // requests, indexed by the global request number).
+  // Workspace: segment totals [B][nseg] and the arrival counters, then one
+  // TreeFinal per request (all requests, indexed by the global request number).
   const size_t seg_bytes = (accept_workspace_bytes(B, V) + 255) / 256 * 256;
   a.segsum = static_cast<double*>(ws);
   TreeFinal* fin = reinterpret_cast<TreeFinal*>(static_cast<char*>(ws) + seg_bytes);

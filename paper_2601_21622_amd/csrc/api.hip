@@ -199,7 +199,7 @@ int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const f
                const float* q_draft, const int32_t* draft_tok, const float* u, const int32_t* kv_len,
                int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len, void* ws, hipStream_t stream,
                hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr, const WarpRow* warp = nullptr,
-               const std::vector<CombineJob>* merges = nullptr) {
+               const std::vector<CombineJob>* merges = nullptr, bool fused = false) {
   for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
     AcceptBatch bt;
     memset(&bt, 0, sizeof(bt));
@@ -213,7 +213,7 @@ int run_accept(const sd_dims_t* d, const float* x, const float* row_lse, const f
     const CombineJob* cj = merges != nullptr ? &(*merges)[r0 / kMaxReqPerLaunch] : nullptr;
     hipError_t e = launch_accept(d->gamma, d->vocab, d->batch, bt, x, row_lse, partials, ntiles, q_draft, draft_tok,
                                  u, ws, accept_len, out_tok, new_kv_len, stream, first ? ev_start : nullptr,
-                                 last ? ev_stop : nullptr, warp, cj);
+                                 last ? ev_stop : nullptr, warp, cj, fused);
     if (e != hipSuccess) return SD_ERR_HIP;
   }
   return SD_OK;
@@ -485,12 +485,14 @@ int verify_step(const sd_dims_t* dims, const void* q, const void* k_pool, const 
   void* vws = static_cast<char*>(workspace) + base;
   const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab, (dims->flags & SD_FLAG_PACKED_VOCAB) != 0);
   float2* partials = static_cast<float2*>(vws);
-  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, vws, stm, ev[2],
-                   ev[3]) != hipSuccess)
-    return SD_ERR_HIP;
+  // The projection launch clears the acceptance's arrival counters, so the
+  // acceptance runs as one launch.
   void* acc_ws = static_cast<char*>(vws) + logits_ws(dims);
+  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, vws, stm, ev[2], ev[3],
+                   accept_arrivals(acc_ws, dims->batch, dims->vocab), dims->batch) != hipSuccess)
+    return SD_ERR_HIP;
   return run_accept(dims, logits, row_lse, partials, vp.ntiles, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
-                    new_kv_len, acc_ws, stm, ev[4], ev[5], nullptr, defer ? &merges : nullptr);
+                    new_kv_len, acc_ws, stm, ev[4], ev[5], nullptr, defer ? &merges : nullptr, true);
 }
 
 }  // namespace
@@ -557,16 +559,18 @@ int sd_verify_step_sampled(const sd_dims_t* dims, const sd_sampling_t* sampling,
   if (st != SD_OK) return st;
   const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab,
                                   (dims->flags & SD_FLAG_PACKED_VOCAB) != 0);
-  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, workspace, stm, ev[2],
-                   ev[3]) != hipSuccess)
-    return SD_ERR_HIP;
+  // The projection launch clears the acceptance's arrival counters, so the
+  // acceptance runs as one launch.
   void* acc_ws = static_cast<char*>(workspace) + logits_ws(dims);
+  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, workspace, stm, ev[2],
+                   ev[3], accept_arrivals(acc_ws, dims->batch, dims->vocab), dims->batch) != hipSuccess)
+    return SD_ERR_HIP;
   WarpRow* warp = reinterpret_cast<WarpRow*>(static_cast<char*>(acc_ws) + accept_ws(dims));
   if (launch_warp(dims->batch * (dims->gamma + 1), dims->vocab, logits, sampling->temperature, sampling->top_k,
                   sampling->top_p, warp, row_lse, row_min_logit, stm, ev[4]) != hipSuccess)
     return SD_ERR_HIP;
   return run_accept(dims, logits, nullptr, nullptr, 0, q_draft, draft_tok, u, kv_len, accept_len, out_tok,
-                    new_kv_len, acc_ws, stm, nullptr, ev[5], warp);
+                    new_kv_len, acc_ws, stm, nullptr, ev[5], warp, nullptr, true);
 }
 
 int sd_accept_tree(const sd_dims_t* dims, const float* logits_or_probs, const float* row_lse, const int32_t* tokens,

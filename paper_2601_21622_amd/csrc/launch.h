@@ -92,9 +92,11 @@ hipError_t launch_pack_vocab(int K, int V, const void* w, void* out, hipStream_t
 // (float2[M][ntiles]) at its start, then, for the deep schedule, the hidden
 // rows repacked into MFMA fragments.
 size_t vocab_workspace_bytes(const VocabPlan& p);
+// `clear` (nclear ints, may be null) is set to zero by the launch: the
+// acceptance's arrival counters, for a fused acceptance launch that follows.
 hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w,
                         float* logits, void* workspace, hipStream_t stream, hipEvent_t ev_start,
-                        hipEvent_t ev_stop);
+                        hipEvent_t ev_stop, int* clear = nullptr, int nclear = 0);
 hipError_t launch_lse_combine(const VocabPlan& p, const float2* partials, float* row_lse,
                               hipStream_t stream);
 
@@ -122,6 +124,9 @@ struct AcceptBatch {
   int32_t kv_len[kMaxReqPerLaunch];
 };
 size_t accept_workspace_bytes(int B, int V);
+// The per-request arrival counters of the fused launch inside an acceptance
+// workspace of accept_workspace_bytes(B, V) (B ints, global request index).
+int* accept_arrivals(void* ws, int B, int V);
 // x: logits with row_lse, or probabilities when row_lse is null.  With
 // `partials` (the vocabulary kernel's per-tile statistics, ntiles per row) the
 // row log-sum-exp is folded first and written to row_lse.  ws holds
@@ -130,13 +135,16 @@ size_t accept_workspace_bytes(int B, int V);
 // With `warp` (one WarpRow per row, from launch_warp) x holds logits and the
 // test and correction use the warped p'; row_lse and partials are then unused.
 // With `combine`, the pick launch also carries that attention merge.
+// With `fused`, the sums and the pick run as one launch, which needs the
+// arrival counters (accept_arrivals) of every request of the batch cleared by
+// an earlier launch on the stream.
 struct CombineJob;
 hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& batch, const float* x,
                          const float* row_lse, const float2* partials, int ntiles,
                          const float* q_draft, const int32_t* draft_tok, const float* u, void* ws,
                          int32_t* accept_len, int32_t* out_tok, int32_t* new_kv_len,
                          hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop,
-                         const WarpRow* warp = nullptr, const CombineJob* combine = nullptr);
+                         const WarpRow* warp = nullptr, const CombineJob* combine = nullptr, bool fused = false);
 
 // Tree verification (N = gamma nodes, position 0 the root, position i + 1 node
 // i): walk the candidate tree, then draw the final token.  ws holds

@@ -42,6 +42,13 @@ namespace sdv {
 namespace {
 
 constexpr int kVThreads = 256;
+
+// Counters a later launch on the stream expects at zero (the acceptance's
+// arrival counters): cleared by the first workgroup of a vocabulary launch.
+__device__ __forceinline__ void clear_counters(int* __restrict__ clear, int nclear) {
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < nclear; i += blockDim.x) clear[i] = 0;
+}
 constexpr int kTileN = 64;  // vocabulary rows per workgroup (4 waves x 16)
 
 // Epilogue of one workgroup of WM x WN waves.  Wave (wm, wn) = (wave / WN,
@@ -162,8 +169,9 @@ template <int MB, int KC, int NW, bool PACKED>
 __global__ __launch_bounds__(NW * kWave)
 void vocab_bf16_kernel(int M, int K, int V, int ntiles, const uint16_t* __restrict__ hidden,
                        const uint16_t* __restrict__ w, float* __restrict__ logits,
-                       float2* __restrict__ partials) {
+                       float2* __restrict__ partials, int* __restrict__ clear, int nclear) {
   using C = VocabCfg<MB, KC, NW>;
+  clear_counters(clear, nclear);
   __shared__ __align__(16) unsigned char abuf[2][C::kBufBytes];
   __shared__ float red[NW][16 * MB];
 
@@ -611,7 +619,9 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
 // fragment (k16, mb) holds row mb*32 + l%32, k 16*k16 + 8*(l/32) .. +8; rows
 // past M are zero.  One thread per 16-byte piece, writes coalesced.
 __global__ __launch_bounds__(kVThreads)
-void pack_hidden_kernel(int M, int K, const uint16_t* __restrict__ hidden, uint16_t* __restrict__ out) {
+void pack_hidden_kernel(int M, int K, const uint16_t* __restrict__ hidden, uint16_t* __restrict__ out,
+                        int* __restrict__ clear, int nclear) {
+  clear_counters(clear, nclear);
   const int mbt = (M + 31) / 32;
   const int64_t pieces = (int64_t)(K / 16) * mbt * 64;
   for (int64_t i = (int64_t)blockIdx.x * kVThreads + threadIdx.x; i < pieces; i += (int64_t)gridDim.x * kVThreads) {
@@ -631,7 +641,8 @@ constexpr int kF32KC = 32;
 __global__ __launch_bounds__(kVThreads)
 void vocab_f32_kernel(int M, int K, int V, int ntiles, const float* __restrict__ hidden,
                       const float* __restrict__ w, float* __restrict__ logits,
-                      float2* __restrict__ partials) {
+                      float2* __restrict__ partials, int* __restrict__ clear, int nclear) {
+  clear_counters(clear, nclear);
   __shared__ float wt[kF32KC][kTileN + 1];  // [k][vocab]
   __shared__ float ht[64][kF32KC + 1];      // [row][k]
   const int tile = blockIdx.x;
@@ -703,33 +714,33 @@ void pack_vocab_kernel(int K, int V, const uint16_t* __restrict__ w, uint16_t* _
 
 template <int MB, int KC>
 hipError_t launch_shallow(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
-                          hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+                          hipStream_t stream, hipEvent_t e0, hipEvent_t e1, int* clear, int nclear) {
   const dim3 grid(p.ntiles, p.mtiles), block(kShallowWaves * kWave);
   const uint16_t* h = static_cast<const uint16_t*>(hidden);
   const uint16_t* wv = static_cast<const uint16_t*>(w);
   if (p.packed)
     hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC, kShallowWaves, true>), grid, block, 0, stream, e0, e1, 0, p.M,
-                          p.K, p.V, p.ntiles, h, wv, logits, partials);
+                          p.K, p.V, p.ntiles, h, wv, logits, partials, clear, nclear);
   else
     hipExtLaunchKernelGGL((vocab_bf16_kernel<MB, KC, kShallowWaves, false>), grid, block, 0, stream, e0, e1, 0, p.M,
-                          p.K, p.V, p.ntiles, h, wv, logits, partials);
+                          p.K, p.V, p.ntiles, h, wv, logits, partials, clear, nclear);
   return hipGetLastError();
 }
 
 template <int MB>
 hipError_t launch_shallow_mb(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
-                             hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
-  if (p.K % 256 == 0) return launch_shallow<MB, 256>(p, hidden, w, logits, partials, stream, e0, e1);
-  return launch_shallow<MB, 32>(p, hidden, w, logits, partials, stream, e0, e1);
+                             hipStream_t stream, hipEvent_t e0, hipEvent_t e1, int* clear, int nclear) {
+  if (p.K % 256 == 0) return launch_shallow<MB, 256>(p, hidden, w, logits, partials, stream, e0, e1, clear, nclear);
+  return launch_shallow<MB, 32>(p, hidden, w, logits, partials, stream, e0, e1, clear, nclear);
 }
 
 template <int MB, int NB, int NW, int S = (NW == 8 ? 3 : 6)>
 hipError_t launch_deep(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
-                       uint16_t* hpacked, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+                       uint16_t* hpacked, hipStream_t stream, hipEvent_t e0, hipEvent_t e1, int* clear, int nclear) {
   const int64_t pieces = (int64_t)(p.K / 16) * ((p.M + 31) / 32) * 64;
   const int pblocks = (int)std::min<int64_t>((pieces + kVThreads - 1) / kVThreads, 4096);
   hipExtLaunchKernelGGL(pack_hidden_kernel, dim3(pblocks), dim3(kVThreads), 0, stream, e0, nullptr, 0, p.M, p.K,
-                        static_cast<const uint16_t*>(hidden), hpacked);
+                        static_cast<const uint16_t*>(hidden), hpacked, clear, nclear);
   const dim3 grid((p.ntiles + 7) / 8 * 8 * p.mtiles), block(NW * kWave);
   const uint16_t* wv = static_cast<const uint16_t*>(w);
   if (p.packed)
@@ -838,26 +849,27 @@ size_t vocab_workspace_bytes(const VocabPlan& p) {
 }
 
 hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const void* w, float* logits,
-                        void* workspace, hipStream_t stream, hipEvent_t e0, hipEvent_t e1) {
+                        void* workspace, hipStream_t stream, hipEvent_t e0, hipEvent_t e1, int* clear, int nclear) {
+  if (clear == nullptr) nclear = 0;
   float2* partials = static_cast<float2*>(workspace);
   uint16_t* hpacked = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + partial_bytes(p));
   if (dtype == 0) {
     hipExtLaunchKernelGGL(vocab_f32_kernel, dim3(p.ntiles, p.mtiles), dim3(kVThreads), 0, stream, e0, e1, 0, p.M, p.K,
                           p.V, p.ntiles, static_cast<const float*>(hidden), static_cast<const float*>(w), logits,
-                          partials);
+                          partials, clear, nclear);
     return hipGetLastError();
   }
   if (!p.deep) {
     switch (p.mblocks) {
-      case 1: return launch_shallow_mb<1>(p, hidden, w, logits, partials, stream, e0, e1);
-      case 2: return launch_shallow_mb<2>(p, hidden, w, logits, partials, stream, e0, e1);
-      case 3: return launch_shallow_mb<3>(p, hidden, w, logits, partials, stream, e0, e1);
-      case 4: return launch_shallow_mb<4>(p, hidden, w, logits, partials, stream, e0, e1);
+      case 1: return launch_shallow_mb<1>(p, hidden, w, logits, partials, stream, e0, e1, clear, nclear);
+      case 2: return launch_shallow_mb<2>(p, hidden, w, logits, partials, stream, e0, e1, clear, nclear);
+      case 3: return launch_shallow_mb<3>(p, hidden, w, logits, partials, stream, e0, e1, clear, nclear);
+      case 4: return launch_shallow_mb<4>(p, hidden, w, logits, partials, stream, e0, e1, clear, nclear);
       default: return hipErrorInvalidValue;
     }
   }
 #define SDV_D(B, N, W) \
-  case B: return launch_deep<B, N, W>(p, hidden, w, logits, partials, hpacked, stream, e0, e1);
+  case B: return launch_deep<B, N, W>(p, hidden, w, logits, partials, hpacked, stream, e0, e1, clear, nclear);
   if (p.waves == 8) {
     switch (p.mblocks) {
       SDV_D(2, 2, 8) SDV_D(3, 2, 8) SDV_D(4, 2, 8) SDV_D(5, 2, 8)

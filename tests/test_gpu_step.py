@@ -63,3 +63,36 @@ def test_step_with_hidden(name):
 @pytest.mark.parametrize("name", ["tiny_f32", "vicuna_small"])
 def test_step_projects_attention_output(name):
     _check(name, False)
+
+
+# 70 requests: two acceptance launches (at most 64 requests each), whose
+# arrival counters are indexed by the global request number.
+MANY = get_config("vicuna7b").replace(batch=70, n_q_heads=4, n_kv_heads=4, hidden=256, vocab=5000,
+                                      lengths=("explicit", tuple(6 + 37 * i for i in range(70))))
+
+
+@pytest.mark.parametrize("fill", [0x00, 0xFF])
+def test_step_acceptance_on_a_stale_workspace(fill):
+    """The step's acceptance runs as one launch whose per-request arrival
+    counters live in the workspace; the step's projection launch clears them.
+    A workspace full of stale bytes, and a second step over the first one's
+    leftovers, give the same outputs as the two-launch sd_accept_resample on
+    the step's own logits and log-sum-exps, and both match the oracle."""
+    cfg = MANY
+    announce(f"stale-workspace step case=vicuna_many fill={fill:#x} B={cfg.batch}")
+    x = make_inputs(cfg)
+    db = DeviceBatch(x)
+    db.ws.fill_(fill)
+    db.step()
+    torch.cuda.synchronize()
+    first = (db.accept_len.clone(), db.out_tok.clone(), db.new_kv_len.clone())
+    db.step()
+    torch.cuda.synchronize()
+    for got, want in zip((db.accept_len, db.out_tok, db.new_kv_len), first):
+        assert torch.equal(got, want)
+    db.accept()  # two launches, on the step's logits and row log-sum-exps
+    torch.cuda.synchronize()
+    for got, want in zip((db.accept_len, db.out_tok, db.new_kv_len), first):
+        assert torch.equal(got, want)
+    ref = accept_resample(to_np(db.logits), to_np(db.lse), x.q_draft, x.draft, x.u, kv_len=x.kv_len)
+    assert_accept_parity(to_np(first[0]), to_np(first[1]), to_np(first[2]), ref)
