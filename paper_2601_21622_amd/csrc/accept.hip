@@ -529,11 +529,12 @@ void accept_pick_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t*
   pick_finish(a, bt, b, l, pos, nrej, rej, rp, uu, my_draft, seg, s_rej, out_tok, new_kv_len);
 }
 
-// Chain and warped modes in one launch (the verification step): the sums
-// stage of accept_sums_kernel, after which the last workgroup of each request
-// to finish its segment totals (counted by a per-request arrival counter,
-// which the vocabulary launch that precedes this one in the step clears)
-// draws the request's token on its first wave, as accept_pick_kernel does.
+// Chain, warped and tree modes in one launch (the verification steps): the
+// sums stage of accept_sums_kernel, after which the last workgroup of each
+// request to finish its segment totals (counted by a per-request arrival
+// counter, which the vocabulary launch that precedes this one in the step
+// clears) draws the request's token on its first wave, as accept_pick_kernel
+// does.
 // Workgroups past the requests carry an attention merge, two merge blocks
 // each.
 __global__ __launch_bounds__(kSumWaves * kWave, kFusedWgsPerCu * kSumWaves / 4)  // waves per SIMD
@@ -553,7 +554,21 @@ void accept_fused_kernel(const AcceptArgs a, const AcceptBatch bt, const float2*
   }
   const int b = blockIdx.y;
   const int req = bt.req0 + b;
-  sums_request<kFusedSegBatch>(a, partials, ntiles, accept_len, blockIdx.x, req, sl);
+  const int G = a.gamma + 1;
+  RowP rp_tree{0.f, 1.f, 0u, -1};
+  int pos_tree = 0;
+  if (a.tree != nullptr) {
+    // Tree verification: the walk (previous launch) chose the row; sum its p.
+    pos_tree = a.tree[req].pos;
+    const int64_t row = (int64_t)req * G + pos_tree;
+    rp_tree = row_p(a, row, a.lse != nullptr ? a.lse[row] : 0.f);
+    const int sg0 = blockIdx.x * a.segs_per_group;
+    const int sg1 = min(a.nseg, sg0 + a.segs_per_group);
+    segment_totals<kFusedSegBatch>(a, a.x + row * a.V, nullptr, rp_tree, false, sg0, sg1, kSumWaves,
+                                   a.segsum + (int64_t)req * a.nseg);
+  } else {
+    sums_request<kFusedSegBatch>(a, partials, ntiles, accept_len, blockIdx.x, req, sl);
+  }
   // Count this workgroup in once its totals are published; the last of the
   // request's gridDim.x workgroups goes on.  The totals are device-scope
   // atomic stores; every wave waits until its stores have completed, and
@@ -568,8 +583,17 @@ void accept_fused_kernel(const AcceptArgs a, const AcceptBatch bt, const float2*
   __syncthreads();
   if (s_last == 0 || threadIdx.x >= kWave) return;
   const int lane = threadIdx.x;
+  const float uu = a.u[(int64_t)req * G + a.gamma];
+  if (a.tree != nullptr) {
+    // The walk wrote the accept length and the candidates rejected at pos.
+    const int l = accept_len[req];
+    const int nrej = a.tree[req].nrej;
+    const int rej = lane < nrej ? a.tree[req].rej_tok[lane] : -1;
+    pick_load_totals(a.segsum + (int64_t)req * a.nseg, a.nseg, seg);
+    pick_finish(a, bt, b, l, pos_tree, nrej, rej, rp_tree, uu, -1, seg, s_rej, out_tok, new_kv_len);
+    return;
+  }
   const int l = sl.l;
-  const float uu = a.u[(int64_t)req * (a.gamma + 1) + a.gamma];
   const int my_draft = lane < a.gamma ? a.draft[(int64_t)req * a.gamma + lane] : -1;
   pick_load_totals(a.segsum + (int64_t)req * a.nseg, a.nseg, seg);
   RowP rp{a.lse != nullptr ? sl.lse[l] : 0.f, 1.f, 0u, -1};
@@ -591,33 +615,51 @@ void accept_fused_kernel(const AcceptArgs a, const AcceptBatch bt, const float2*
 // is drawn there from p without the rejected candidates by the sums and pick
 // kernels.  All test operands are gathered at once (lane i: node i's token
 // under its parent's row); the walk itself runs on registers and ballots.
-__global__ __launch_bounds__(kWave)
+// With `partials` (a whole tree step), the block's kSumWaves waves first fold
+// the request's row log-sum-exps from the vocabulary kernel's per-tile
+// statistics and write them to a.lse; wave 0 then walks.
+__global__ __launch_bounds__(kSumWaves * kWave)
 void tree_walk_kernel(const AcceptArgs a, const AcceptBatch bt, const int32_t* __restrict__ tokens,
                       const int32_t* __restrict__ parent, TreeFinal* __restrict__ fin,
                       int32_t* __restrict__ accept_len, int32_t* __restrict__ out_tok,
-                      int32_t* __restrict__ out_node, int32_t* __restrict__ new_kv_len) {
+                      int32_t* __restrict__ out_node, int32_t* __restrict__ new_kv_len,
+                      const float2* __restrict__ partials, int ntiles) {
+  __shared__ float s_lse[kWave];
   const int b = blockIdx.x;
   const int req = bt.req0 + b;
-  const int lane = threadIdx.x;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
   const int N = a.gamma;
   const int G = N + 1;
 
+  // Wave 0 gathers the test operands while the waves fold the row
+  // log-sum-exps (row j on wave j mod kSumWaves).
   int tok = -1, par = -1;
-  double pc = 0.0;
+  float xv = 0.f;
   float uc = 1.f;
-  if (lane < N) {
+  if (wave == 0 && lane < N) {
     tok = tokens[(int64_t)req * N + lane];
     const int pp = parent[(int64_t)req * N + lane];
     par = (pp >= -1 && pp < lane) ? pp : -1;
     uc = a.u[(int64_t)req * G + lane];
-    if (tok >= 0 && tok < a.V) {
-      const int64_t row = (int64_t)req * G + par + 1;
-      const float xv = a.x[row * a.V + tok];
-      pc = a.lse != nullptr ? exp((double)xv - (double)a.lse[row]) : (double)xv;
-    } else {
-      tok = -1;
-    }
+    if (tok >= 0 && tok < a.V) xv = a.x[((int64_t)req * G + par + 1) * a.V + tok];
+    else tok = -1;
   }
+  if (partials != nullptr) {
+    for (int j = wave; j < G; j += kSumWaves) {
+      const float v = row_lse_from_partials(partials + ((int64_t)req * G + j) * ntiles, ntiles);
+      if (lane == 0) {
+        s_lse[j] = v;
+        const_cast<float*>(a.lse)[(int64_t)req * G + j] = v;
+      }
+    }
+  } else if (a.lse != nullptr && threadIdx.x < G) {
+    s_lse[threadIdx.x] = a.lse[(int64_t)req * G + threadIdx.x];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  double pc = 0.0;
+  if (tok >= 0) pc = a.lse != nullptr ? exp((double)xv - (double)s_lse[par + 1]) : (double)xv;
 
   int pos = 0, l = 0, nrej = 0, rej_tok = -1;
   int path = -1;  // lane j: the j-th accepted node
@@ -731,7 +773,8 @@ size_t accept_tree_workspace_bytes(int B, int V) {
 hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& bt, const float* x, const float* row_lse,
                               const int32_t* tokens, const int32_t* parent, const float* u, void* ws,
                               int32_t* accept_len, int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len,
-                              hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop, const CombineJob* combine) {
+                              hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop, const CombineJob* combine,
+                              const float2* partials, int ntiles, bool fused) {
   if (bt.nreq <= 0) return hipSuccess;
   AcceptArgs a;
   a.gamma = N;
@@ -752,18 +795,25 @@ hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& bt, const 
   a.segsum = static_cast<double*>(ws);
   TreeFinal* fin = reinterpret_cast<TreeFinal*>(static_cast<char*>(ws) + seg_bytes);
   a.tree = fin;
-  hipExtLaunchKernelGGL(tree_walk_kernel, dim3(bt.nreq), dim3(kWave), 0, stream, ev_start, nullptr, 0, a, bt, tokens,
-                        parent, fin, accept_len, out_tok, out_node, new_kv_len);
+  hipExtLaunchKernelGGL(tree_walk_kernel, dim3(bt.nreq), dim3(kSumWaves * kWave), 0, stream, ev_start, nullptr, 0, a,
+                        bt, tokens, parent, fin, accept_len, out_tok, out_node, new_kv_len, partials, ntiles);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int S = (a.nseg + a.segs_per_group - 1) / a.segs_per_group;
+  CombineJob cj;
+  memset(&cj, 0, sizeof(cj));
+  if (combine != nullptr) cj = *combine;
+  if (fused) {
+    const int extra = cj.nblocks > 0 ? ((cj.nblocks + 1) / 2 + S - 1) / S : 0;
+    hipExtLaunchKernelGGL(accept_fused_kernel, dim3(S, bt.nreq + extra), dim3(kSumWaves * kWave), 0, stream, nullptr,
+                          ev_stop, 0, a, bt, (const float2*)nullptr, 0, accept_len, out_tok, new_kv_len,
+                          accept_arrivals(ws, B, V), cj);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(accept_sums_kernel, dim3(S, bt.nreq), dim3(kSumWaves * kWave), 0, stream, a, bt,
                      (const float2*)nullptr, 0, accept_len);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  CombineJob cj;
-  memset(&cj, 0, sizeof(cj));
-  if (combine != nullptr) cj = *combine;
   hipExtLaunchKernelGGL(accept_pick_kernel, dim3(bt.nreq + cj.nblocks), dim3(kCombineThreads), 0, stream, nullptr, ev_stop, 0, a,
                         bt, accept_len, out_tok, new_kv_len, cj);
   return hipGetLastError();

@@ -233,7 +233,8 @@ int run_accept_tree(const sd_dims_t* d, const float* x, const float* row_lse, co
                     const int32_t* parent, const float* u, const int32_t* kv_len, int32_t* accept_len,
                     int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len, void* ws, hipStream_t stream,
                     hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr,
-                    const std::vector<CombineJob>* merges = nullptr) {
+                    const std::vector<CombineJob>* merges = nullptr, const float2* partials = nullptr, int ntiles = 0,
+                    bool fused = false) {
   for (int r0 = 0; r0 < d->batch; r0 += kMaxReqPerLaunch) {
     AcceptBatch bt;
     memset(&bt, 0, sizeof(bt));
@@ -246,7 +247,7 @@ int run_accept_tree(const sd_dims_t* d, const float* x, const float* row_lse, co
     const CombineJob* cj = merges != nullptr ? &(*merges)[r0 / kMaxReqPerLaunch] : nullptr;
     hipError_t e = launch_accept_tree(d->gamma, d->vocab, d->batch, bt, x, row_lse, tokens, parent, u, ws, accept_len,
                                       out_tok, out_node, new_kv_len, stream, first ? ev_start : nullptr,
-                                      last ? ev_stop : nullptr, cj);
+                                      last ? ev_stop : nullptr, cj, partials, ntiles, fused);
     if (e != hipSuccess) return SD_ERR_HIP;
   }
   return SD_OK;
@@ -638,11 +639,18 @@ int sd_verify_step_tree(const sd_dims_t* dims, const void* q, const void* k_pool
                      defer ? &merges : nullptr);
   if (st != SD_OK) return st;
   void* vws = static_cast<char*>(workspace) + base;
-  st = run_logits(dims, hidden != nullptr ? hidden : attn_out, w_vocab, logits, row_lse, vws, stm, ev[2], ev[3]);
-  if (st != SD_OK) return st;
+  // The projection launch clears the acceptance's arrival counters; the walk
+  // launch folds the row log-sum-exps from the projection's statistics, and
+  // the final draw runs as one launch.
+  const VocabPlan vp = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab,
+                                  (dims->flags & SD_FLAG_PACKED_VOCAB) != 0);
+  void* acc_ws = static_cast<char*>(vws) + logits_ws(dims);
+  if (launch_vocab(dims->dtype, vp, hidden != nullptr ? hidden : attn_out, w_vocab, logits, vws, stm, ev[2], ev[3],
+                   accept_arrivals(acc_ws, dims->batch, dims->vocab), dims->batch) != hipSuccess)
+    return SD_ERR_HIP;
   return run_accept_tree(dims, logits, row_lse, tokens, parent, u, kv_len, accept_len, out_tok, out_node,
-                         new_kv_len, static_cast<char*>(vws) + logits_ws(dims), stm, ev[4], ev[5],
-                         defer ? &merges : nullptr);
+                         new_kv_len, acc_ws, stm, ev[4], ev[5], defer ? &merges : nullptr,
+                         static_cast<const float2*>(vws), vp.ntiles, true);
 }
 
 int sd_tree_commit_kv(const sd_dims_t* dims, void* k_pool, void* v_pool, const int64_t* kv_off,

@@ -149,13 +149,15 @@ hipError_t launch_accept(int gamma, int V, int B, const AcceptBatch& batch, cons
 // Tree verification (N = gamma nodes, position 0 the root, position i + 1 node
 // i): walk the candidate tree, then draw the final token.  ws holds
 // accept_tree_workspace_bytes(B, V).  out_node [B][N + 1]: the accepted nodes,
-// then -1.
+// then -1.  With `partials` (ntiles per row) the walk launch first folds the
+// row log-sum-exps and writes them to row_lse; `fused` as for launch_accept.
 size_t accept_tree_workspace_bytes(int B, int V);
 hipError_t launch_accept_tree(int N, int V, int B, const AcceptBatch& batch, const float* x, const float* row_lse,
                               const int32_t* tokens, const int32_t* parent, const float* u, void* ws,
                               int32_t* accept_len, int32_t* out_tok, int32_t* out_node, int32_t* new_kv_len,
                               hipStream_t stream, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr,
-                              const CombineJob* combine = nullptr);
+                              const CombineJob* combine = nullptr, const float2* partials = nullptr, int ntiles = 0,
+                              bool fused = false);
 
 // Acceptance rate of every draft position: beta[b * gamma + i] = sum_v
 // min(p(v), q_draft[b][i][v]), p from row b * (gamma + 1) + i of x (logits

@@ -9,6 +9,7 @@
   1e-6 band, so it cannot be bit-exact)."""
 
 import numpy as np
+from scipy.special import logsumexp
 import pytest
 import torch
 
@@ -48,6 +49,9 @@ def _check(name, use_hidden):
     logits_ref, lse_ref = verify_logits(h, x.f32("w"))
     assert_close_rows(to_np(db.logits), logits_ref, rtol, f"step logits[{name}]")
     g_logits, g_lse = to_np(db.logits), to_np(db.lse)
+    # The acceptance folds the row log-sum-exps from the projection's tile
+    # statistics; they must be those of the logits themselves.
+    assert np.max(np.abs(g_lse - logsumexp(g_logits.astype(np.float64), axis=1))) < 1e-4
     ref = accept_resample(g_logits, g_lse, x.q_draft, x.draft, x.u, kv_len=x.kv_len)
     near = assert_accept_parity(to_np(db.accept_len), to_np(db.out_tok), to_np(db.new_kv_len), ref)
     indep = accept_resample(logits_ref, lse_ref, x.q_draft, x.draft, x.u, kv_len=x.kv_len)

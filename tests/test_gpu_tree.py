@@ -10,6 +10,7 @@ a chain tree must reproduce sd_verify_attention bit for bit.
 import zlib
 
 import numpy as np
+from scipy.special import logsumexp
 import pytest
 import torch
 
@@ -166,10 +167,13 @@ def test_tree_accept_matches_oracle(name, B, N, V, probs_mode):
     announce(f"tree accept case={name}: near-threshold {near}, mean depth {got[0].mean():.2f}")
 
 
-@pytest.mark.parametrize("projection_input", ["hidden", "attention"])
-def test_tree_step_matches_oracle(projection_input):
+@pytest.mark.parametrize("projection_input,stale", [("hidden", False), ("attention", False), ("hidden", True)])
+def test_tree_step_matches_oracle(projection_input, stale):
     """The projection reads the caller's hidden rows (the attention merge then
-    rides in the acceptance's last launch) or the attention output."""
+    rides in the acceptance's last launch) or the attention output.  The walk
+    launch folds the row log-sum-exps, which must match the logits' own; the
+    final draw's arrival counters live in the workspace, which may start out
+    full of stale bytes (the step's projection launch clears them)."""
     cfg = get_config("llama3_8b").replace(batch=3, gamma=9, n_q_heads=8, n_kv_heads=2, hidden=1024, vocab=4099,
                                           lengths=("explicit", (10, 700, 1500)))
     announce(f"tree step case=gqa_small input={projection_input} B={cfg.batch} nodes={cfg.gamma} V={cfg.vocab}")
@@ -178,6 +182,8 @@ def test_tree_step_matches_oracle(projection_input):
     parent = random_parents(rng, cfg.batch, cfg.gamma)
     tokens = rng.integers(0, cfg.vocab, size=(cfg.batch, cfg.gamma)).astype(np.int32)
     db = DeviceBatch(x)
+    if stale:
+        db.ws.fill_(0xFF)
     node = torch.empty_like(db.out_tok)
     hidden = db.hidden if projection_input == "hidden" else None
     sd.sd_verify_step_tree(db.dims, db.q, db.k, db.v, x.kv_off, x.kv_len, tensor(parent), db.scale, hidden, db.w,
@@ -186,6 +192,8 @@ def test_tree_step_matches_oracle(projection_input):
     torch.cuda.synchronize()
     ref_attn = tree_attention(x.f32("q"), x.f32("k_pool"), x.f32("v_pool"), x.kv_off, x.kv_len, cfg.n_kv_heads, parent)
     assert_close_rows(to_np(db.attn), ref_attn, RTOL[cfg.dtype], "tree step attention")
+    g_logits = to_np(db.logits).astype(np.float64)
+    assert np.max(np.abs(to_np(db.lse) - logsumexp(g_logits, axis=1))) < 1e-4
     ref = accept_tree(to_np(db.logits), to_np(db.lse), tokens, parent, x.u, kv_len=x.kv_len)
     near = _assert_tree_parity([to_np(db.accept_len), to_np(db.out_tok), to_np(node), to_np(db.new_kv_len)], ref)
     announce(f"tree step: near-threshold {near}")
