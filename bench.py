@@ -494,7 +494,7 @@ def main() -> int:
 
     # Attention with its split-KV merge: standalone sd_verify_attention calls
     # (partials kernel, then the merge kernel) back to back.  In the step the
-    # merge rides in the acceptance's pick launch, so the attention kernel's
+    # merge rides in the acceptance launch, so the attention kernel's
     # own time above leaves it out.
     att_calls = [sd.prepare_verify_attention(dims, t["q"], t["k_pool"], t["v_pool"], x.kv_off, x.kv_len, scale,
                                              t["attn"], t["ws"])

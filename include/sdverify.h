@@ -25,7 +25,9 @@
  *     alive until that work completes.  The library allocates no device memory,
  *     keeps no pointer after returning, enqueues work only (never synchronises)
  *     and is re-entrant.  Scratch space comes from the caller's `workspace`;
- *     its size is given by sd_workspace_bytes.
+ *     its size is given by sd_workspace_bytes.  Its contents on entry do not
+ *     matter: what a call needs at zero (the per-request arrival counters of a
+ *     step's one-launch acceptance) it clears itself, on the same stream.
  *   - Device pointers to Q/K/V/hidden/W/workspace must be 16-byte aligned;
  *     float/int32 arrays 4-byte aligned.
  *   - Return value: SD_OK or a negative status (see sd_status_string).  All
@@ -34,7 +36,9 @@
  *   - Device-array preconditions that are not checked (documented only):
  *     draft tokens lie in [0, vocab) (a token outside it is treated as
  *     rejected, never read out of bounds); q rows are distributions.
- *   - Results are deterministic: no floating-point atomics, fixed reduction order.
+ *   - Results are deterministic: no floating-point atomics, fixed reduction order
+ *     (the one integer atomic only counts workgroups in; which one comes last
+ *     does not change any result).
  */
 #ifndef SDVERIFY_H
 #define SDVERIFY_H
@@ -202,7 +206,8 @@ SD_API int sd_accept_resample(const sd_dims_t* dims, const float* logits_or_prob
  *                  enabled): start/stop of the attention kernel (without its
  *                  combine), of the vocabulary projection (for more than 64
  *                  rows: hidden repacking through the projection kernel) and
- *                  of the acceptance (segment sums through the pick kernel).
+ *                  of the acceptance (one launch in a step: the segment sums,
+ *                  then the draw by the last workgroup of each request).
  *                  They are recorded by the kernel
  *                  launches themselves (no extra work on the stream), so the
  *                  elapsed time of each pair is that span's execution time.
@@ -338,8 +343,8 @@ SD_API int sd_accept_tree(const sd_dims_t* dims, const float* logits_or_probs, c
 /*
  * One whole tree verification step: sd_verify_attention_tree, sd_verify_logits
  * (row_lse is an output), then sd_accept_tree.  Arguments as in those calls
- * and sd_verify_step; kernel_events' last pair spans the tree walk through the
- * pick kernel.
+ * and sd_verify_step; kernel_events' last pair spans the tree walk (which
+ * also folds the row log-sum-exps) through the final draw.
  */
 SD_API int sd_verify_step_tree(const sd_dims_t* dims, const void* q, const void* k_pool, const void* v_pool,
                                const int64_t* kv_off, const int32_t* kv_len, const int32_t* parent, float scale,
