@@ -68,3 +68,12 @@ def test_more_than_one_gpu_is_refused(monkeypatch, capsys):
     monkeypatch.setattr(sys, "argv", ["bench.py", "--gpus", "2"])
     assert bench.main() == 2
     assert "one GPU" in capsys.readouterr().err
+
+
+def test_warmup_has_a_time_floor_besides_the_step_count():
+    """--warmup steps always run; --warmup-ms (default 200 ms) keeps the
+    warm-up going until the GPU has been busy that long, so that a short
+    --warmup does not time steps run at idle clocks."""
+    args = bench.parser().parse_args(["--steps", "20", "--warmup", "5"])
+    assert args.warmup == 5 and args.steps == 20 and args.warmup_ms == 200.0
+    assert bench.parser().parse_args(["--warmup-ms", "0"]).warmup_ms == 0.0
