@@ -204,8 +204,9 @@ SD_API int sd_accept_resample(const sd_dims_t* dims, const float* logits_or_prob
  * the three calls; attn_out, logits, row_lse are outputs the caller owns.
  *   kernel_events  (host) NULL, or 6 hipEvent_t handles (created with timing
  *                  enabled): start/stop of the attention kernel (without its
- *                  combine), of the vocabulary projection (for more than 64
- *                  rows: hidden repacking through the projection kernel) and
+ *                  combine), of the vocabulary projection kernel (for more
+ *                  than 64 rows the hidden repacking launch before it is
+ *                  outside the pair) and
  *                  of the acceptance (one launch in a step: the segment sums,
  *                  then the draw by the last workgroup of each request).
  *                  They are recorded by the kernel

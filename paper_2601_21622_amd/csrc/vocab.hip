@@ -739,15 +739,18 @@ hipError_t launch_deep(const VocabPlan& p, const void* hidden, const void* w, fl
                        uint16_t* hpacked, hipStream_t stream, hipEvent_t e0, hipEvent_t e1, int* clear, int nclear) {
   const int64_t pieces = (int64_t)(p.K / 16) * ((p.M + 31) / 32) * 64;
   const int pblocks = (int)std::min<int64_t>((pieces + kVThreads - 1) / kVThreads, 4096);
-  hipExtLaunchKernelGGL(pack_hidden_kernel, dim3(pblocks), dim3(kVThreads), 0, stream, e0, nullptr, 0, p.M, p.K,
+  // The events bracket the projection kernel alone (the repacking is a few
+  // microseconds of latency before it), so that they time the same launch a
+  // kernel trace lists.
+  hipExtLaunchKernelGGL(pack_hidden_kernel, dim3(pblocks), dim3(kVThreads), 0, stream, nullptr, nullptr, 0, p.M, p.K,
                         static_cast<const uint16_t*>(hidden), hpacked, clear, nclear);
   const dim3 grid((p.ntiles + 7) / 8 * 8 * p.mtiles), block(NW * kWave);
   const uint16_t* wv = static_cast<const uint16_t*>(w);
   if (p.packed)
-    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, S, NW, true>), grid, block, 0, stream, nullptr, e1, 0, p.M, p.K,
+    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, S, NW, true>), grid, block, 0, stream, e0, e1, 0, p.M, p.K,
                           p.V, p.ntiles, p.mtiles, hpacked, wv, logits, partials);
   else
-    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, S, NW, false>), grid, block, 0, stream, nullptr, e1, 0, p.M, p.K,
+    hipExtLaunchKernelGGL((vocab_bf16_deep_kernel<MB, NB, S, NW, false>), grid, block, 0, stream, e0, e1, 0, p.M, p.K,
                           p.V, p.ntiles, p.mtiles, hpacked, wv, logits, partials);
   return hipGetLastError();
 }
