@@ -13,6 +13,8 @@ namespace sdv {
 
 // Threads per combine block: one per (row, 4 consecutive d) of a pair.
 constexpr int kCombineThreads = 256;
+// Chunks per pair whose partials a thread loads in one round.
+constexpr int kCombineBatch = 8;
 
 inline int combine_zblocks(const AttnShape& s) {
   return (s.rows * (s.D / 4) + kCombineThreads - 1) / kCombineThreads;
@@ -42,17 +44,41 @@ __device__ __forceinline__ void combine_block(const AttnShape& s, const AttnBatc
   if (i >= s.rows * D4) return;
   const int row = i / D4, d = (i - row * D4) * 4;
   float mx = kNegBig;
-#pragma unroll 8
-  for (int c = c0; c < c1; ++c) mx = fmaxf(mx, parts.m[((int64_t)c * s.Hkv + g) * s.rows + row]);
   float den = 0.f;
   f32x4 num = {0.f, 0.f, 0.f, 0.f};
+  if (c1 - c0 <= kCombineBatch) {
+    // Every chunk's (m, l, o) loaded in one round, then the same arithmetic
+    // in the same order as below.
+    float mv[kCombineBatch], lv[kCombineBatch];
+    f32x4 ov[kCombineBatch];
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k) {
+      const int64_t slot = (int64_t)min(c0 + k, c1 - 1) * s.Hkv + g;
+      mv[k] = parts.m[slot * s.rows + row];
+      lv[k] = parts.l[slot * s.rows + row];
+      ov[k] = *reinterpret_cast<const f32x4*>(parts.o + (slot * s.rows + row) * s.D + d);
+    }
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k)
+      if (c0 + k < c1) mx = fmaxf(mx, mv[k]);
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k)
+      if (c0 + k < c1) {
+        const float a = exp2f(mv[k] - mx);
+        den = fmaf(a, lv[k], den);
+        num += a * ov[k];
+      }
+  } else {
+#pragma unroll 8
+    for (int c = c0; c < c1; ++c) mx = fmaxf(mx, parts.m[((int64_t)c * s.Hkv + g) * s.rows + row]);
 #pragma unroll 4
-  for (int c = c0; c < c1; ++c) {
-    const int64_t slot = (int64_t)c * s.Hkv + g;
-    const float a = exp2f(parts.m[slot * s.rows + row] - mx);
-    den = fmaf(a, parts.l[slot * s.rows + row], den);
-    const f32x4 o = *reinterpret_cast<const f32x4*>(parts.o + (slot * s.rows + row) * s.D + d);
-    num += a * o;
+    for (int c = c0; c < c1; ++c) {
+      const int64_t slot = (int64_t)c * s.Hkv + g;
+      const float a = exp2f(parts.m[slot * s.rows + row] - mx);
+      den = fmaf(a, parts.l[slot * s.rows + row], den);
+      const f32x4 o = *reinterpret_cast<const f32x4*>(parts.o + (slot * s.rows + row) * s.D + d);
+      num += a * o;
+    }
   }
   const int j = row / s.group;
   const int h = g * s.group + (row - j * s.group);
