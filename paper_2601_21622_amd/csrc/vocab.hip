@@ -615,6 +615,295 @@ void vocab_bf16_deep_kernel(int M, int K, int V, int ntiles, int mtiles, const u
   tile_epilogue32<MB, NB, NW>(acc, M, V, ntiles, tile, m0, blk0, logits, partials, red);
 }
 
+// Wide deep schedule: four waves (one per SIMD), four blocks of 32 vocabulary
+// entries per wave (a 512-wide tile) and up to seven 32-row blocks, so a CU
+// pulls its M-tile of hidden rows once per 512 vocabulary entries instead of
+// once per 256.  A wave then holds up to 28 accumulators (448 registers): the
+// compiler keeps MFMA accumulators in the 256 accumulation registers only, so
+// the first 16 accumulators are left to it and the MFMAs of the others are
+// written out with their accumulators in VGPRs.  With the VGPRs taken by
+// accumulators, no load lands in registers: W and the hidden fragments both go
+// to LDS by buffer DMA (a 32-bit lane offset per operation, the chunk in a
+// scalar), three 48 KB stages, chunks issued two ahead; each wave DMAs and
+// reads its own W fragments and a quarter of the shared hidden ones.  The
+// loop runs a multiple of three chunks; chunks past the end are read through
+// an empty buffer range, which returns zeros, so they add nothing.
+constexpr int kWideNB = 4;     // 32-entry vocabulary blocks per wave
+constexpr int kWideAgpr = 16;  // accumulators kept in the accumulation registers
+constexpr int kWideMaxMB = 7;  // 16 + 12 accumulators of 16 registers
+
+__device__ __forceinline__ void mfma32x32x16_vgpr(f32x16& c, bf16x8 a, bf16x8 b) {
+  asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+}
+// The MFMAs above are opaque to the compiler's hazard tracking: separate the
+// zeroing of their accumulators before the loop, and the reads of the
+// epilogue, from them by more wait states than an XDL op of 8 passes needs.
+__device__ __forceinline__ void mfma_asm_fence() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+// Copy of an accumulator held in accumulation registers, read where it is
+// used: left to itself the compiler copies every such accumulator to VGPRs
+// at the end of the loop, which does not fit next to the VGPR accumulators.
+__device__ __forceinline__ f32x16 agpr_take(const f32x16& a) {
+  f32x16 v;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    float t;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(t) : "a"(a[r]));
+    v[r] = t;
+  }
+  return v;
+}
+
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+constexpr int kRawBufferWord3 = 0x00020000;  // gfx9 raw buffer: 32-bit data format, no swizzle
+__device__ __forceinline__ BufRsrc raw_buffer(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRawBufferWord3);
+}
+// Buffer DMA: lane l copies 16 bytes at byte offset voff + soff of the buffer
+// into LDS at lds + 16*l; offsets past the buffer's size read zeros.  NT sets
+// the nontemporal hint (read-once data, as for the register loads of W).
+template <bool NT>
+__device__ __forceinline__ void dma_16B_buffer_to_lds(BufRsrc r, uint32_t voff, uint32_t soff, void* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, (int)voff, (int)soff,
+                                           0, NT ? 2 : 0);
+}
+
+// Epilogue of the wide schedule, one 32-row block at a time (the blocks with
+// VGPR accumulators first, which frees their registers): store the block's
+// logits, form the wave's maximum and sum of exponentials per row, then
+// combine the four waves' (maximum, sum) pairs of a row in wave order, each
+// sum rescaled to the tile maximum.
+template <int MB, int NB, int NW>
+__device__ __forceinline__ void tile_epilogue_wide(const f32x16 (&acc)[MB][NB], int M, int V, int ntiles, int tile,
+                                                   int m0, int blk0, float* __restrict__ logits,
+                                                   float2* __restrict__ partials, float2 (*red)[MB * 32]) {
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int j = lane & 31;
+  const int h = lane >> 5;
+  const bool full = (V % 4) == 0 && (blk0 + NB) * 32 <= V;  // wave-uniform
+#pragma unroll
+  for (int mb = MB - 1; mb >= 0; --mb) {
+    f32x16 av[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) av[nb] = (mb * NB + nb < kWideAgpr) ? agpr_take(acc[mb][nb]) : acc[mb][nb];
+    const int m = m0 + mb * 32 + j;
+    float x = -INFINITY;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int v0 = (blk0 + nb) * 32 + 8 * g + 4 * h;
+        const f32x4 q = {av[nb][4 * g], av[nb][4 * g + 1], av[nb][4 * g + 2], av[nb][4 * g + 3]};
+        float* dst = logits + (int64_t)m * V + v0;
+        if (full) {
+          if (m < M) *reinterpret_cast<f32x4*>(dst) = q;
+          x = fmaxf(x, fmaxf(fmaxf(q[0], q[1]), fmaxf(q[2], q[3])));
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (m < M && v0 + i < V) dst[i] = q[i];
+            x = (v0 + i < V) ? fmaxf(x, q[i]) : x;
+          }
+        }
+      }
+    }
+    x = fmaxf(x, __shfl_xor(x, 32));
+    float sm = 0.f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = (blk0 + nb) * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        sm += (full || v < V) ? expf(av[nb][r] - x) : 0.f;
+      }
+    sm += __shfl_xor(sm, 32);
+    if (h == 0) red[wave][mb * 32 + j] = make_float2(x, sm);
+  }
+  __syncthreads();
+  if (wave == 0 && h == 0) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int r = mb * 32 + j;
+      const int m = m0 + r;
+      if (m < M) {
+        float mx = red[0][r].x;
+#pragma unroll
+        for (int w = 1; w < NW; ++w) mx = fmaxf(mx, red[w][r].x);
+        float sm = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+          const float2 e = red[w][r];
+          sm += e.y > 0.f ? e.y * expf(e.x - mx) : 0.f;  // a wave wholly past V holds (-inf, 0)
+        }
+        partials[(int64_t)m * ntiles + tile] = make_float2(mx, sm);
+      }
+    }
+  }
+}
+
+template <int MB, bool PACKED>
+__global__ __launch_bounds__(4 * kWave, 1)
+void vocab_bf16_wide_kernel(int M, int K, int V, int ntiles, int mtiles, const uint16_t* __restrict__ hpacked,
+                            const uint16_t* __restrict__ w, float* __restrict__ logits,
+                            float2* __restrict__ partials) {
+  constexpr int NB = kWideNB, NW = 4, S = 3;
+  constexpr int kFrags = 2 * MB;               // hidden fragments per chunk
+  constexpr int kHd = (kFrags + NW - 1) / NW;  // hidden DMAs per wave and chunk
+  constexpr int kWd = 2 * NB;                  // W DMAs per wave and chunk
+  constexpr int kOps = kHd + kWd;              // memory operations per wave and chunk
+  constexpr int kHBytes = NW * kHd * 1024;
+  constexpr int kStage = kHBytes + NW * kWd * 1024;
+  static_assert(MB >= 2 && MB <= kWideMaxMB, "accumulators: 16 + 12 of 16 registers");
+  static_assert(kOps <= 2 * MB * NB, "memory operations ride between MFMAs");
+  __shared__ __align__(1024) unsigned char lds0[kStage], lds1[kStage], lds2[kStage];
+  __shared__ float2 red[NW][MB * 32];
+
+  // Workgroup id -> (tile, M-tile) as in the deep kernel: the M-tiles of one
+  // vocabulary tile share an XCD.
+  const int grp = 8 * mtiles;
+  const int tile = (blockIdx.x / grp) * 8 + (blockIdx.x & 7);
+  if (tile >= ntiles) return;
+  const int m0 = ((blockIdx.x % grp) >> 3) * MB * 32;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int blk0 = (tile * NW + wave) * NB;  // first 32-entry vocabulary block of the wave
+  const int nchunks = K / 32;
+
+  // W fragment (nb, ks) of chunk c: byte woff[nb][ks] + c*wstep of W.
+  // Packed layout: 32-entry block b is 16-row blocks 2b (lanes with bit 4
+  // clear) and 2b+1, 512 B each per 16-wide k-step; blocks past the packed
+  // rows read the last one, and a block whose upper half is past them reads
+  // its lower half twice (rows past V are never stored).  Row-major: lane l
+  // reads row 32b + l%32 (clamped to V-1), k 8*(l/32) .. +8 of the step.
+  // The plan takes this schedule only for W under 4 GB.
+  const int nblk = (V + 15) / 16;
+  uint32_t woff[NB][2];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int b = blk0 + nb;
+    uint32_t o;
+    if (PACKED) {
+      const int lo16 = min(2 * b, nblk - 1);
+      const bool upper = 2 * b + 1 < nblk;
+      o = (uint32_t)lo16 * 1024u + 2u * ((upper ? ((lane >> 4) & 1) * 512 : 0) + (lane & 15) * 8 + (lane >> 5) * 128);
+    } else {
+      const int r0 = min(b * 32, V - 1);
+      o = 2u * ((uint32_t)(r0 + min(lane & 31, V - 1 - r0)) * (uint32_t)K + (lane >> 5) * 8);
+    }
+    woff[nb][0] = o;
+    woff[nb][1] = o + (PACKED ? 512u : 32u);
+  }
+  const uint32_t wstep = PACKED ? (uint32_t)nblk * 1024u : 64u;  // bytes per 32-wide chunk
+  const uint32_t wbytes = PACKED ? (uint32_t)nchunks * wstep : (uint32_t)V * (uint32_t)K * 2u;
+
+  // Hidden DMA i of this wave moves fragment f = wave + 4i of a chunk into
+  // LDS fragment f, as the deep kernel's do: numbers past 2*MB are dummies
+  // (every lane reads the last fragment's first 16 bytes), blocks past the
+  // packed rows re-read the last one, and lanes of rows past M in the last
+  // block read the last row's bytes.
+  const int mbt = (M + 31) / 32;
+  const uint32_t hstep = 2u * mbt * 1024u;  // bytes per 32-wide chunk
+  uint32_t hoff[kHd];
+#pragma unroll
+  for (int i = 0; i < kHd; ++i) {
+    const int f = wave + NW * i;
+    const int fs = min(f, kFrags - 1);
+    const int mbg = min(mbt - 1, m0 / 32 + (fs >> 1));
+    const int rlast = M - 1 - mbg * 32;
+    hoff[i] = (uint32_t)((fs & 1) * mbt + mbg) * 1024u +
+              (f < kFrags ? 16u * ((lane & 32) + min(lane & 31, rlast)) : 0u);
+  }
+  const BufRsrc wbuf = raw_buffer(w, wbytes);
+  const BufRsrc hbuf = raw_buffer(hpacked, (uint32_t)nchunks * hstep);
+  const BufRsrc nobuf = raw_buffer(w, 0u);  // every read past its end: zeros
+
+  // Operation j of chunk c into LDS stage dst.
+  auto issue_op = [&](int j, unsigned char* dst, int c) {
+    const bool live = c < nchunks;  // uniform
+    if (j < kHd) {
+      dma_16B_buffer_to_lds<false>(live ? hbuf : nobuf, hoff[j], live ? (uint32_t)c * hstep : 0u,
+                                   dst + (wave + NW * j) * 1024);
+    } else {
+      const int nb = (j - kHd) >> 1, ks = (j - kHd) & 1;
+      dma_16B_buffer_to_lds<true>(live ? wbuf : nobuf, woff[nb][ks], live ? (uint32_t)c * wstep : 0u,
+                                  dst + kHBytes + (wave * kWd + 2 * nb + ks) * 1024);
+    }
+  };
+  auto read_h = [&](const unsigned char* src, int q) -> bf16x8 {  // q = ks*MB + mb
+    const int f = 2 * (q % MB) + q / MB;
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(src + f * 1024 + lane * 16));
+  };
+  auto read_w = [&](const unsigned char* src, int nb, int ks) -> bf16x8 {
+    return __builtin_bit_cast(
+        bf16x8, *reinterpret_cast<const u32x4*>(src + kHBytes + (wave * kWd + 2 * nb + ks) * 1024 + lane * 16));
+  };
+
+  f32x16 acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
+  mfma_asm_fence();
+
+#pragma unroll
+  for (int c = 0; c < S - 1; ++c)
+#pragma unroll
+    for (int j = 0; j < kOps; ++j) issue_op(j, c == 0 ? lds0 : lds1, c);
+  // A wave's W fragments are its own (only its own DMA writes them), so it
+  // reads those of the first k-step of the next chunk as soon as its own
+  // loads have landed, before the barrier the hidden fragments need.
+  bf16x8 wf[2][NB];
+  wait_vmcnt<kOps>();  // chunk 0 has landed
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) wf[0][nb] = read_w(lds0, nb, 0);
+  lds_barrier();
+  for (int c0 = 0; c0 < nchunks; c0 += S) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      const int c = c0 + s;
+      const unsigned char* cur = s == 0 ? lds0 : (s == 1 ? lds1 : lds2);
+      unsigned char* nxt = s == 0 ? lds2 : (s == 1 ? lds0 : lds1);  // chunk c+2 goes where chunk c-1 was
+      bf16x8 hf[2];
+      hf[0] = read_h(cur, 0);
+      // One MFMA, then at most a DMA and a fragment read: the hidden
+      // fragment of the next (ks, mb) is read four MFMAs before its first
+      // use, the W fragments of the second k-step during the first.
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int q = ks * MB + mb;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const int i = q * NB + nb;
+            if (mb * NB + nb < kWideAgpr)
+              acc[mb][nb] = mfma32x32x16(wf[ks][nb], hf[q & 1], acc[mb][nb]);
+            else
+              mfma32x32x16_vgpr(acc[mb][nb], wf[ks][nb], hf[q & 1]);
+            if (i < kOps) issue_op(i, nxt, c + S - 1);
+            if (nb == 0 && q + 1 < kFrags) hf[(q + 1) & 1] = read_h(cur, q + 1);
+            if (ks == 0 && mb == MB - 2) wf[1][nb] = read_w(cur, nb, 1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+      wait_vmcnt<kOps>();  // chunk c+1 has landed; chunk c+2 stays in flight
+      const unsigned char* after = s == 0 ? lds1 : (s == 1 ? lds2 : lds0);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) wf[0][nb] = read_w(after, nb, 0);
+      lds_barrier();
+    }
+  }
+  wait_vmcnt<0>();
+  mfma_asm_fence();
+  tile_epilogue_wide<MB, NB, NW>(acc, M, V, ntiles, tile, m0, blk0, logits, partials, red);
+}
+
 // Hidden rows [M][K] -> fragments [K/16][ceil(M/32)][64 lanes][8]: lane l of
 // fragment (k16, mb) holds row mb*32 + l%32, k 16*k16 + 8*(l/32) .. +8; rows
 // past M are zero.  One thread per 16-byte piece, writes coalesced.
@@ -755,6 +1044,24 @@ hipError_t launch_deep(const VocabPlan& p, const void* hidden, const void* w, fl
   return hipGetLastError();
 }
 
+template <int MB>
+hipError_t launch_wide(const VocabPlan& p, const void* hidden, const void* w, float* logits, float2* partials,
+                       uint16_t* hpacked, hipStream_t stream, hipEvent_t e0, hipEvent_t e1, int* clear, int nclear) {
+  const int64_t pieces = (int64_t)(p.K / 16) * ((p.M + 31) / 32) * 64;
+  const int pblocks = (int)std::min<int64_t>((pieces + kVThreads - 1) / kVThreads, 4096);
+  hipExtLaunchKernelGGL(pack_hidden_kernel, dim3(pblocks), dim3(kVThreads), 0, stream, nullptr, nullptr, 0, p.M, p.K,
+                        static_cast<const uint16_t*>(hidden), hpacked, clear, nclear);
+  const dim3 grid((p.ntiles + 7) / 8 * 8 * p.mtiles), block(4 * kWave);
+  const uint16_t* wv = static_cast<const uint16_t*>(w);
+  if (p.packed)
+    hipExtLaunchKernelGGL((vocab_bf16_wide_kernel<MB, true>), grid, block, 0, stream, e0, e1, 0, p.M, p.K, p.V,
+                          p.ntiles, p.mtiles, hpacked, wv, logits, partials);
+  else
+    hipExtLaunchKernelGGL((vocab_bf16_wide_kernel<MB, false>), grid, block, 0, stream, e0, e1, 0, p.M, p.K, p.V,
+                          p.ntiles, p.mtiles, hpacked, wv, logits, partials);
+  return hipGetLastError();
+}
+
 // Deep schedules: NB blocks of 32 vocabulary entries per wave, NW waves per
 // workgroup (one or two per SIMD), and the most 32-row blocks per M-tile
 // that keep a wave's accumulators (MB x NB x 16) in its share of the
@@ -763,7 +1070,7 @@ hipError_t launch_deep(const VocabPlan& p, const void* hidden, const void* w, fl
 struct DeepShape {
   int nb, nw, cap;
 };
-constexpr DeepShape kDeepShapes[3] = {{1, 4, 12}, {2, 4, 7}, {2, 8, 5}};
+constexpr DeepShape kDeepShapes[4] = {{1, 4, 12}, {2, 4, 7}, {2, 8, 5}, {kWideNB, 4, kWideMaxMB}};
 constexpr int kShallowMaxBlocks = 4;  // 16-row blocks of the shallow schedule
 
 // Per-CU cost of a deep plan in the inflow model of the deep kernel: the
@@ -824,7 +1131,11 @@ VocabPlan vocab_plan(int dtype, int M, int K, int V, bool packed) {
     const int blocks32 = (M + 31) / 32;
     p.deep = true;
     double best = 0.0;
-    for (int i = 0; i < 3; ++i) {
+    // The wide schedule addresses W and the hidden rows with 32-bit offsets.
+    const bool small = (uint64_t)K * (((uint64_t)V + 31) / 32 * 32) * 2 < (1ull << 32) &&
+                       (uint64_t)K * (uint64_t)blocks32 * 64 < (1ull << 32);
+    for (int i = 0; i < 4; ++i) {
+      if (kDeepShapes[i].nb == kWideNB && !small) continue;
       int mt, mb;
       const double cost = deep_cost(blocks32, V, kDeepShapes[i], &mt, &mb);
       if (i == 0 || cost < best) {
@@ -873,6 +1184,17 @@ hipError_t launch_vocab(int dtype, const VocabPlan& p, const void* hidden, const
   }
 #define SDV_D(B, N, W) \
   case B: return launch_deep<B, N, W>(p, hidden, w, logits, partials, hpacked, stream, e0, e1, clear, nclear);
+  if (p.nbw == 2 * kWideNB) {
+    switch (p.mblocks) {
+      case 2: return launch_wide<2>(p, hidden, w, logits, partials, hpacked, stream, e0, e1, clear, nclear);
+      case 3: return launch_wide<3>(p, hidden, w, logits, partials, hpacked, stream, e0, e1, clear, nclear);
+      case 4: return launch_wide<4>(p, hidden, w, logits, partials, hpacked, stream, e0, e1, clear, nclear);
+      case 5: return launch_wide<5>(p, hidden, w, logits, partials, hpacked, stream, e0, e1, clear, nclear);
+      case 6: return launch_wide<6>(p, hidden, w, logits, partials, hpacked, stream, e0, e1, clear, nclear);
+      case 7: return launch_wide<7>(p, hidden, w, logits, partials, hpacked, stream, e0, e1, clear, nclear);
+      default: return hipErrorInvalidValue;
+    }
+  }
   if (p.waves == 8) {
     switch (p.mblocks) {
       SDV_D(2, 2, 8) SDV_D(3, 2, 8) SDV_D(4, 2, 8) SDV_D(5, 2, 8)

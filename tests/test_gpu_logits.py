@@ -38,7 +38,19 @@ CASES = {
     # Two blocks per wave, four waves (256-wide tiles): one M-tile of 7 row
     # blocks, then two M-tiles; K of 3 and 5 chunks (the 6-stage ring runs
     # past the last chunk), V odd.
+    "m224_k96_v32992": _v.replace(batch=32, gamma=6, n_q_heads=2, n_kv_heads=2, hidden=96, vocab=32992,
+                                  lengths=("fixed", 8)),
+    "m336_k160_v32001": _v.replace(batch=48, gamma=6, n_q_heads=2, n_kv_heads=2, hidden=160, vocab=32001,
+                                   lengths=("fixed", 8)),
+    # Four blocks per wave, four waves (512-wide tiles, accumulators in both
+    # register files, 3-stage ring run in steps of three chunks, the ones
+    # past K read as zeros): 7 row blocks with K of 3, 4 and 5 chunks; 200
+    # rows (a partial last block) with a ragged last tile; two M-tiles.
     "m224_k96_v100001": _v.replace(batch=32, gamma=6, n_q_heads=2, n_kv_heads=2, hidden=96, vocab=100001,
+                                   lengths=("fixed", 8)),
+    "m224_k128_v100001": _v.replace(batch=32, gamma=6, n_q_heads=2, n_kv_heads=2, hidden=128, vocab=100001,
+                                    lengths=("fixed", 8)),
+    "m200_k160_v70003": _v.replace(batch=25, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=160, vocab=70003,
                                    lengths=("fixed", 8)),
     "m416_k160_v100001": _v.replace(batch=52, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=160, vocab=100001,
                                     lengths=("fixed", 8)),
@@ -68,7 +80,8 @@ def test_logits_match_oracle(name):
 
 
 @pytest.mark.parametrize("name", ["m18_k512_v1000", "m18_k512_v1003", "m100_k256_v777", "m336_k256_v130",
-                                  "m272_k96_v65537", "m416_k160_v100001", "m100_k160_v100003"])
+                                  "m272_k96_v65537", "m224_k96_v32992", "m416_k160_v100001", "m200_k160_v70003",
+                                  "m100_k160_v100003"])
 def test_packed_vocab_matches_row_major_bitwise(name):
     """The packed layout changes where W is read from, not the arithmetic:
     logits and log-sum-exp must be bit-identical to the row-major path."""
