@@ -545,10 +545,10 @@ def main() -> int:
     attn_merged_gbps = attn_bytes / (ms_attn_merged * 1e-3) / 1e9 if ms_attn_merged else None
     vocab_gbps = vocab_bytes / (st_mean[1] * 1e-3) / 1e9
     vocab_tflops = vocab_flops / (st_mean[1] * 1e-3) / 1e12
-    # Kernel names as rocprofv3 lists them: the vocabulary projection runs the
-    # deep schedule above 64 rows, attention the register-staged kernel for a
+    # Kernel names as rocprofv3 lists them: the library names the projection
+    # kernel its plan picks; attention runs the register-staged kernel for a
     # single 16-row block per KV head.
-    vocab_kernel = "vocab_bf16_deep_kernel" if M > 64 else "vocab_bf16_kernel"
+    vocab_kernel = sd.sd_vocab_kernel_name(dims)
     rows = G * (cfg.n_q_heads // cfg.n_kv_heads)
     attn_kernel = "attn_bf16_reg_kernel" if rows <= 16 else "attn_bf16_kernel"
     roof_attn = {"bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",

@@ -492,6 +492,16 @@ typedef struct {
 SD_API int sd_expand_layer(const sd_expand_t* e, const float* draft_logits, int32_t* tokens, int32_t* parent,
                            float* q_child, sd_stream_t stream);
 
+/*
+ * Name of the vocabulary-projection kernel that sd_verify_logits and the
+ * verification steps launch for `dims`, as a kernel trace lists it without
+ * template arguments ("vocab_bf16_kernel", "vocab_bf16_deep_kernel",
+ * "vocab_bf16_wide_kernel" or "vocab_f32_kernel"): for tools that match
+ * measurements to kernels.  Host only; a static string, or NULL for an
+ * invalid shape.
+ */
+SD_API const char* sd_vocab_kernel_name(const sd_dims_t* dims);
+
 /* Static description of a status code. */
 SD_API const char* sd_status_string(int status);
 

@@ -52,6 +52,7 @@ from ._binding import (  # noqa: F401
     sd_verify_step_sampled,
     sd_verify_step_tree,
     sd_version,
+    sd_vocab_kernel_name,
     sd_vocab_packed_bytes,
     sd_workspace_bytes,
 )

@@ -161,6 +161,8 @@ def library() -> ctypes.CDLL:
     lib.sd_vocab_packed_bytes.restype = SZ
     lib.sd_pack_vocab.argtypes = [DP, P, P, P]
     lib.sd_pack_vocab.restype = ctypes.c_int
+    lib.sd_vocab_kernel_name.argtypes = [DP]
+    lib.sd_vocab_kernel_name.restype = ctypes.c_char_p
     lib.sd_status_string.argtypes = [ctypes.c_int]
     lib.sd_status_string.restype = ctypes.c_char_p
     lib.sd_version.argtypes = []
@@ -229,6 +231,11 @@ def _check(status: int, where: str) -> None:
 
 def sd_workspace_bytes(dims: Dims, max_kv_len: int) -> int:
     return int(library().sd_workspace_bytes(ctypes.byref(dims), int(max_kv_len)))
+
+
+def sd_vocab_kernel_name(dims: Dims):
+    name = library().sd_vocab_kernel_name(ctypes.byref(dims))
+    return None if name is None else name.decode()
 
 
 def sd_vocab_packed_bytes(dims: Dims) -> int:

@@ -749,6 +749,17 @@ int sd_verify_step_static(const sd_dims_t* dims, const void* q, const void* k_po
                      nullptr);
 }
 
+const char* sd_vocab_kernel_name(const sd_dims_t* dims) {
+  if (check_dims(dims) != SD_OK) return nullptr;
+  const VocabPlan p = vocab_plan(dims->dtype, dims->batch * (dims->gamma + 1), dims->hidden, dims->vocab,
+                                 (dims->flags & SD_FLAG_PACKED_VOCAB) != 0);
+  if (dims->dtype == SD_DTYPE_F32) return "vocab_f32_kernel";
+  if (!p.deep) return "vocab_bf16_kernel";
+  // The wide schedule is the deep shape with four 32-entry blocks per wave
+  // on four waves (16-entry blocks per wave: 8).
+  return (p.nbw == 8 && p.waves == 4) ? "vocab_bf16_wide_kernel" : "vocab_bf16_deep_kernel";
+}
+
 const char* sd_status_string(int status) {
   switch (status) {
     case SD_OK: return "SD_OK: success";

@@ -31,10 +31,33 @@ def test_library_loads_and_exports_header_symbols():
                           "sd_acceptance_rate", "sd_verify_attention_paged", "sd_verify_step_paged",
                           "sd_kv_pool_create", "sd_kv_pool_destroy", "sd_kv_pool_reserve", "sd_kv_pool_truncate",
                           "sd_kv_pool_release", "sd_kv_pool_free_pages", "sd_kv_pool_tag_pages",
-                          "sd_kv_pool_block_table", "sd_expand_layer", "sd_verify_step_static"}
+                          "sd_kv_pool_block_table", "sd_expand_layer", "sd_verify_step_static",
+                          "sd_vocab_kernel_name"}
     for n in names:
         assert hasattr(lib, n), n
     assert sd.sd_version().count(".") == 2
+
+
+def test_vocab_kernel_name_follows_the_plan():
+    """The projection kernel the plan picks: the shallow schedule up to 64
+    rows, the wide one where one M-tile of up to 224 rows meets a vocabulary
+    large enough for 512-wide tiles to fill the chip, the deep one otherwise."""
+    from workloads import get_config
+
+    def name(cfg, **kw):
+        d = dict(batch=cfg.batch, gamma=cfg.gamma, n_q_heads=cfg.n_q_heads, n_kv_heads=cfg.n_kv_heads,
+                 head_dim=cfg.head_dim, hidden=cfg.hidden, vocab=cfg.vocab, dtype=1 if cfg.dtype == "bf16" else 0)
+        d.update(kw)
+        return sd.sd_vocab_kernel_name(sd.Dims(**d))
+
+    assert name(get_config("tiny")) == "vocab_f32_kernel"
+    assert name(get_config("vicuna7b")) == "vocab_bf16_kernel"
+    assert name(get_config("pooled")) == "vocab_bf16_deep_kernel"
+    assert name(get_config("llama3_8b")) == "vocab_bf16_wide_kernel"
+    assert name(get_config("llama3_8b"), flags=sd.SD_FLAG_PACKED_VOCAB) == "vocab_bf16_wide_kernel"
+    assert name(get_config("llama70b_share")) == "vocab_bf16_deep_kernel"
+    assert name(get_config("llama3_8b"), vocab=30000) == "vocab_bf16_deep_kernel"
+    assert sd.sd_vocab_kernel_name(dims(head_dim=96)) is None
 
 
 def test_status_strings():
