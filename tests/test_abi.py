@@ -57,6 +57,9 @@ def test_vocab_kernel_name_follows_the_plan():
     assert name(get_config("llama3_8b"), flags=sd.SD_FLAG_PACKED_VOCAB) == "vocab_bf16_wide_kernel"
     assert name(get_config("llama70b_share")) == "vocab_bf16_deep_kernel"
     assert name(get_config("llama3_8b"), vocab=30000) == "vocab_bf16_deep_kernel"
+    # W past 4 GB: the wide schedule's 32-bit offsets rule it out.
+    assert name(get_config("llama3_8b"), hidden=16384, vocab=2_000_000) == "vocab_bf16_deep_kernel"
+    assert name(get_config("llama3_8b"), hidden=8192, vocab=250_000) == "vocab_bf16_wide_kernel"
     assert sd.sd_vocab_kernel_name(dims(head_dim=96)) is None
 
 
