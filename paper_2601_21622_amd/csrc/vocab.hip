@@ -5,13 +5,13 @@
 // four consecutive vocabulary entries of one hidden row, which is what the
 // logits store and the row statistics want.
 //
-// A workgroup (4 waves) owns a tile of vocabulary rows for all hidden rows of
-// its M-tile, so W (the dominant stream, K*V*2 bytes) is read from HBM once.
-// Every wave streams its own W fragments straight into registers, either from
-// the [V][K] layout or from the fragment-ordered copy sd_pack_vocab makes at
-// weight-load time (1 KB contiguous per fragment).  The hidden rows, shared by
-// every workgroup and L2-resident, are staged per K-chunk in LDS in
-// fragment order and read by all four waves.  Two schedules:
+// A workgroup owns a tile of vocabulary rows for all hidden rows of its
+// M-tile, so W (the dominant stream, K*V*2 bytes) is read from HBM once.
+// Every wave streams its own W fragments, either from the [V][K] layout or
+// from the fragment-ordered copy sd_pack_vocab makes at weight-load time (1 KB
+// contiguous per fragment).  The hidden rows, shared by every workgroup and
+// L2-resident, are staged per K-chunk in LDS in fragment order and read by
+// all waves.  Three schedules:
 //   * shallow (at most 64 hidden rows), MFMA 16x16x32: one 16-entry
 //     vocabulary block per wave, 256-wide K-chunks, one chunk of prefetch;
 //     several workgroups per CU keep enough W in flight.
@@ -21,10 +21,13 @@
 //     waves (one per SIMD) with 1 or 2 blocks of 32 vocabulary entries each,
 //     W in a 6-slot register ring and hidden in 6 LDS stages; or eight waves
 //     (two per SIMD) with 2 blocks each, a 512-wide tile on a 3-stage ring.
-//     vocab_plan picks the shape whose per-CU inflow (W misses plus hidden
-//     hits) is smallest.  Workgroups that share a vocabulary tile (several
-//     M-tiles) are dealt to the same XCD.
-// W fragments are loaded with the nontemporal hint in both schedules: W is
+//   * wide (deep rows, large vocabularies): four waves with four blocks of
+//     32 vocabulary entries each, a 512-wide tile whose accumulators fill
+//     both register files; W and hidden both go to LDS by buffer DMA.
+//     vocab_plan picks, among the deep shapes and the wide one, the one whose
+//     per-CU inflow (W misses plus hidden hits) is smallest.  Workgroups that
+//     share a vocabulary tile (several M-tiles) are dealt to the same XCD.
+// W fragments are loaded with the nontemporal hint in every schedule: W is
 // read once per launch and should not evict the hidden rows or the logits.
 // The epilogue writes the float32 logits and, per (row, tile), the tile
 // maximum and the sum of exp(logit - maximum); the row log-sum-exp is folded
