@@ -50,6 +50,12 @@ CASES = {
                                    lengths=("fixed", 8)),
     "m224_k128_v100001": _v.replace(batch=32, gamma=6, n_q_heads=2, n_kv_heads=2, hidden=128, vocab=100001,
                                     lengths=("fixed", 8)),
+    # K of one and two chunks: the prologue's second chunk, or the loop's
+    # whole second and third, read as zeros.
+    "m224_k32_v100001": _v.replace(batch=32, gamma=6, n_q_heads=1, n_kv_heads=1, head_dim=64, hidden=32,
+                                   vocab=100001, lengths=("fixed", 8)),
+    "m224_k64_v100001": _v.replace(batch=32, gamma=6, n_q_heads=1, n_kv_heads=1, head_dim=64, hidden=64,
+                                   vocab=100001, lengths=("fixed", 8)),
     "m200_k160_v70003": _v.replace(batch=25, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=160, vocab=70003,
                                    lengths=("fixed", 8)),
     "m416_k160_v100001": _v.replace(batch=52, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=160, vocab=100001,
