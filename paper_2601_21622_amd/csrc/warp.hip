@@ -18,6 +18,10 @@
 //      ceil(top_p * kept mass) (with no top-k cut, the kept mass is the
 //      total of the first level's histogram, which holds every entry);
 //   4. lse = max / T + log(kept mass).
+// In either descent over a long row the second level also gathers the keys
+// inside the first level's bucket into LDS; when they fit, the third level
+// reads those instead of the row (the same entries, so the same integer
+// sums).
 // Masses are exp((logit - max) / T) in float32, scaled by 2^S and truncated to
 // 64-bit integers (S = 62 - ceil(log2 V), so a whole row cannot overflow);
 // integer sums make every histogram and total independent of the order of
@@ -38,6 +42,11 @@ constexpr int kWarpWaves = kWarpThreads / kWave;
 constexpr int kBuckets = 2048;
 static_assert(kBuckets == 2 * kWarpThreads, "the level-0 total reads two buckets per thread");
 constexpr int kCand = 2048;  // candidates the small-k path can hold
+// Keys of the entries inside the first level's bucket that a descent's
+// second level gathers into LDS, so that its third level histograms them
+// instead of passing over the row again (when they fit).
+constexpr int kKeep = 16384;
+constexpr int kKeepMinV = 65536;
 
 __device__ __forceinline__ float key_value(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
@@ -220,8 +229,54 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
   __shared__ uint32_t s_n, s_bound, s_theta, s_pdone;
   __shared__ unsigned long long s_w;
 
+
   const int row = blockIdx.x;
   const float* x = logits + (int64_t)row * V;
+  float m_row = 0.f;  // the row's largest logit, once known
+  __shared__ uint32_t s_keep[kKeep];
+  __shared__ uint32_t s_nkeep;
+
+  // One level of a radix descent: histogram (counts and masses) of the
+  // entries whose key is at least `floor` and whose bits above the level's
+  // digit equal `prefix`.  Level 1 also gathers those entries' keys; level 2
+  // reads the gathered keys when all of them fit.
+  auto histogram = [&](int level, const Level& lv, uint32_t prefix, uint32_t floor) {
+    for (int i = threadIdx.x; i < lv.nb; i += kWarpThreads) {
+      hcnt[i] = 0;
+      hmass[i] = 0;
+    }
+    if (threadIdx.x == 0 && level == 1) s_nkeep = 0;
+    __syncthreads();
+    const float* xr = logits + (int64_t)blockIdx.x * V;
+    auto add = [&](uint32_t k, float xv) {  // xv = key_value(k)
+      const int b = (k >> lv.shift) & (lv.nb - 1);
+      atomicAdd(&hcnt[b], 1u);
+      atomicAdd(&hmass[b], fixed_mass(xv, m_row, inv_t, scale));
+    };
+    // Rows short enough to stay in L2 are read again instead: the gathered
+    // level measured slower at 32,000 entries, faster at 128,256.
+    const bool use_keep = V >= kKeepMinV;
+    const bool gather = use_keep && level == 1;
+    if (use_keep && level == 2 && s_nkeep <= (uint32_t)kKeep) {
+      const int n = (int)s_nkeep;
+      for (int i = threadIdx.x; i < n; i += kWarpThreads) {
+        const uint32_t k = s_keep[i];
+        if (k >= floor && (k & lv.hmask) == prefix) add(k, key_value(k));
+      }
+    } else {
+      row_pass(xr, V, [&](int, float xv) {
+        const uint32_t k = order_key(xv);
+        if (k >= floor && (k & lv.hmask) == prefix) {
+          add(k, xv);
+          if (gather) {
+            const uint32_t i = atomicAdd(&s_nkeep, 1u);
+            if (i < (uint32_t)kKeep) s_keep[i] = k;
+          }
+        }
+      });
+    }
+    __syncthreads();
+  };
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -261,6 +316,7 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
     return;
   }
   const float m = key_value(s_kmax);
+  m_row = m;
 
   // Mass of the whole row (no top-k), or of the top-k set.
   uint32_t theta = 0;
@@ -353,20 +409,7 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
     unsigned long long above = 0;
     for (int level = 0; level < 3; ++level) {
       const Level lv = level_of(level);
-      for (int i = tid; i < lv.nb; i += kWarpThreads) {
-        hcnt[i] = 0;
-        hmass[i] = 0;
-      }
-      __syncthreads();
-      row_pass(x, V, [&](int, float xv) {
-        const uint32_t k = order_key(xv);
-        if ((k & lv.hmask) == prefix) {
-          const int b = (k >> lv.shift) & (lv.nb - 1);
-          atomicAdd(&hcnt[b], 1u);
-          atomicAdd(&hmass[b], fixed_mass(xv, m, inv_t, scale));
-        }
-      });
-      __syncthreads();
+      histogram(level, lv, prefix, 0u);
       if (wave == 0) select_bucket<false>(hcnt, hmass, lv.nb, krem, &s_bucket, &s_cnt_above, &s_mass_above);
       __syncthreads();
       const uint32_t b = s_bucket;
@@ -407,20 +450,7 @@ void warp_kernel(int V, const float* __restrict__ logits, float inv_t, int greed
     unsigned long long above = 0;
     for (int level = 0; level < 3; ++level) {
       const Level lv = level_of(level);
-      for (int i = tid; i < lv.nb; i += kWarpThreads) {
-        hcnt[i] = 0;
-        hmass[i] = 0;
-      }
-      __syncthreads();
-      row_pass(x, V, [&](int, float xv) {
-        const uint32_t k = order_key(xv);
-        if (k >= theta && (k & lv.hmask) == prefix) {
-          const int b = (k >> lv.shift) & (lv.nb - 1);
-          atomicAdd(&hcnt[b], 1u);
-          atomicAdd(&hmass[b], fixed_mass(xv, m, inv_t, scale));
-        }
-      });
-      __syncthreads();
+      histogram(level, lv, prefix, theta);
       if (!w_known) {  // level 0 over every entry: W = the histogram's total
         unsigned long long t = hmass[tid] + hmass[tid + kWarpThreads];
         for (int off = 32; off >= 1; off >>= 1) t += shfl_xor_u64(t, off);
