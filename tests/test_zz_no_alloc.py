@@ -15,6 +15,8 @@ from gpu_util import DeviceBatch, announce
 pytestmark = pytest.mark.gpu
 
 LARGE = get_config("llama3_8b").replace(batch=6, lengths=("explicit", (5000, 900, 8200, 3100, 64, 12000)))
+# 224 projection rows and a large vocabulary: the wide projection schedule.
+WIDE = get_config("llama3_8b").replace(batch=32, hidden=256, vocab=100001, lengths=("fixed", 64))
 SMALL = get_config("vicuna7b").replace(batch=3, n_q_heads=8, n_kv_heads=8, hidden=1024, vocab=5000,
                                        lengths=("explicit", (40, 300, 1200)))
 
@@ -57,3 +59,13 @@ def test_static_scratch_step_matches_workspace_step_twice():
     assert small < big
     announce(f"static-scratch step: {LARGE.name} ({big} keys) then {SMALL.name} ({small} keys) identical to "
              f"the workspace step")
+
+
+def test_static_scratch_step_matches_workspace_step_wide_projection():
+    """The same, with the wide projection schedule on the static scratch,
+    then the small problem again."""
+    assert sd.sd_vocab_kernel_name(sd.Dims.of(WIDE, packed_vocab=True)) == "vocab_bf16_wide_kernel"
+    wide = _check(WIDE, packed=True)
+    small = _check(SMALL, packed=True)
+    assert small < wide
+    announce(f"static-scratch step (wide projection): identical to the workspace step")
