@@ -64,6 +64,15 @@ CASES = {
     # not a multiple of 32, V odd.
     "m100_k160_v100003": _v.replace(batch=20, gamma=4, n_q_heads=2, n_kv_heads=2, hidden=160, vocab=100003,
                                     lengths=("fixed", 8)),
+    # Degenerate vocabularies (one, two, three entries) on the shallow and
+    # the deep schedules and in float32: every tile but the first is empty.
+    "m18_k64_v1": _v.replace(batch=3, n_q_heads=2, n_kv_heads=2, hidden=64, vocab=1, lengths=("fixed", 8)),
+    "m100_k64_v1": _v.replace(batch=20, gamma=4, n_q_heads=2, n_kv_heads=2, hidden=64, vocab=1,
+                              lengths=("fixed", 8)),
+    "m48_k64_v2": _v.replace(batch=8, n_q_heads=2, n_kv_heads=2, hidden=64, vocab=2, lengths=("fixed", 8)),
+    "m416_k64_v3": _v.replace(batch=52, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=64, vocab=3,
+                              lengths=("fixed", 8)),
+    "f32_m10_k64_v1": get_config("tiny").replace(batch=2, gamma=4, hidden=64, vocab=1, lengths=("fixed", 8)),
     "f32_m70_k128_v65": get_config("tiny").replace(batch=14, gamma=4, hidden=128, vocab=65, lengths=("fixed", 8)),
 }
 
@@ -87,7 +96,7 @@ def test_logits_match_oracle(name):
 
 @pytest.mark.parametrize("name", ["m18_k512_v1000", "m18_k512_v1003", "m100_k256_v777", "m336_k256_v130",
                                   "m272_k96_v65537", "m224_k96_v32992", "m416_k160_v100001", "m200_k160_v70003",
-                                  "m100_k160_v100003"])
+                                  "m100_k160_v100003", "m100_k64_v1", "m416_k64_v3"])
 def test_packed_vocab_matches_row_major_bitwise(name):
     """The packed layout changes where W is read from, not the arithmetic:
     logits and log-sum-exp must be bit-identical to the row-major path."""
