@@ -26,6 +26,12 @@ CASES = {
                                                    lengths=("explicit", (6, 600, 1300))),
     "gqa_small": get_config("llama3_8b").replace(batch=2, n_q_heads=8, n_kv_heads=2, hidden=1024, vocab=2500,
                                                  lengths=("explicit", (7, 900))),
+    # Degenerate vocabularies: one token (p = q = 1, every draft accepted)
+    # on the deep projection, two tokens on the shallow one.
+    "vocab1_deep": get_config("vicuna7b").replace(batch=20, gamma=4, n_q_heads=2, n_kv_heads=2, hidden=64, vocab=1,
+                                                  lengths=("fixed", 40)),
+    "vocab2": get_config("vicuna7b").replace(batch=3, n_q_heads=2, n_kv_heads=2, hidden=64, vocab=2,
+                                             lengths=("explicit", (6, 70, 300))),
 }
 
 
