@@ -72,6 +72,9 @@ CASES = {
     "m48_k64_v2": _v.replace(batch=8, n_q_heads=2, n_kv_heads=2, hidden=64, vocab=2, lengths=("fixed", 8)),
     "m416_k64_v3": _v.replace(batch=52, gamma=7, n_q_heads=2, n_kv_heads=2, hidden=64, vocab=3,
                               lengths=("fixed", 8)),
+    # The largest vocabulary the boundary takes (2,097,152 entries).
+    "m18_k32_v2097152": _v.replace(batch=3, n_q_heads=2, n_kv_heads=2, hidden=32, vocab=2097152,
+                                   lengths=("fixed", 8)),
     "f32_m10_k64_v1": get_config("tiny").replace(batch=2, gamma=4, hidden=64, vocab=1, lengths=("fixed", 8)),
     "f32_m70_k128_v65": get_config("tiny").replace(batch=14, gamma=4, hidden=128, vocab=65, lengths=("fixed", 8)),
 }
